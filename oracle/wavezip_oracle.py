@@ -1,0 +1,341 @@
+"""WaveZip token-condensation pass -- plain CPU oracle in float64 NumPy.
+
+TEST INFRASTRUCTURE ONLY.  This module is the slow, obviously-correct statement
+of what the GPU path computes.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import it; the product path never does, and it
+shares no code, constants or helpers with the HIP kernels.
+
+Source: "WaveZip: Wavelet-Driven Space-Time Decoupling for Video Token
+Condensation", Sec. 3 (Method).  Every function names the passage it follows.
+Points where the paper is silent or ambiguous follow these readings:
+
+  * multi-token query: a score against the query is the maximum over query
+    tokens of the cosine (Sec. 3.2.1 defines one global query embedding);
+  * a cosine with a zero-norm vector is 0;
+  * the rank-preserving normalisation of Eq. (7) is a per-frame min-max, and a
+    frame whose scores are all equal gets M = 0; gamma of Sec. 3.2.2 is the
+    same min-max over all T frames (0 when degenerate);
+  * frame 0 is always retained by the frame filter (delta_1 = 0 by Eq. (8));
+    delta is clamped to [0, 2] against rounding;
+  * the down-sampling of the gate in Eq. (10) is pair averaging, applied once
+    per decomposition level; J temporal levels gate every detail level;
+  * odd-length signals are extended by repeating the last sample before every
+    Haar step (half-point symmetric extension), and cropped after synthesis;
+  * the orthonormal Haar filters are used in 1-D and, separably, in 2-D; the
+    2-D transform is the single-level Haar version of Eq. (12)-(15);
+  * Eq. (16)'s Round is realised as a capped largest-remainder (Hamilton)
+    apportionment so that Eq. (5) (budgets sum to B) holds with 0 <= n <= N;
+    remainder ties go to the smaller frame index; if every weight is zero the
+    weights are uniform;
+  * the budget-guided interpolation of Eq. (17) is replaced by keeping the n_m
+    tokens of largest saliency a (ties -> smaller index), emitted in raster
+    order; frames are concatenated in temporal order as in Eq. (19).
+
+Arrays: X is [T, H, W, C] and query is [Q, C], both float64 holding the exact
+values of the (already cast) inputs.  Indices are 0-based.  parity pinned:
+every function below is checked by tests against closed forms, invariants,
+hand-derived cases and a pure-Python brute force.
+"""
+import numpy as np
+
+_INV_SQRT2 = 1.0 / np.sqrt(2.0)
+
+
+# ---------------------------------------------------------------------------
+# Cross-Modal Scorer, similarity branch (Sec. 3.2.1)
+# ---------------------------------------------------------------------------
+
+def cosine_matrix(U, V):
+    """cos(u_i, v_j) for rows of U [n, C] and V [m, C]; 0 where a norm is 0."""
+    dots = U @ V.T
+    nu = np.sqrt(np.sum(U * U, axis=1))
+    nv = np.sqrt(np.sum(V * V, axis=1))
+    den = nu[:, None] * nv[None, :]
+    out = np.zeros_like(dots)
+    nz = den > 0
+    out[nz] = dots[nz] / den[nz]
+    return out
+
+
+def token_saliency(X, query):
+    """Spatial saliency a_{t,n} (Sec. 3.2.1, token-wise cosine with the query).
+
+    Returns a [T, H*W]: max over query tokens of cos(x_{t,n}, q_j).
+    """
+    T, H, W, C = X.shape
+    cos = cosine_matrix(X.reshape(T * H * W, C), query)
+    return cos.max(axis=1).reshape(T, H * W)
+
+
+def pooled_features(X):
+    """Spatially average-pooled frame features v-bar_t (Sec. 3.2.1, Eq. (8))."""
+    return X.mean(axis=(1, 2))
+
+
+def frame_relevance(vbar, query):
+    """Temporal relevance r_t: cosine of the pooled frame with the query (Sec. 3.2.1)."""
+    return cosine_matrix(vbar, query).max(axis=1)
+
+
+# ---------------------------------------------------------------------------
+# Visual Change Estimator (Sec. 3.2.2)
+# ---------------------------------------------------------------------------
+
+def visual_change(vbar):
+    """delta_t of Eq. (8): cosine distance of adjacent pooled features; delta_1 = 0."""
+    T = vbar.shape[0]
+    delta = np.zeros(T)
+    for t in range(1, T):
+        c = cosine_matrix(vbar[t:t + 1], vbar[t - 1:t])[0, 0]
+        delta[t] = min(max(1.0 - c, 0.0), 2.0)
+    return delta
+
+
+def min_max(v):
+    """Min-max normalisation to [0, 1]; all-equal input gives zeros."""
+    lo, hi = np.min(v), np.max(v)
+    if hi > lo:
+        return (v - lo) / (hi - lo)
+    return np.zeros_like(v)
+
+
+def temporal_gate(delta):
+    """gamma_t = min-max normalised delta over the temporal axis (Sec. 3.2.2)."""
+    return min_max(delta)
+
+
+def retained_frames(delta, tau):
+    """Frame Filter of Sec. 3.2.2: keep t with delta_t >= tau, frame 0 always."""
+    return [0] + [t for t in range(1, len(delta)) if delta[t] >= tau]
+
+
+def saliency_map(a_t):
+    """M_t of Eq. (7): per-frame rank-preserving (min-max) normalisation of a."""
+    return min_max(a_t)
+
+
+# ---------------------------------------------------------------------------
+# Haar wavelet (Eq. (9), (11), (12), (15))
+# ---------------------------------------------------------------------------
+
+def _extend_even(x, axis):
+    """Repeat the last sample along `axis` when its length is odd."""
+    if x.shape[axis] % 2 == 0:
+        return x
+    last = np.take(x, [x.shape[axis] - 1], axis=axis)
+    return np.concatenate([x, last], axis=axis)
+
+
+def haar_analysis(x, axis=0):
+    """One orthonormal Haar analysis step along `axis` -> (approximation, detail).
+
+    A_k = (x_{2k} + x_{2k+1}) / sqrt(2),  D_k = (x_{2k} - x_{2k+1}) / sqrt(2),
+    after extending an odd-length axis by its last sample.
+    """
+    xe = _extend_even(np.asarray(x, dtype=np.float64), axis)
+    n = xe.shape[axis]
+    even = np.take(xe, np.arange(0, n, 2), axis=axis)
+    odd = np.take(xe, np.arange(1, n, 2), axis=axis)
+    return (even + odd) * _INV_SQRT2, (even - odd) * _INV_SQRT2
+
+
+def haar_synthesis(A, D, length, axis=0):
+    """Inverse of `haar_analysis`: interleave (A+D)/sqrt(2), (A-D)/sqrt(2), crop to `length`."""
+    even = (A + D) * _INV_SQRT2
+    odd = (A - D) * _INV_SQRT2
+    shape = list(A.shape)
+    shape[axis] = 2 * A.shape[axis]
+    out = np.empty(shape)
+    idx = [slice(None)] * len(shape)
+    idx[axis] = slice(0, None, 2)
+    out[tuple(idx)] = even
+    idx[axis] = slice(1, None, 2)
+    out[tuple(idx)] = odd
+    idx[axis] = slice(0, length)
+    return out[tuple(idx)]
+
+
+def pair_average(g):
+    """Average pooling by pairs (the down-sampling P of Eq. (10)); odd length repeats the last entry."""
+    ge = _extend_even(np.asarray(g, dtype=np.float64), 0)
+    return 0.5 * (ge[0::2] + ge[1::2])
+
+
+# ---------------------------------------------------------------------------
+# Wavelet Temporal Allocator (Eq. (9)-(11))
+# ---------------------------------------------------------------------------
+
+def wavelet_temporal_allocator(R, Gamma, levels):
+    """Rectified relevance R-tilde.
+
+    Level j = 1..J: (A_j, D_j) = DWT(A_{j-1}) with A_0 = R (Eq. (9)); the gate is
+    pooled to the detail resolution, Gamma-bar_j = P(Gamma-bar_{j-1}), and
+    D-tilde_j = Gamma-bar_j * D_j (Eq. (10)); the inverse DWT then rebuilds the
+    sequence level by level (Eq. (11)).  With J = 1 this is the paper's
+    single-level WTA.
+    """
+    A = np.asarray(R, dtype=np.float64)
+    g = np.asarray(Gamma, dtype=np.float64)
+    lengths, details = [], []
+    for _ in range(levels):
+        lengths.append(A.shape[0])
+        A, D = haar_analysis(A)
+        g = pair_average(g)
+        details.append(g * D)
+    for j in reversed(range(levels)):
+        A = haar_synthesis(A, details[j], lengths[j])
+    return A
+
+
+# ---------------------------------------------------------------------------
+# Token Assigner: frame budgets (Eq. (16) with the constraint of Eq. (5))
+# ---------------------------------------------------------------------------
+
+def allocate_budget(r_tilde, B, N):
+    """Integer budgets n_m >= 0 for the retained frames, sum = min(B, L*N), each <= N.
+
+    Quota q_m = R * w_m / sum(w) with w = max(r-tilde, 0) (Eq. (16)).  A frame whose
+    quota reaches N is fixed at N and the rest of the budget is re-apportioned
+    among the others; otherwise every frame gets floor(q_m) and the leftover
+    tokens go to the largest fractional parts, smaller index first on ties.
+    """
+    return allocate_budget_trace(r_tilde, B, N)[0]
+
+
+def allocate_budget_trace(r_tilde, B, N):
+    """`allocate_budget` plus a record of its last apportionment round.
+
+    The record holds the quotas `q` of the frames `active` in that round, the
+    number `left` of leftover tokens handed out by fractional part, whether the
+    all-zero-weight rule (`uniform`) or the spread-after-capping rule
+    (`reactivated`) fired, and the frames fixed at N (`capped`).
+    """
+    L = len(r_tilde)
+    n = np.zeros(L, dtype=np.int64)
+    trace = dict(q=np.zeros(0), active=np.zeros(0, dtype=np.int64), left=0,
+                 uniform=False, reactivated=False, capped=np.zeros(L, dtype=bool))
+    if B >= L * N:
+        n[:] = N
+        trace["capped"][:] = True
+        return n, trace
+    w = np.maximum(np.asarray(r_tilde, dtype=np.float64), 0.0)
+    if np.sum(w) == 0.0:
+        w = np.ones(L)
+        trace["uniform"] = True
+    capped = np.zeros(L, dtype=bool)
+    active = w > 0
+    R = int(B)
+    while R > 0:
+        if not np.any(active):
+            # every positively weighted frame is full: spread the rest evenly
+            active = ~capped
+            w = np.where(capped, 0.0, 1.0)
+            trace["reactivated"] = True
+        idx = np.nonzero(active)[0]
+        q = R * w[idx] / np.sum(w[idx])
+        full = q >= N
+        if np.any(full):
+            n[idx[full]] = N
+            capped[idx[full]] = True
+            active[idx[full]] = False
+            R -= N * int(np.count_nonzero(full))
+            continue
+        base = np.floor(q)
+        left = R - int(np.sum(base))
+        frac = q - base
+        order = np.lexsort((idx, -frac))       # frac descending, then index ascending
+        n[idx] = base.astype(np.int64)
+        n[idx[order[:left]]] += 1
+        trace.update(q=q, active=idx, left=left)
+        R = 0
+    trace["capped"] = capped
+    return n, trace
+
+
+# ---------------------------------------------------------------------------
+# Wavelet Spatial Modulator (Eq. (12)-(15)) with the single-level Haar basis
+# ---------------------------------------------------------------------------
+
+def haar_analysis_2d(F):
+    """Single-level separable 2-D Haar of F [H, W, ...] -> (LL, LH, HL, HH) (Eq. (12)).
+
+    The first letter is the filter along the height axis, the second along the width.
+    """
+    lo_w, hi_w = haar_analysis(F, axis=1)
+    LL, HL = haar_analysis(lo_w, axis=0)
+    LH, HH = haar_analysis(hi_w, axis=0)
+    return LL, LH, HL, HH
+
+
+def haar_synthesis_2d(LL, LH, HL, HH, H, W):
+    """Inverse of `haar_analysis_2d`, cropped to H x W (Eq. (15))."""
+    lo_w = haar_synthesis(LL, HL, H, axis=0)
+    hi_w = haar_synthesis(LH, HH, H, axis=0)
+    return haar_synthesis(lo_w, hi_w, W, axis=1)
+
+
+def block_average(Mhw):
+    """Average-pool an H x W map to the Haar subband grid (P of Eq. (13))."""
+    Me = _extend_even(_extend_even(np.asarray(Mhw, dtype=np.float64), 0), 1)
+    return 0.25 * (Me[0::2, 0::2] + Me[0::2, 1::2] + Me[1::2, 0::2] + Me[1::2, 1::2])
+
+
+def wavelet_spatial_modulator(F, Mhw, lam):
+    """X-tilde_m for one frame F [H, W, C] with saliency map Mhw [H, W].
+
+    G_m = lam * P(M_m) (Eq. (13)); the three detail subbands are multiplied by G_m
+    (Eq. (14)) and the frame is rebuilt by the inverse transform (Eq. (15)); the
+    approximation LL is left unchanged.
+    """
+    H, W = Mhw.shape
+    LL, LH, HL, HH = haar_analysis_2d(F)
+    G = lam * block_average(Mhw)
+    G = G[:, :, None]
+    return haar_synthesis_2d(LL, G * LH, G * HL, G * HH, H, W)
+
+
+# ---------------------------------------------------------------------------
+# Token Assigner: selection and concatenation (Eq. (17) replaced, Eq. (19))
+# ---------------------------------------------------------------------------
+
+def select_tokens(a_t, n_t):
+    """Indices of the n_t largest saliency scores (ties -> smaller index), ascending."""
+    order = np.lexsort((np.arange(len(a_t)), -np.asarray(a_t)))
+    return np.sort(order[:n_t])
+
+
+def condense(X, query, B, levels=1, lam=1.5, tau=0.0):
+    """The whole pass C(X, Q) of Eq. (4)/(6); returns every intermediate.
+
+    Keys: a [T,N], vbar [T,C], r [T], delta [T], gamma [T], retained (list),
+    r_tilde [L], budget [T] (0 for dropped frames), offset [T+1], M [T,N],
+    tokens [offset[T], C], index [offset[T]] (flat t*N + h*W + w).
+    """
+    X = np.asarray(X, dtype=np.float64)
+    query = np.asarray(query, dtype=np.float64)
+    T, H, W, C = X.shape
+    N = H * W
+    a = token_saliency(X, query)
+    vbar = pooled_features(X)
+    r = frame_relevance(vbar, query)
+    delta = visual_change(vbar)
+    gamma = temporal_gate(delta)
+    kept_frames = retained_frames(delta, tau)
+    r_tilde = wavelet_temporal_allocator(r[kept_frames], gamma[kept_frames], levels)
+    n_kept = allocate_budget(r_tilde, B, N)
+    budget = np.zeros(T, dtype=np.int64)
+    budget[kept_frames] = n_kept
+    offset = np.concatenate([[0], np.cumsum(budget)]).astype(np.int64)
+    M = np.stack([saliency_map(a[t]) for t in range(T)])
+    tokens = np.zeros((int(offset[T]), C))
+    index = np.zeros(int(offset[T]), dtype=np.int64)
+    for t in range(T):
+        if budget[t] == 0:
+            continue
+        sel = select_tokens(a[t], int(budget[t]))
+        Xt = wavelet_spatial_modulator(X[t], M[t].reshape(H, W), lam)
+        tokens[offset[t]:offset[t + 1]] = Xt.reshape(N, C)[sel]
+        index[offset[t]:offset[t + 1]] = t * N + sel
+    return dict(a=a, vbar=vbar, r=r, delta=delta, gamma=gamma, retained=kept_frames,
+                r_tilde=r_tilde, budget=budget, offset=offset, M=M,
+                tokens=tokens, index=index)

@@ -1,0 +1,343 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each `pin_*` function raises AssertionError when the oracle disagrees with a
+closed form, an invariant, a hand-derived fixture or the pure-Python brute
+force.  The pins run as ordinary tests, and again under planted mistakes
+(test_oracle_mutations.py) to show that each plausible slip is caught.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+
+import brute
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _expr(s):
+    """Evaluate a closed-form fixture expression (numbers, + - * / and sqrt only)."""
+    allowed = set("0123456789.+-*/() sqrt")
+    if not set(s) <= allowed:
+        raise ValueError(f"unexpected characters in {s!r}")
+    return float(eval(s, {"__builtins__": {}}, {"sqrt": math.sqrt}))
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+# ---------------------------------------------------------------------------
+# 1-D Haar and the temporal allocator (Eq. (9)-(11))
+# ---------------------------------------------------------------------------
+
+def pin_haar1d_hand_values():
+    s2 = math.sqrt(2.0)
+    A, D = oracle.haar_analysis(np.array([1.0, 3.0]))
+    assert np.allclose(A, [4 / s2], rtol=0, atol=1e-15) and np.allclose(D, [-2 / s2], rtol=0, atol=1e-15)
+    # odd length: [1, 2, 4] is extended to [1, 2, 4, 4]
+    A, D = oracle.haar_analysis(np.array([1.0, 2.0, 4.0]))
+    assert np.allclose(A, [3 / s2, 8 / s2], atol=1e-15) and np.allclose(D, [-1 / s2, 0.0], atol=1e-15)
+    A, D = oracle.haar_analysis(np.array([5.0, 1.0, -2.0, 2.0]))
+    assert np.allclose(A, [6 / s2, 0.0], atol=1e-15) and np.allclose(D, [4 / s2, -4 / s2], atol=1e-15)
+
+
+def pin_haar1d_perfect_reconstruction():
+    rng = np.random.default_rng(11)
+    for n in range(1, 34):
+        x = rng.standard_normal(n)
+        A, D = oracle.haar_analysis(x)
+        y = oracle.haar_synthesis(A, D, n)
+        assert y.shape == (n,)
+        assert np.max(np.abs(y - x)) <= 1e-12
+
+
+def pin_haar1d_parseval():
+    rng = np.random.default_rng(12)
+    for n in range(2, 34, 2):
+        x = rng.standard_normal(n)
+        A, D = oracle.haar_analysis(x)
+        assert abs(np.sum(x * x) - np.sum(A * A) - np.sum(D * D)) <= 1e-12 * np.sum(x * x)
+    # odd length: energy of the extended signal
+    x = rng.standard_normal(7)
+    A, D = oracle.haar_analysis(x)
+    xe = np.append(x, x[-1])
+    assert abs(np.sum(xe * xe) - np.sum(A * A) - np.sum(D * D)) <= 1e-12 * np.sum(xe * xe)
+
+
+def pin_haar1d_matrix_form():
+    """Analysis equals the orthonormal Haar matrix applied to the signal."""
+    n = 8
+    Hm = np.zeros((n, n))
+    for k in range(n // 2):
+        Hm[k, 2 * k] = Hm[k, 2 * k + 1] = 1 / math.sqrt(2)
+        Hm[n // 2 + k, 2 * k] = 1 / math.sqrt(2)
+        Hm[n // 2 + k, 2 * k + 1] = -1 / math.sqrt(2)
+    assert np.allclose(Hm @ Hm.T, np.eye(n), atol=1e-15)
+    x = np.random.default_rng(13).standard_normal(n)
+    A, D = oracle.haar_analysis(x)
+    assert np.allclose(np.concatenate([A, D]), Hm @ x, atol=1e-14)
+
+
+def pin_wta_special_cases():
+    rng = np.random.default_rng(14)
+    for L in range(1, 20):
+        R = rng.standard_normal(L)
+        for J in (1, 2, 3):
+            # a fully open gate keeps every detail: perfect reconstruction
+            assert np.max(np.abs(oracle.wavelet_temporal_allocator(R, np.ones(L), J) - R)) <= 1e-12
+        # a closed gate at one level replaces each pair by its mean
+        out = oracle.wavelet_temporal_allocator(R, np.zeros(L), 1)
+        Re = np.append(R, R[-1]) if L % 2 else R
+        means = np.repeat(0.5 * (Re[0::2] + Re[1::2]), 2)[:L]
+        assert np.max(np.abs(out - means)) <= 1e-12
+    # two closed levels on a length divisible by 4 give block means of 4
+    R = rng.standard_normal(12)
+    out = oracle.wavelet_temporal_allocator(R, np.zeros(12), 2)
+    assert np.allclose(out, np.repeat(R.reshape(3, 4).mean(axis=1), 4), atol=1e-12)
+
+
+def pin_wta_hand_gate():
+    """J=1, R = (r0, r1), gate (g0, g1): r~0 = (r0+r1)/2 + g(r0-r1)/2 with g = (g0+g1)/2."""
+    r0, r1, g0, g1 = 0.3, -0.1, 0.2, 0.6
+    g = 0.5 * (g0 + g1)
+    out = oracle.wavelet_temporal_allocator(np.array([r0, r1]), np.array([g0, g1]), 1)
+    assert np.allclose(out, [(r0 + r1) / 2 + g * (r0 - r1) / 2, (r0 + r1) / 2 - g * (r0 - r1) / 2], atol=1e-15)
+    # J=2 on four samples with gates (1,0,0,1): level-1 details scaled by (1/2, 1/2), level 2 by 1/2
+    R = np.array([1.0, 2.0, 4.0, 8.0])
+    out = oracle.wavelet_temporal_allocator(R, np.array([1.0, 0.0, 0.0, 1.0]), 2)
+    pair = np.array([1.5, 6.0])                    # level-1 approximations / sqrt2
+    top = pair.mean() + 0.5 * (pair - pair.mean())  # level-2 detail halved
+    expect = np.array([top[0] - 0.25, top[0] + 0.25, top[1] - 1.0, top[1] + 1.0])
+    assert np.allclose(out, expect, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# 2-D Haar and the spatial modulator (Eq. (12)-(15))
+# ---------------------------------------------------------------------------
+
+def pin_haar2d_explicit_butterflies():
+    rng = np.random.default_rng(21)
+    F = rng.standard_normal((4, 6, 3))
+    LL, LH, HL, HH = oracle.haar_analysis_2d(F)
+    p00, p01, p10, p11 = F[0::2, 0::2], F[0::2, 1::2], F[1::2, 0::2], F[1::2, 1::2]
+    assert np.allclose(LL, (p00 + p01 + p10 + p11) / 2, atol=1e-14)
+    assert np.allclose(LH, (p00 - p01 + p10 - p11) / 2, atol=1e-14)
+    assert np.allclose(HL, (p00 + p01 - p10 - p11) / 2, atol=1e-14)
+    assert np.allclose(HH, (p00 - p01 - p10 + p11) / 2, atol=1e-14)
+
+
+def pin_haar2d_reconstruction_and_parseval():
+    rng = np.random.default_rng(22)
+    for H, W in [(2, 2), (3, 3), (4, 7), (13, 13), (14, 14), (1, 5), (5, 1)]:
+        F = rng.standard_normal((H, W, 2))
+        bands = oracle.haar_analysis_2d(F)
+        assert np.max(np.abs(oracle.haar_synthesis_2d(*bands, H, W) - F)) <= 1e-12
+        Fe = np.concatenate([F, F[-1:]], axis=0) if H % 2 else F
+        Fe = np.concatenate([Fe, Fe[:, -1:]], axis=1) if W % 2 else Fe
+        energy = sum(np.sum(b * b) for b in bands)
+        assert abs(energy - np.sum(Fe * Fe)) <= 1e-12 * np.sum(Fe * Fe)
+
+
+def pin_wsm_closed_form():
+    """Gating the three detail bands by g gives mu_b + g (x - mu_b) on each padded 2x2 block."""
+    rng = np.random.default_rng(23)
+    for H, W in [(2, 2), (3, 5), (14, 14), (13, 13)]:
+        F = rng.standard_normal((H, W, 3))
+        M = rng.random((H, W))
+        lam = 1.5
+        out = oracle.wavelet_spatial_modulator(F, M, lam)
+        for h in range(H):
+            for w in range(W):
+                rows = [h - h % 2, min(h - h % 2 + 1, H - 1)]
+                cols = [w - w % 2, min(w - w % 2 + 1, W - 1)]
+                mu = sum(F[r, c] for r in rows for c in cols) / 4
+                g = lam * sum(M[r, c] for r in rows for c in cols) / 4
+                assert np.allclose(out[h, w], mu + g * (F[h, w] - mu), atol=1e-12)
+
+
+def pin_wsm_unit_and_zero_gate():
+    rng = np.random.default_rng(24)
+    F = rng.standard_normal((5, 7, 4))
+    # lambda * mean(M) = 1 everywhere: identity
+    assert np.allclose(oracle.wavelet_spatial_modulator(F, np.full((5, 7), 2 / 3), 1.5), F, atol=1e-12)
+    # lambda = 0: every token becomes its (padded) block mean
+    out = oracle.wavelet_spatial_modulator(F, rng.random((5, 7)), 0.0)
+    assert np.allclose(out[0, 0], F[0:2, 0:2].mean(axis=(0, 1)), atol=1e-12)
+    assert np.allclose(out[4, 6], F[4, 6], atol=1e-12)            # corner block is one token repeated
+    assert np.allclose(out[4, 2], F[4, 2:4].mean(axis=0), atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Scores and the visual change estimator (Sec. 3.2.1, Eq. (7), Eq. (8))
+# ---------------------------------------------------------------------------
+
+def pin_cosine_cases():
+    v = np.array([[1.0, 2.0, -1.0]])
+    X = np.stack([np.stack([np.tile(v, (2, 1))] * 2)] * 3)   # three identical frames
+    d = oracle.visual_change(oracle.pooled_features(X))
+    assert np.allclose(d, 0.0, atol=1e-15)
+    ortho = np.array([[1.0, 0.0]]), np.array([[0.0, 3.0]])
+    anti = np.array([[1.0, -2.0]]), np.array([[-2.0, 4.0]])
+    assert abs(oracle.visual_change(np.concatenate(ortho))[1] - 1.0) <= 1e-15
+    assert abs(oracle.visual_change(np.concatenate(anti))[1] - 2.0) <= 1e-15
+    assert oracle.visual_change(np.array([[0.0, 0.0], [1.0, 2.0]]))[1] == 1.0   # zero vector: cos = 0
+    assert np.allclose(oracle.cosine_matrix(np.array([[2.0, 0.0]]), np.array([[0.0, 0.0], [5.0, 0.0]])), [[0.0, 1.0]])
+
+
+def pin_scores_scale_invariance_and_range():
+    rng = np.random.default_rng(31)
+    X = rng.standard_normal((3, 4, 5, 6))
+    q = rng.standard_normal((3, 6))
+    a = oracle.token_saliency(X, q)
+    assert a.shape == (3, 20) and np.all(a <= 1 + 1e-15) and np.all(a >= -1 - 1e-15)
+    scale = rng.random((3, 4, 5, 1)) + 0.5
+    assert np.allclose(oracle.token_saliency(X * scale, q * 7.0), a, atol=1e-14)
+    # a token equal to a query token scores 1
+    X2 = X.copy()
+    X2[1, 2, 3] = 4.0 * q[2]
+    assert abs(oracle.token_saliency(X2, q)[1, 2 * 5 + 3] - 1.0) <= 1e-14
+    # max over query tokens, brute loop
+    for t, n in [(0, 0), (2, 19)]:
+        x = X[t].reshape(20, 6)[n]
+        best = max(float(x @ qj) / (np.linalg.norm(x) * np.linalg.norm(qj)) for qj in q)
+        assert abs(a[t, n] - best) <= 1e-14
+    # relevance uses the pooled mean; scaling tokens of a frame uniformly leaves r unchanged
+    r = oracle.frame_relevance(oracle.pooled_features(X), q)
+    r2 = oracle.frame_relevance(oracle.pooled_features(X * 3.0), q)
+    assert np.allclose(r, r2, atol=1e-14)
+
+
+def pin_minmax_maps():
+    a = np.array([0.2, -0.4, 0.8, 0.8])
+    M = oracle.saliency_map(a)
+    assert np.allclose(M, [0.5, 0.0, 1.0, 1.0]) and oracle.saliency_map(np.full(4, 0.3)).tolist() == [0.0] * 4
+    g = oracle.temporal_gate(np.array([0.0, 0.5, 0.25, 1.0]))
+    assert np.allclose(g, [0.0, 0.5, 0.25, 1.0])
+    assert oracle.retained_frames(np.array([0.0, 0.1, 0.3, 0.05, 0.3]), 0.3) == [0, 2, 4]
+
+
+# ---------------------------------------------------------------------------
+# Budgets (Eq. (16) under Eq. (5))
+# ---------------------------------------------------------------------------
+
+def pin_budget_hand_cases():
+    assert oracle.allocate_budget(np.array([10.0, 1.0, 1.0]), 6, 4).tolist() == [4, 1, 1]    # cap then re-apportion
+    assert oracle.allocate_budget(np.array([0.3, 0.2, 0.5]), 7, 10).tolist() == [2, 1, 4]    # 2.1, 1.4, 3.5
+    assert oracle.allocate_budget(np.array([1.0, 1.0, 1.0]), 4, 10).tolist() == [2, 1, 1]    # ties -> smaller index
+    assert oracle.allocate_budget(np.array([-1.0, -0.5, 0.0]), 5, 10).tolist() == [2, 2, 1]  # all weights zero: uniform
+    assert oracle.allocate_budget(np.array([0.5, -1.0, 0.5]), 4, 10).tolist() == [2, 0, 2]   # negative relevance gets 0
+    assert oracle.allocate_budget(np.array([0.5, 0.1]), 30, 10).tolist() == [10, 10]          # shortfall: all full
+    assert oracle.allocate_budget(np.array([5.0, 0.0, 0.0]), 6, 4).tolist() == [4, 1, 1]      # full, then spread evenly
+    assert oracle.allocate_budget(np.array([0.2, 0.7]), 0, 10).tolist() == [0, 0]
+
+
+def pin_budget_invariants(cases=300, seed=41):
+    rng = np.random.default_rng(seed)
+    for _ in range(cases):
+        L = int(rng.integers(1, 12))
+        N = int(rng.integers(1, 30))
+        B = int(rng.integers(0, L * N + 5))
+        w = rng.standard_normal(L) * rng.choice([1e-3, 1.0, 100.0])
+        n = oracle.allocate_budget(w, B, N)
+        assert n.sum() == min(B, L * N)
+        assert np.all(n >= 0) and np.all(n <= N)
+        pos = np.maximum(w, 0)
+        if B < L * N and pos.sum() > 0:
+            q = B * pos / pos.sum()
+            if np.all(q < N):
+                assert np.all((n == np.floor(q)) | (n == np.ceil(q)))
+                assert np.all(n[pos == 0] == 0)
+
+
+def pin_budget_least_squares_brute():
+    """Without caps, largest remainders minimise sum (n - q)^2 over integer vectors with sum B."""
+    rng = np.random.default_rng(42)
+    for _ in range(60):
+        L = int(rng.integers(1, 5))
+        N = 8
+        B = int(rng.integers(0, 9))
+        w = rng.random(L) + 0.05
+        q = B * w / w.sum()
+        if np.any(q >= N):
+            continue
+        n = oracle.allocate_budget(w, B, N)
+        best = min(sum((c - qq) ** 2 for c, qq in zip(v, q))
+                   for v in itertools.product(range(N + 1), repeat=L) if sum(v) == B)
+        assert abs(sum((c - qq) ** 2 for c, qq in zip(n, q)) - best) <= 1e-12
+
+
+def pin_budget_matches_brute():
+    rng = np.random.default_rng(43)
+    for _ in range(200):
+        L = int(rng.integers(1, 7))
+        N = int(rng.integers(1, 9))
+        B = int(rng.integers(0, L * N + 3))
+        w = rng.standard_normal(L)
+        assert oracle.allocate_budget(w, B, N).tolist() == brute._apportion(list(w), B, N)
+
+
+# ---------------------------------------------------------------------------
+# Selection and end to end
+# ---------------------------------------------------------------------------
+
+def pin_selection_brute():
+    rng = np.random.default_rng(51)
+    for _ in range(100):
+        N = int(rng.integers(1, 12))
+        a = np.round(rng.standard_normal(N), 1)          # rounded: many exact ties
+        n = int(rng.integers(0, N + 1))
+        expect = sorted(sorted(range(N), key=lambda i: (-a[i], i))[:n])
+        assert oracle.select_tokens(a, n).tolist() == expect
+
+
+def _check_golden(fix, out):
+    exp = fix["expect"]
+    for key in ("a", "r", "delta", "gamma", "r_tilde"):
+        if key in exp:
+            want = np.array([[_expr(e) for e in row] for row in exp[key]] if isinstance(exp[key][0], list)
+                            else [_expr(e) for e in exp[key]])
+            assert np.allclose(np.asarray(out[key]), want, rtol=0, atol=1e-14), key
+    assert list(out["budget"]) == exp["budget"]
+    assert list(out["index"]) == exp["index"]
+    want = np.array([[_expr(e) for e in row] for row in exp["tokens"]])
+    assert np.allclose(np.asarray(out["tokens"]), want, rtol=0, atol=1e-14)
+
+
+def pin_golden_hand_cases():
+    for name in ("hand_2frame_2x2.json", "hand_1frame_3x3.json"):
+        fix = _load(name)
+        X, q = np.array(fix["X"], dtype=float), np.array(fix["query"], dtype=float)
+        out = oracle.condense(X, q, fix["B"], fix["levels"], fix["lam"], fix["tau"])
+        _check_golden(fix, out)
+        _check_golden(fix, brute.condense(fix["X"], fix["query"], fix["B"], fix["levels"], fix["lam"], fix["tau"]))
+        if "modulated_frame" in fix["expect"]:
+            Mt = oracle.saliency_map(out["a"][0]).reshape(3, 3)
+            mod = oracle.wavelet_spatial_modulator(X[0], Mt, fix["lam"])[:, :, 0]
+            want = np.array([[_expr(e) for e in row] for row in fix["expect"]["modulated_frame"]])
+            assert np.allclose(mod, want, atol=1e-14)
+
+
+def pin_end_to_end_brute(cases=40, seed=61):
+    rng = np.random.default_rng(seed)
+    for _ in range(cases):
+        T, H, W = (int(v) for v in rng.integers(1, 5, size=3))
+        C, Q = int(rng.integers(1, 4)), int(rng.integers(1, 3))
+        X = rng.standard_normal((T, H, W, C))
+        q = rng.standard_normal((Q, C))
+        B = int(rng.integers(0, T * H * W + 2))
+        J = int(rng.integers(1, 3))
+        tau = float(rng.choice([0.0, 0.4]))
+        o = oracle.condense(X, q, B, J, 1.5, tau)
+        b = brute.condense(X.tolist(), q.tolist(), B, J, 1.5, tau)
+        assert list(o["budget"]) == b["budget"]
+        assert list(o["index"]) == b["index"]
+        assert np.allclose(o["tokens"], np.array(b["tokens"]).reshape(o["tokens"].shape), atol=1e-12)
+        assert np.allclose(o["r_tilde"], b["r_tilde"], atol=1e-12)
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
