@@ -1,0 +1,175 @@
+"""Benchmark of the WaveZip condensation pass (wz_condense) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--out-dtype bf16|f32]
+
+One step = one wz_condense call over one seeded synthetic input set of the
+workload (default: T=64 frames of 14x14 tokens, C=3584 bf16, 32 query tokens,
+B=1254, 2 temporal levels).  Inputs are resident in HBM before timing; the
+call cycles through enough separate copies of the input (>= 512 MB in all)
+that the 256 MB Infinity Cache cannot serve a repeated frame tensor.
+
+Prints one JSON line: frames condensed per second (value), tokens/s, the
+algorithmic HBM rate of the whole call, the roofline of the dominant kernel
+(the relevance pass, timed with HIP events on its stream) and the CPU oracle's
+rate on the host as a reported baseline.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+METRIC = "frames condensed/s and achieved HBM GB/s (T=64, 14×14, C=3584 bf16)"
+HBM_PEAK_GBPS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="t64_14x14_c3584")
+    ap.add_argument("--out-dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time spent timing the oracle (0 disables)")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(wl, out_bytes):
+    """Bytes the pass must move per call: frames read once, query, condensed rows, indices, budgets."""
+    s_in = 2 if wl.dtype == "bf16" else 4
+    return (wl.T * wl.N * wl.C * s_in + wl.Q * wl.C * s_in + wl.B * wl.C * out_bytes + 4 * wl.B + 4 * wl.T)
+
+
+def relevance_bytes(wl):
+    """Bytes the relevance pass must move: frames and query read, scores written."""
+    s_in = 2 if wl.dtype == "bf16" else 4
+    return wl.T * wl.N * wl.C * s_in + wl.Q * wl.C * s_in + 4 * wl.T * wl.N + 8 * wl.T
+
+
+def cpu_baseline(inp, wl, seconds):
+    """Time the CPU oracle (as written) on whole passes over the same input until ~`seconds` elapse."""
+    import numpy as np  # noqa: F401
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # noqa: BLE001
+        threads = len(os.sched_getaffinity(0))
+    X, q = inp.X_f64(), inp.query_f64()
+    calls, t0 = 0, time.perf_counter()
+    while True:
+        oracle.condense(X, q, wl.B, wl.levels, wl.lam, wl.tau)
+        calls += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": wl.T * calls / el, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{calls} full passes of the float64 NumPy oracle over the same {wl.name} input "
+                      f"({wl.T} frames each), {el:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the pass is single-GPU by design.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2607_23265_amd import synth
+    from paper_2607_23265_amd import wavezip as wz
+
+    wl = synth.WORKLOADS[args.workload]
+    out_dtype = wz.WZ_BF16 if args.out_dtype == "bf16" else wz.WZ_F32
+    p = wz.problem_of(wl, out_dtype)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    inp = synth.generate(wl)
+    X0, q0 = wz.to_device(inp, dev)
+    nsets = max(1, math.ceil(2 * MALL_BYTES / X0.numel() / X0.element_size()))
+    Xs = [X0] + [X0.clone() for _ in range(nsets - 1)]
+    qs = [q0] + [q0.clone() for _ in range(nsets - 1)]
+    ws = wz.new_workspace(p, dev)
+    out = wz._out_tokens(p, dev)
+    stream = torch.cuda.current_stream(dev)
+
+    for i in range(args.warmup):
+        wz.condense(p, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        wz.condense(p, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+
+    # dominant kernel: the relevance pass, launched alone back to back on the same stream
+    a = torch.empty(wl.T * wl.N, dtype=torch.float32, device=dev)
+    r = torch.empty(wl.T, dtype=torch.float32, device=dev)
+    d = torch.empty(wl.T, dtype=torch.float32, device=dev)
+    import ctypes
+    L = wz.lib()
+    cfg = p.config()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+
+    def rel(i):
+        st = L.wz_relevance(ctypes.byref(cfg), wz._ptr(Xs[i % nsets]), wz._ptr(qs[i % nsets]), wz._ptr(a),
+                            wz._ptr(r), wz._ptr(d), wz._ptr(ws), ws.numel(), sp)
+        if st != 0:
+            raise wz.WZError(st, "wz_relevance")
+
+    for i in range(args.warmup):
+        rel(i)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        rel(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    k1_ms = ev0.elapsed_time(ev1) / args.steps
+    k1_bytes = relevance_bytes(wl)
+    k1_gbps = k1_bytes / (k1_ms * 1e-3) / 1e9
+
+    out_bytes = 2 if out_dtype == wz.WZ_BF16 else 4
+    call_bytes = algorithmic_bytes(wl, out_bytes)
+    frames_s = wl.T / (ms_step * 1e-3)
+    line = {
+        "metric": METRIC,
+        "value": frames_s,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "T": wl.T, "H": wl.H, "W": wl.W, "C": wl.C, "Q": wl.Q, "B": wl.B,
+                   "levels": wl.levels, "lambda": wl.lam, "tau": wl.tau, "in_dtype": wl.dtype,
+                   "out_dtype": args.out_dtype, "seed": wl.seed, "input_copies": nsets},
+        "tokens_per_s": wl.T * wl.N / (ms_step * 1e-3),
+        "hbm_gbps": call_bytes / (ms_step * 1e-3) / 1e9,
+        "hbm_frac": call_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "bytes_per_step": call_bytes,
+        "wall_s": wall,
+        "roofline": {"kernel": "relevance pass (wz_relevance)", "bound": "hbm", "achieved": k1_gbps,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k1_gbps / HBM_PEAK_GBPS,
+                     "traffic": None, "bytes_per_launch": k1_bytes, "us_per_launch": k1_ms * 1e3},
+    }
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

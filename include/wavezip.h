@@ -1,0 +1,148 @@
+/*
+ * wavezip.h -- C ABI of the WaveZip token-condensation pass on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The pass implements the query-conditioned condensation C(X, Q) -> Z~ of
+ * Sec. 3.1, Eq. (4)-(5): T frames of H x W visual tokens with C channels and a
+ * query of Q tokens go in; at most B tokens come out, with per-frame budgets
+ * n_t >= 0 that sum to B.  It has four stages, each with its own entry point:
+ *
+ *   wz_relevance            similarity scores a_{t,n}, frame relevance r_t and
+ *                           visual change delta_t (Sec. 3.2.1, Eq. (8));
+ *   wz_temporal_budget      gate gamma, frame filter, gated temporal Haar DWT
+ *                           and its inverse, and integer budgets
+ *                           (Sec. 3.2.2, Eq. (9)-(11), Eq. (16) with Eq. (5));
+ *   wz_spatial_dwt_condense saliency map, per-frame selection and the
+ *                           saliency-gated 2-D Haar modulation, compacted in
+ *                           temporal order (Eq. (7), Eq. (12)-(15), Eq. (19));
+ *   wz_condense             the three stages in sequence.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers: every array argument is a DEVICE pointer owned by the caller.  The
+ *   library never allocates, frees or keeps device memory, and keeps no state
+ *   between calls.  Arrays are dense, row-major and contiguous.
+ * Layouts: X is [T][H][W][C] (channels fastest); query is [Q][C]; both hold
+ *   cfg->in_dtype.  A token's flat index is t*H*W + h*W + w (0-based).
+ * Alignment: X, query and out_tokens must be 16-byte aligned; float and int32
+ *   arrays 4-byte aligned; the workspace 256-byte aligned.
+ * Streams: `stream` is a hipStream_t passed as void* (NULL = the default
+ *   stream).  All work is enqueued asynchronously on it; nothing is copied
+ *   back to the host.  Calls on distinct buffers may run concurrently.
+ * Errors: the returned status covers argument validation and kernel-launch
+ *   errors only.  When validation fails nothing is enqueued.  Device-side
+ *   errors surface on the stream like any HIP error.
+ * Determinism: for fixed inputs every output is bitwise reproducible (all
+ *   reductions run in a fixed order; no floating-point atomics).
+ * Readings of the paper used throughout: with several query tokens a score is
+ *   the maximum over query tokens of the cosine; a cosine involving a zero
+ *   vector is 0; min-max normalisations of an all-equal input give 0; frame 0
+ *   is always retained; odd lengths are extended by repeating the last sample
+ *   before each Haar step; Eq. (16)'s rounding is a capped largest-remainder
+ *   apportionment (ties to the smaller frame index); the interpolation of
+ *   Eq. (17) is replaced by keeping each frame's n_t most salient tokens (ties
+ *   to the smaller index) in raster order.
+ */
+#ifndef WAVEZIP_H
+#define WAVEZIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WZ_OK = 0,
+  WZ_ERR_NULL = 1,       /* a required pointer is NULL                        */
+  WZ_ERR_ALIGN = 2,      /* a pointer violates its alignment                  */
+  WZ_ERR_SHAPE = 3,      /* a dimension is out of the supported range         */
+  WZ_ERR_DTYPE = 4,      /* unknown in_dtype / out_dtype                      */
+  WZ_ERR_PARAM = 5,      /* levels, lambda or tau out of range                */
+  WZ_ERR_BUDGET = 6,     /* B < 0 or B > T*H*W                                */
+  WZ_ERR_WORKSPACE = 7,  /* workspace smaller than wz_workspace_bytes()       */
+  WZ_ERR_DEVICE = 8      /* a HIP call or kernel launch failed                */
+} wz_status;
+
+typedef enum { WZ_F32 = 0, WZ_BF16 = 1 } wz_dtype;
+
+/* Problem description.  Supported ranges (anything else is WZ_ERR_SHAPE /
+ * WZ_ERR_PARAM): 1 <= T <= 2048; 1 <= H, W and H*W <= 4096; 1 <= Q <= 1024;
+ * 8 <= C <= 65536 with C % 8 == 0; 1 <= levels <= 16; lambda_ finite and
+ * >= 0; tau in [0, 2].                                                        */
+typedef struct {
+  int32_t T, H, W, C, Q;
+  int32_t in_dtype;   /* wz_dtype of X and query                               */
+  int32_t out_dtype;  /* wz_dtype of out_tokens (WZ_F32 keeps full precision)  */
+  int32_t levels;     /* J, temporal Haar levels (the paper uses 1)            */
+  int64_t B;          /* global token budget, 0 <= B <= T*H*W                  */
+  float lambda_;      /* WSM modulation strength (the paper's default: 1.5)    */
+  float tau;          /* frame-filter threshold on delta; 0 keeps every frame  */
+} wz_config;
+
+/* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`
+ * (0 if cfg is invalid).  The workspace holds per-tile partial sums and the
+ * intermediate scores; its contents on entry are ignored.                     */
+size_t wz_workspace_bytes(const wz_config* cfg);
+
+/* Stage 1 -- Cross-Modal Scorer (similarity branch, Sec. 3.2.1) and Visual
+ * Change Estimator (Sec. 3.2.2, Eq. (8)).  One pass over X computes
+ *   tok_score[t*H*W + n] = a_{t,n} = max_j cos(x_{t,n}, q_j)          [T*H*W]
+ *   frame_rel[t]         = r_t = max_j cos(v_t, q_j)                  [T]
+ *   frame_delta[t]       = delta_t = clamp(1 - cos(v_t, v_{t-1}), 0, 2),
+ *                          delta_0 = 0                                  [T]
+ * where v_t is the spatial mean of frame t's tokens.  Accumulation is fp32.
+ * ws: at least wz_workspace_bytes(cfg) bytes of device memory.              */
+wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
+                       float* tok_score, float* frame_rel, float* frame_delta,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Stage 2 -- Wavelet Temporal Allocator and budget (Sec. 3.2.2; Eq. (9)-(11);
+ * Eq. (16) under Eq. (5)).  From r and delta (as produced by wz_relevance):
+ * gamma = min-max(delta) over all T frames; retained set M = {0} U
+ * {t : delta_t >= tau}; J-level orthonormal Haar DWT of r over M with every
+ * detail level multiplied by gamma pair-averaged to its resolution; inverse
+ * DWT -> r~; budgets from w = max(r~, 0) (uniform if all zero), capped at
+ * H*W per frame, summing to min(B, |M|*H*W).  Arithmetic is fp64.
+ * Outputs: budget[T] (0 for dropped frames); offset[T+1] with offset[0] = 0
+ * and offset[t+1] = offset[t] + budget[t] (offset[T] = tokens emitted);
+ * rel_rect[T] = r~ for retained frames and 0 for dropped ones (may be NULL). */
+wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel,
+                             const float* frame_delta, int32_t* budget,
+                             int32_t* offset, float* rel_rect, void* stream);
+
+/* Stage 3 -- Wavelet Spatial Modulator and Token Assigner (Eq. (7),
+ * Eq. (12)-(15), Eq. (19)).  For every frame with budget[t] > 0: M_t =
+ * min-max(tok_score of frame t); keep the budget[t] tokens of largest score
+ * (ties -> smaller index); for each kept token take its 2x2 Haar block of the
+ * grid (last row/column repeated when H or W is odd), compute LL/LH/HL/HH,
+ * multiply the three detail bands by g = lambda_ * mean(M over the block),
+ * invert, and write the token's reconstructed features to row offset[t] + k
+ * of out_tokens ([offset[T]][C], cfg->out_dtype), k = the token's rank in
+ * raster order among the frame's kept tokens; out_index gets its flat index.
+ * Rows from offset[T] on are not written.  budget/offset must satisfy
+ * 0 <= budget[t] <= H*W and offset = exclusive prefix sum of budget (as
+ * produced by wz_temporal_budget); out_tokens must hold offset[T] <= B rows.  */
+wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X,
+                                  const float* tok_score, const int32_t* budget,
+                                  const int32_t* offset, void* out_tokens,
+                                  int32_t* out_index, void* stream);
+
+/* The whole pass C(X, Q) of Eq. (4)/(6): stage 1, 2 and 3 in sequence on one
+ * stream, intermediates kept in `ws`.  out_tokens [B][C] (cfg->out_dtype) and
+ * out_index [B] receive offset[T] rows (= B unless the frame filter leaves
+ * fewer than B tokens).  budget [T] and offset [T+1] are optional outputs
+ * (NULL: kept in the workspace).                                              */
+wz_status wz_condense(const wz_config* cfg, const void* X, const void* query,
+                      void* out_tokens, int32_t* out_index, int32_t* budget,
+                      int32_t* offset, void* ws, size_t ws_bytes, void* stream);
+
+/* Static, human-readable name of a status code.                               */
+const char* wz_status_str(wz_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WAVEZIP_H */

@@ -1,0 +1,132 @@
+// C ABI of the condensation pass: argument validation, workspace carve-up and
+// the launch sequence.  Declarations and contracts are in include/wavezip.h.
+#include <cmath>
+#include <cstdint>
+
+#include "wz_internal.h"
+
+using namespace wz;
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+wz_status check_config(const wz_config* c) {
+  if (!c) return WZ_ERR_NULL;
+  if ((c->in_dtype != WZ_F32 && c->in_dtype != WZ_BF16) || (c->out_dtype != WZ_F32 && c->out_dtype != WZ_BF16))
+    return WZ_ERR_DTYPE;
+  if (c->T < 1 || c->T > 2048 || c->H < 1 || c->W < 1 || int64_t(c->H) * c->W > 4096 || c->Q < 1 ||
+      c->Q > 1024 || c->C < 8 || c->C > 65536 || c->C % 8 != 0)
+    return WZ_ERR_SHAPE;
+  if (c->levels < 1 || c->levels > 16 || !std::isfinite(c->lambda_) || c->lambda_ < 0.f ||
+      !std::isfinite(c->tau) || c->tau < 0.f || c->tau > 2.f)
+    return WZ_ERR_PARAM;
+  if (c->B < 0 || c->B > int64_t(c->T) * c->H * c->W) return WZ_ERR_BUDGET;
+  return WZ_OK;
+}
+
+wz_status check_ptr(const void* p, uintptr_t align) {
+  if (!p) return WZ_ERR_NULL;
+  if (!aligned(p, align)) return WZ_ERR_ALIGN;
+  return WZ_OK;
+}
+
+#define WZ_TRY(expr)                 \
+  do {                               \
+    const wz_status st_ = (expr);    \
+    if (st_ != WZ_OK) return st_;    \
+  } while (0)
+
+wz_status from_hip(hipError_t e) { return e == hipSuccess ? WZ_OK : WZ_ERR_DEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+size_t wz_workspace_bytes(const wz_config* cfg) {
+  if (check_config(cfg) != WZ_OK) return 0;
+  return workspace_layout(*cfg, nullptr).bytes;
+}
+
+const char* wz_status_str(wz_status s) {
+  switch (s) {
+    case WZ_OK: return "WZ_OK";
+    case WZ_ERR_NULL: return "WZ_ERR_NULL: a required pointer is NULL";
+    case WZ_ERR_ALIGN: return "WZ_ERR_ALIGN: a pointer is not suitably aligned";
+    case WZ_ERR_SHAPE: return "WZ_ERR_SHAPE: a dimension is out of the supported range";
+    case WZ_ERR_DTYPE: return "WZ_ERR_DTYPE: unknown data type";
+    case WZ_ERR_PARAM: return "WZ_ERR_PARAM: levels, lambda or tau out of range";
+    case WZ_ERR_BUDGET: return "WZ_ERR_BUDGET: B must satisfy 0 <= B <= T*H*W";
+    case WZ_ERR_WORKSPACE: return "WZ_ERR_WORKSPACE: workspace too small or misaligned";
+    case WZ_ERR_DEVICE: return "WZ_ERR_DEVICE: a HIP call or kernel launch failed";
+  }
+  return "unknown wz_status";
+}
+
+wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query, float* tok_score,
+                       float* frame_rel, float* frame_delta, void* ws, size_t ws_bytes, void* stream) {
+  WZ_TRY(check_config(cfg));
+  WZ_TRY(check_ptr(X, 16));
+  WZ_TRY(check_ptr(query, 16));
+  WZ_TRY(check_ptr(tok_score, 4));
+  WZ_TRY(check_ptr(frame_rel, 4));
+  WZ_TRY(check_ptr(frame_delta, 4));
+  if (!ws) return WZ_ERR_NULL;
+  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
+  if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
+  return from_hip(launch_relevance(*cfg, X, query, tok_score, frame_rel, frame_delta, w,
+                                   static_cast<hipStream_t>(stream)));
+}
+
+wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const float* frame_delta,
+                             int32_t* budget, int32_t* offset, float* rel_rect, void* stream) {
+  WZ_TRY(check_config(cfg));
+  WZ_TRY(check_ptr(frame_rel, 4));
+  WZ_TRY(check_ptr(frame_delta, 4));
+  WZ_TRY(check_ptr(budget, 4));
+  WZ_TRY(check_ptr(offset, 4));
+  if (rel_rect && !aligned(rel_rect, 4)) return WZ_ERR_ALIGN;
+  return from_hip(launch_temporal_budget(*cfg, frame_rel, frame_delta, budget, offset, rel_rect,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const float* tok_score,
+                                  const int32_t* budget, const int32_t* offset, void* out_tokens,
+                                  int32_t* out_index, void* stream) {
+  WZ_TRY(check_config(cfg));
+  WZ_TRY(check_ptr(X, 16));
+  WZ_TRY(check_ptr(tok_score, 4));
+  WZ_TRY(check_ptr(budget, 4));
+  WZ_TRY(check_ptr(offset, 4));
+  if (cfg->B > 0) {
+    WZ_TRY(check_ptr(out_tokens, 16));
+    WZ_TRY(check_ptr(out_index, 4));
+  }
+  return from_hip(launch_spatial_condense(*cfg, X, tok_score, budget, offset, out_tokens, out_index,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
+                      int32_t* out_index, int32_t* budget, int32_t* offset, void* ws, size_t ws_bytes,
+                      void* stream) {
+  WZ_TRY(check_config(cfg));
+  WZ_TRY(check_ptr(X, 16));
+  WZ_TRY(check_ptr(query, 16));
+  if (cfg->B > 0) {
+    WZ_TRY(check_ptr(out_tokens, 16));
+    WZ_TRY(check_ptr(out_index, 4));
+  }
+  if (budget && !aligned(budget, 4)) return WZ_ERR_ALIGN;
+  if (offset && !aligned(offset, 4)) return WZ_ERR_ALIGN;
+  if (!ws) return WZ_ERR_NULL;
+  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
+  if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* bud = budget ? budget : w.budget;
+  int32_t* off = offset ? offset : w.offset;
+  WZ_TRY(from_hip(launch_relevance(*cfg, X, query, w.tok_score, w.frame_rel, w.frame_delta, w, s)));
+  WZ_TRY(from_hip(launch_temporal_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s)));
+  return from_hip(launch_spatial_condense(*cfg, X, w.tok_score, bud, off, out_tokens, out_index, s));
+}
+
+}  // extern "C"
