@@ -82,8 +82,13 @@ typedef struct {
 } wz_config;
 
 /* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`
- * (0 if cfg is invalid).  The workspace holds per-tile partial sums and the
- * intermediate scores; its contents on entry are ignored.                     */
+ * (0 if cfg is invalid).  The workspace holds per-tile partial sums, the
+ * intermediate scores and, in its first bytes, the counters with which the
+ * relevance kernel finds the last workgroup of each frame.  Zero-fill a
+ * workspace once before its first use; every call leaves those counters at
+ * zero again, so the same workspace can be reused by later calls of any cfg
+ * (one call at a time per workspace).  Apart from the counters, contents on
+ * entry are ignored.                                                          */
 size_t wz_workspace_bytes(const wz_config* cfg);
 
 /* Stage 1 -- Cross-Modal Scorer (similarity branch, Sec. 3.2.1) and Visual
@@ -93,7 +98,8 @@ size_t wz_workspace_bytes(const wz_config* cfg);
  *   frame_delta[t]       = delta_t = clamp(1 - cos(v_t, v_{t-1}), 0, 2),
  *                          delta_0 = 0                                  [T]
  * where v_t is the spatial mean of frame t's tokens.  Accumulation is fp32.
- * ws: at least wz_workspace_bytes(cfg) bytes of device memory.              */
+ * ws: at least wz_workspace_bytes(cfg) bytes of device memory, zero-filled
+ * before its first use (see wz_workspace_bytes).  One kernel launch.       */
 wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
                        float* tok_score, float* frame_rel, float* frame_delta,
                        void* ws, size_t ws_bytes, void* stream);

@@ -36,33 +36,55 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiling of the relevance pass: every workgroup owns one tile of up to
-// 16 * kMaxMTiles consecutive tokens of one frame and reads all C channels.
+// Tiling of the relevance pass: every workgroup owns one tile of up to 32
+// consecutive tokens of one frame and reads all C channels of them.
 // ---------------------------------------------------------------------------
-constexpr int kMaxMTiles = 4;
+constexpr int kXcds = 8;  // MI355X: workgroups are dealt to the 8 XCDs round robin
 
 struct Tiling {
   int tiles_per_frame;  // ceil(N / tile_tokens)
   int tile_tokens;      // tokens per tile (the last tile of a frame may be shorter)
   int mtiles;           // 16-row MFMA tiles per workgroup tile
+  int grid;             // workgroups: frames rounded up to a multiple of kXcds, times tiles
 };
 
 inline Tiling relevance_tiling(const wz_config& c) {
   const int N = c.H * c.W;
-  // Tiles of at most 32 tokens (two 16-row MFMA tiles), balanced within a frame.
-  const int cap = 32;
+  const int cap = 32;  // two 16-row MFMA tiles
   Tiling t;
   t.tiles_per_frame = (N + cap - 1) / cap;
   t.tile_tokens = (N + t.tiles_per_frame - 1) / t.tiles_per_frame;
   t.mtiles = (t.tile_tokens + 15) / 16;
+  t.grid = (c.T + kXcds - 1) / kXcds * kXcds * t.tiles_per_frame;
   return t;
 }
 
+// Workgroup b handles frame t = (b / kXcds / tiles) * kXcds + b % kXcds and
+// tile (b / kXcds) % tiles, so every tile of a frame runs on the same XCD
+// (its L2 then holds the partial sums the frame's last workgroup combines).
+__device__ __forceinline__ void tile_of_block(int b, int tiles, int& t, int& tile) {
+  const int xcd = b % kXcds, slot = b / kXcds;
+  tile = slot % tiles;
+  t = (slot / tiles) * kXcds + xcd;
+}
+
+// Counters the relevance pass uses to find the last workgroup of a frame and
+// of a pair of adjacent frames.  They sit at the start of the workspace, are
+// left at zero by every call, and must be zero before the first call.
+constexpr int kMaxFrames = 2048;
+struct Counters {
+  int frame[kMaxFrames];     // tiles of frame t finished
+  int pair[kMaxFrames + 1];  // frames t-1, t finished (for delta_t)
+};
+
 // Workspace carve-up (all offsets 256-byte aligned).
 struct Workspace {
+  Counters* ctr;       // zero between calls
   float* pool_part;    // [T][tiles][C]  per-tile channel sums
   float* sig_part;     // [T][tiles][Q]  per-tile sums of x . q_j
-  float* rq;           // [Q]            1 / ||q_j|| (0 for a zero query token)
+  float* pooled;       // [T][C]         per-frame channel sums p_t
+  double* pnorm2;      // [T]            |p_t|^2
+  float* rq;           // [Q]            1 / |q_j| (0 for a zero query token)
   float* tok_score;    // [T*N]
   float* frame_rel;    // [T]
   float* frame_delta;  // [T]
@@ -79,8 +101,11 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   Workspace w;
   size_t off = 0;
   auto take = [&](size_t bytes) { char* p = base ? base + off : nullptr; off += align256(bytes); return p; };
+  w.ctr = reinterpret_cast<Counters*>(take(sizeof(Counters)));
   w.pool_part = reinterpret_cast<float*>(take(T * tiles * C * 4));
   w.sig_part = reinterpret_cast<float*>(take(T * tiles * Q * 4));
+  w.pooled = reinterpret_cast<float*>(take(T * C * 4));
+  w.pnorm2 = reinterpret_cast<double*>(take(T * 8));
   w.rq = reinterpret_cast<float*>(take(Q * 4));
   w.tok_score = reinterpret_cast<float*>(take(T * N * 4));
   w.frame_rel = reinterpret_cast<float*>(take(T * 4));

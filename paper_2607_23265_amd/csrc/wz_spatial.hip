@@ -2,12 +2,12 @@
 // Assigner's compaction (Eq. (19)), with the interpolation of Eq. (17)
 // replaced by saliency-ranked selection.
 //
-// Grid: `sub` workgroups per frame.  Each workgroup of frame t
+// Grid: `sub` workgroups of 4 waves per frame.  Each workgroup of frame t
 //   1. loads the frame's scores a_{t,.} into LDS and forms the saliency map
 //      M = min-max(a) (Eq. (7); M = 0 if all scores are equal);
 //   2. marks the budget[t] highest-scoring tokens (ties: smaller index) and
 //      lists them in raster order (block prefix scan);
-//   3. for every sub-th kept token: reads the token's 2x2 Haar block (the last
+//   3. gives each wave one kept token at a time: it reads the token's 2x2 Haar block (the last
 //      row / column repeated when H or W is odd), forms LL, LH, HL, HH with the
 //      orthonormal 2-D Haar butterflies (Eq. (12)), multiplies LH, HL, HH by
 //      g = lambda * mean(M over the block) (Eq. (13)-(14)), inverts for the
@@ -170,7 +170,9 @@ __global__ __launch_bounds__(kThreads) void k_spatial_condense(const In* __restr
   const int nvec = C / V;
   // rows beyond the kept count or beyond B are never written
   const int rows = int(min((long long)min(nt, total), B - base));
-  for (int k = part; k < rows; k += sub) {
+  constexpr int kWaves = kThreads / kWave;
+  constexpr int UNR = 4;  // channel vectors per lane in flight (4 loads each)
+  for (int k = part * kWaves + wave; k < rows; k += sub * kWaves) {
     const int n = s_kept[k];
     const int h = n / W, w = n - h * W;
     const int i0 = h & ~1, j0 = w & ~1;
@@ -183,33 +185,46 @@ __global__ __launch_bounds__(kThreads) void k_spatial_condense(const In* __restr
     const In* p10 = Xt + size_t(i1 * W + j0) * C;
     const In* p11 = Xt + size_t(i1 * W + j1) * C;
     Out* dst = out_tokens + size_t(base + k) * C;
-    for (int v = tid; v < nvec; v += kThreads) {
-      float x00[V], x01[V], x10[V], x11[V], y[V];
-      Load8<In>::run(p00 + v * V, x00);
-      Load8<In>::run(p01 + v * V, x01);
-      Load8<In>::run(p10 + v * V, x10);
-      Load8<In>::run(p11 + v * V, x11);
+    for (int v0 = lane; v0 < nvec; v0 += UNR * kWave) {
+      float x00[UNR][V], x01[UNR][V], x10[UNR][V], x11[UNR][V];
 #pragma unroll
-      for (int i = 0; i < V; ++i) {
-        // orthonormal 2-D Haar butterflies of the block (Eq. (12))
-        const float LL = 0.5f * ((x00[i] + x01[i]) + (x10[i] + x11[i]));
-        const float LH = 0.5f * ((x00[i] - x01[i]) + (x10[i] - x11[i]));
-        const float HL = 0.5f * ((x00[i] + x01[i]) - (x10[i] + x11[i]));
-        const float HH = 0.5f * ((x00[i] - x01[i]) - (x10[i] - x11[i]));
-        // gate the detail bands (Eq. (14)) and invert at the token's position (Eq. (15))
-        y[i] = 0.5f * (LL + g * (sw * LH + sh * HL + (sw * sh) * HH));
+      for (int u = 0; u < UNR; ++u) {
+        const int v = v0 + u * kWave;
+        if (v < nvec) {
+          Load8<In>::run(p00 + v * V, x00[u]);
+          Load8<In>::run(p01 + v * V, x01[u]);
+          Load8<In>::run(p10 + v * V, x10[u]);
+          Load8<In>::run(p11 + v * V, x11[u]);
+        }
       }
-      store_row<Out, V>(dst + v * V, y);
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int v = v0 + u * kWave;
+        if (v >= nvec) break;
+        float y[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+          // orthonormal 2-D Haar butterflies of the block (Eq. (12))
+          const float LL = 0.5f * ((x00[u][i] + x01[u][i]) + (x10[u][i] + x11[u][i]));
+          const float LH = 0.5f * ((x00[u][i] - x01[u][i]) + (x10[u][i] - x11[u][i]));
+          const float HL = 0.5f * ((x00[u][i] + x01[u][i]) - (x10[u][i] + x11[u][i]));
+          const float HH = 0.5f * ((x00[u][i] - x01[u][i]) - (x10[u][i] - x11[u][i]));
+          // gate the detail bands (Eq. (14)) and invert at the token's position (Eq. (15))
+          y[i] = 0.5f * (LL + g * (sw * LH + sh * HL + (sw * sh) * HH));
+        }
+        store_row<Out, V>(dst + v * V, y);
+      }
     }
-    if (tid == 0) out_index[base + k] = t * N + n;
+    if (lane == 0) out_index[base + k] = t * N + n;
   }
 }
 
 template <typename In, typename Out>
 void launch_typed(const wz_config& c, const void* X, const float* tok_score, const int32_t* budget,
                   const int32_t* offset, void* out_tokens, int32_t* out_index, hipStream_t s) {
-  // enough workgroups to spread the kept rows over the chip
-  const int sub = std::max(1, std::min(16, (2048 + c.T - 1) / c.T));
+  // one wave per kept row: about B / T rows per frame, 4 waves per workgroup
+  const long long per_frame = (c.B + c.T - 1) / c.T;
+  const int sub = int(std::max<long long>(1, std::min<long long>(64, (per_frame + 3) / 4)));
   hipLaunchKernelGGL((k_spatial_condense<In, Out>), dim3(c.T * sub), dim3(kThreads), 0, s,
                      static_cast<const In*>(X), tok_score, budget, offset, c.H, c.W, c.C, (long long)c.B, c.lambda_, sub,
                      static_cast<Out*>(out_tokens), out_index);

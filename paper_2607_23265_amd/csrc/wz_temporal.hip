@@ -1,9 +1,9 @@
 // Stage 2: Wavelet Temporal Allocator (Sec. 3.2.2 gate and frame filter,
 // Eq. (9)-(11)) and the integer frame budgets (Eq. (16) under Eq. (5)).
 //
-// The whole stage is a few hundred fp64 operations per frame, so it runs as
-// ONE workgroup of 1024 threads with every array in LDS; frame t is handled by
-// thread t (and t + 1024).  Steps:
+// The whole stage is a few fp64 operations per frame, so it runs as ONE
+// workgroup with every array in LDS: one wave when T <= 64 (no cross-wave
+// synchronisation at all), 256 threads up to T = 256, 1024 beyond.  Steps:
 //   gamma  = min-max(delta) over all T frames (0 if all equal);
 //   M      = {0} U {t >= 1 : delta_t >= tau}, compacted in temporal order;
 //   WTA    = J levels of orthonormal Haar analysis of r over M (odd lengths
@@ -19,72 +19,75 @@
 namespace wz {
 namespace {
 
-constexpr int kThreads = 1024;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kTMax = 2048;
-constexpr int kPer = kTMax / kThreads;  // frames per thread
+constexpr int kTMax = kMaxFrames;
 constexpr int kMaxLevels = 16;
 
 enum : unsigned char { kIdle = 0, kActive = 1, kFull = 2 };
 
 struct Shared {
-  double a[kTMax];                  // approximation being transformed, then r~
-  double g[kTMax];                  // gate, pooled with the approximation
-  double det[kTMax + kMaxLevels];   // gated detail coefficients of every level
-  double w[kTMax];                  // weights, then fractional parts
-  int idx[kTMax];                   // frame index of each retained position
-  int n[kTMax];                     // budget of each retained position
-  int fb[kTMax];                    // budget of each frame
+  double a[2][kTMax];              // approximation (ping-pong), then r~ in a[0]
+  double g[2][kTMax];              // gate pooled alongside (ping-pong); g[0] reused for weights
+  double det[kTMax + kMaxLevels];  // gated detail coefficients of every level
+  int idx[kTMax];                  // frame index of each retained position
+  int n[kTMax];                    // budget of each retained position
+  int fb[kTMax];                   // budget of each frame
   unsigned char state[kTMax];
-  double dred[kWaves];
-  int ired[kWaves];
+  double dred[16];
+  int ired[16];
   int lens[kMaxLevels];
   int doffs[kMaxLevels];
 };
 
-__device__ double block_sum(double v, Shared& sh) {
+template <int NT>
+__device__ double bsum(double v, Shared& sh) {
   v = wave_sum_f64(v);
+  if (NT == kWave) return v;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sh.dred[wave] = v;
   __syncthreads();
   double s = 0.0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) s += sh.dred[i];
+  for (int i = 0; i < NT / kWave; ++i) s += sh.dred[i];
   return s;
 }
 
-__device__ double block_min_max(double v, bool want_max, Shared& sh) {
+template <int NT>
+__device__ double bminmax(double v, bool want_max, Shared& sh) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
     const double o = __shfl_xor(v, m, kWave);
     v = want_max ? fmax(v, o) : fmin(v, o);
   }
+  if (NT == kWave) return v;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sh.dred[wave] = v;
   __syncthreads();
   double r = sh.dred[0];
-  for (int i = 1; i < kWaves; ++i) r = want_max ? fmax(r, sh.dred[i]) : fmin(r, sh.dred[i]);
+#pragma unroll
+  for (int i = 1; i < NT / kWave; ++i) r = want_max ? fmax(r, sh.dred[i]) : fmin(r, sh.dred[i]);
   return r;
 }
 
-__device__ int block_sum_int(int v, Shared& sh) {
+template <int NT>
+__device__ int bsum_int(int v, Shared& sh) {
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  if (NT == kWave) return v;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sh.ired[wave] = v;
   __syncthreads();
   int s = 0;
 #pragma unroll
-  for (int i = 0; i < kWaves; ++i) s += sh.ired[i];
+  for (int i = 0; i < NT / kWave; ++i) s += sh.ired[i];
   return s;
 }
 
-// Exclusive prefix sum of v over the block in thread order (thread i's
-// contribution precedes thread i+1's); returns the prefix, `total` gets the sum.
-__device__ int block_exclusive_scan(int v, int& total, Shared& sh) {
+// Exclusive prefix sum over the block in thread order; `total` gets the sum.
+template <int NT>
+__device__ int bscan_excl(int v, int& total, Shared& sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int inc = v;
 #pragma unroll
@@ -92,29 +95,38 @@ __device__ int block_exclusive_scan(int v, int& total, Shared& sh) {
     const int o = __shfl_up(inc, d, kWave);
     if (lane >= d) inc += o;
   }
+  if (NT == kWave) {
+    total = __shfl(inc, 63, kWave);
+    return inc - v;
+  }
   __syncthreads();
   if (lane == 63) sh.ired[wave] = inc;
   __syncthreads();
   int before = 0;
   total = 0;
-  for (int i = 0; i < kWaves; ++i) {
+#pragma unroll
+  for (int i = 0; i < NT / kWave; ++i) {
     if (i < wave) before += sh.ired[i];
     total += sh.ired[i];
   }
   return before + inc - v;
 }
 
-__global__ __launch_bounds__(kThreads) void k_temporal_budget(const float* __restrict__ rel,
-                                                              const float* __restrict__ delta, int T, int N,
-                                                              long long B, int levels, float tau,
-                                                              int32_t* __restrict__ budget,
-                                                              int32_t* __restrict__ offset,
-                                                              float* __restrict__ rel_rect) {
+// NT threads handle up to TV frames; thread tid owns frames tid*kPer .. tid*kPer+kPer-1.
+template <int NT, int TV>
+__global__ __launch_bounds__(NT) void k_temporal_budget(const float* __restrict__ rel,
+                                                        const float* __restrict__ delta, int T, int N,
+                                                        long long B, int levels, float tau,
+                                                        int32_t* __restrict__ budget,
+                                                        int32_t* __restrict__ offset,
+                                                        float* __restrict__ rel_rect) {
+  constexpr int kPer = (TV + NT - 1) / NT;  // frames per thread (contiguous run)
+  static_assert(kPer <= 32 && TV <= kTMax, "frame mask holds 32 frames per thread");
   __shared__ Shared sh;
   const int tid = threadIdx.x;
   const double inv_sqrt2 = 0.70710678118654752440;
 
-  // ---- gamma = min-max(delta); retained set M --------------------------------
+  // ---- gamma = min-max(delta); retained set M (thread tid owns frames tid*kPer ..) ----
   double dv[kPer], lo = INFINITY, hi = -INFINITY;
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
@@ -122,144 +134,132 @@ __global__ __launch_bounds__(kThreads) void k_temporal_budget(const float* __res
     dv[k] = t < T ? double(delta[t]) : 0.0;
     if (t < T) { lo = fmin(lo, dv[k]); hi = fmax(hi, dv[k]); }
   }
-  lo = block_min_max(lo, false, sh);
-  hi = block_min_max(hi, true, sh);
-  int keep[kPer], cnt = 0;
+  lo = bminmax<NT>(lo, false, sh);
+  hi = bminmax<NT>(hi, true, sh);
+  int cnt = 0;
+  unsigned keep = 0;
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     const int t = tid * kPer + k;
-    keep[k] = t < T && (t == 0 || dv[k] >= double(tau));
-    cnt += keep[k];
+    if (t < T && (t == 0 || dv[k] >= double(tau))) { keep |= 1u << k; ++cnt; }
   }
   int L = 0;
-  int pos = block_exclusive_scan(cnt, L, sh);
+  int pos = bscan_excl<NT>(cnt, L, sh);
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
-    const int t = tid * kPer + k;
-    if (keep[k]) {
+    if (keep & (1u << k)) {
+      const int t = tid * kPer + k;
       sh.idx[pos] = t;
-      sh.a[pos] = double(rel[t]);
-      sh.g[pos] = hi > lo ? (dv[k] - lo) / (hi - lo) : 0.0;
+      sh.a[0][pos] = double(rel[t]);
+      sh.g[0][pos] = hi > lo ? (dv[k] - lo) / (hi - lo) : 0.0;
       ++pos;
     }
   }
   __syncthreads();
 
-  // ---- WTA: J-level gated Haar analysis ---------------------------------------
-  int len = L, doff = 0;
+  // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)) ------------------------
+  int len = L, doff = 0, cur = 0;
   for (int lev = 0; lev < levels; ++lev) {
-    const int half = (len + 1) / 2;  // <= kThreads because L <= kTMax
+    const int half = (len + 1) / 2;
     if (tid == 0) { sh.lens[lev] = len; sh.doffs[lev] = doff; }
-    double A = 0.0, Dg = 0.0, gp = 0.0;
-    if (tid < half) {
-      const int i0 = 2 * tid, i1 = min(2 * tid + 1, len - 1);
-      const double x0 = sh.a[i0], x1 = sh.a[i1];
-      A = (x0 + x1) * inv_sqrt2;
-      const double D = (x0 - x1) * inv_sqrt2;
-      gp = 0.5 * (sh.g[i0] + sh.g[i1]);
-      Dg = gp * D;
+    const double* A0 = sh.a[cur];
+    const double* G0 = sh.g[cur];
+    for (int k = tid; k < half; k += NT) {
+      const int i0 = 2 * k, i1 = min(2 * k + 1, len - 1);
+      const double x0 = A0[i0], x1 = A0[i1];
+      const double gp = 0.5 * (G0[i0] + G0[i1]);
+      sh.a[cur ^ 1][k] = (x0 + x1) * inv_sqrt2;
+      sh.g[cur ^ 1][k] = gp;
+      sh.det[doff + k] = gp * ((x0 - x1) * inv_sqrt2);
     }
     __syncthreads();
-    if (tid < half) { sh.a[tid] = A; sh.g[tid] = gp; sh.det[doff + tid] = Dg; }
-    __syncthreads();
+    cur ^= 1;
     doff += half;
     len = half;
   }
-  // ---- inverse DWT (Eq. (11)) --------------------------------------------------
+  // ---- inverse DWT (Eq. (11)) ---------------------------------------------------
   for (int lev = levels - 1; lev >= 0; --lev) {
     const int plen = sh.lens[lev];
     const int half = (plen + 1) / 2;
-    double e = 0.0, o = 0.0;
-    if (tid < half) {
-      const double A = sh.a[tid], D = sh.det[sh.doffs[lev] + tid];
-      e = (A + D) * inv_sqrt2;
-      o = (A - D) * inv_sqrt2;
+    const double* A0 = sh.a[cur];
+    double* A1 = sh.a[cur ^ 1];
+    for (int k = tid; k < half; k += NT) {
+      const double A = A0[k], D = sh.det[sh.doffs[lev] + k];
+      A1[2 * k] = (A + D) * inv_sqrt2;
+      if (2 * k + 1 < plen) A1[2 * k + 1] = (A - D) * inv_sqrt2;
     }
     __syncthreads();
-    if (tid < half) {
-      sh.a[2 * tid] = e;
-      if (2 * tid + 1 < plen) sh.a[2 * tid + 1] = o;
-    }
-    __syncthreads();
+    cur ^= 1;
   }
+  const double* rt = sh.a[cur];  // r~ over the retained positions
+  double* w = sh.g[cur ^ 1];      // free buffer: weights, then fractional parts
 
-  // ---- budgets (Eq. (16), Eq. (5)) ----------------------------------------------
+  // ---- budgets (Eq. (16), Eq. (5)) ------------------------------------------------
   const long long cap_total = (long long)L * N;
   if (B >= cap_total) {
-    for (int i = tid; i < L; i += kThreads) sh.n[i] = N;
+    for (int i = tid; i < L; i += NT) sh.n[i] = N;
   } else {
     double wsum = 0.0;
-    for (int i = tid; i < L; i += kThreads) {
-      const double w = fmax(sh.a[i], 0.0);
-      sh.w[i] = w;
-      wsum += w;
+    for (int i = tid; i < L; i += NT) {
+      const double wi = fmax(rt[i], 0.0);
+      w[i] = wi;
+      wsum += wi;
     }
-    wsum = block_sum(wsum, sh);
-    for (int i = tid; i < L; i += kThreads) {
-      if (wsum == 0.0) sh.w[i] = 1.0;
-      sh.state[i] = sh.w[i] > 0.0 ? kActive : kIdle;
+    wsum = bsum<NT>(wsum, sh);
+    for (int i = tid; i < L; i += NT) {
+      if (wsum == 0.0) w[i] = 1.0;
+      sh.state[i] = w[i] > 0.0 ? kActive : kIdle;
       sh.n[i] = 0;
     }
     __syncthreads();
     long long R = B;
     while (R > 0) {
       int na = 0;
-      for (int i = tid; i < L; i += kThreads) na += sh.state[i] == kActive;
-      na = block_sum_int(na, sh);
+      for (int i = tid; i < L; i += NT) na += sh.state[i] == kActive;
+      na = bsum_int<NT>(na, sh);
       if (na == 0) {  // every weighted frame is full: spread the rest evenly
-        for (int i = tid; i < L; i += kThreads)
-          if (sh.state[i] != kFull) { sh.state[i] = kActive; sh.w[i] = 1.0; }
+        for (int i = tid; i < L; i += NT)
+          if (sh.state[i] != kFull) { sh.state[i] = kActive; w[i] = 1.0; }
         __syncthreads();
       }
       double S = 0.0;
-      for (int i = tid; i < L; i += kThreads)
-        if (sh.state[i] == kActive) S += sh.w[i];
-      S = block_sum(S, sh);
+      for (int i = tid; i < L; i += NT)
+        if (sh.state[i] == kActive) S += w[i];
+      S = bsum<NT>(S, sh);
       const double Rd = double(R);
       int full = 0;
-      for (int i = tid; i < L; i += kThreads)
-        if (sh.state[i] == kActive && Rd * sh.w[i] / S >= double(N)) ++full;
-      full = block_sum_int(full, sh);
+      for (int i = tid; i < L; i += NT)
+        if (sh.state[i] == kActive && Rd * w[i] / S >= double(N)) ++full;
+      full = bsum_int<NT>(full, sh);
       if (full > 0) {
-        for (int i = tid; i < L; i += kThreads)
-          if (sh.state[i] == kActive && Rd * sh.w[i] / S >= double(N)) { sh.state[i] = kFull; sh.n[i] = N; }
+        for (int i = tid; i < L; i += NT)
+          if (sh.state[i] == kActive && Rd * w[i] / S >= double(N)) { sh.state[i] = kFull; sh.n[i] = N; }
         __syncthreads();
         R -= (long long)full * N;
         continue;
       }
       int base_sum = 0;
-      for (int i = tid; i < L; i += kThreads) {
+      for (int i = tid; i < L; i += NT) {
         if (sh.state[i] == kActive) {
-          const double q = Rd * sh.w[i] / S;
+          const double q = Rd * w[i] / S;
           const double b = floor(q);
           sh.n[i] = int(b);
           base_sum += int(b);
-          sh.w[i] = q - b;  // fractional part from here on
+          w[i] = q - b;  // fractional part from here on
         }
       }
-      const int left = int(R) - block_sum_int(base_sum, sh);
-      // rank of each active frame by (fraction desc, index asc)
-      int plus[kPer];
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) {
-        const int i = tid + k * kThreads;
-        plus[k] = 0;
-        if (i < L && sh.state[i] == kActive) {
-          const double f = sh.w[i];
-          int rank = 0;
-          for (int j = 0; j < L; ++j) {
-            if (sh.state[j] != kActive) continue;
-            const double fj = sh.w[j];
-            rank += (fj > f) || (fj == f && j < i);
-          }
-          plus[k] = rank < left;
+      const int left = int(R) - bsum_int<NT>(base_sum, sh);
+      // +1 for the `left` active frames ranked first by (fraction desc, index asc)
+      for (int i = tid; i < L; i += NT) {
+        if (sh.state[i] != kActive) continue;
+        const double f = w[i];
+        int rank = 0;
+        for (int j = 0; j < L; ++j) {
+          if (sh.state[j] != kActive) continue;
+          const double fj = w[j];
+          rank += (fj > f) || (fj == f && j < i);
         }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) {
-        const int i = tid + k * kThreads;
-        if (i < L) sh.n[i] += plus[k];
+        if (rank < left) sh.n[i] += 1;
       }
       R = 0;
     }
@@ -267,32 +267,32 @@ __global__ __launch_bounds__(kThreads) void k_temporal_budget(const float* __res
   __syncthreads();
 
   // ---- scatter to frames, offsets, rectified relevance ----------------------------
-  for (int t = tid; t < T; t += kThreads) { sh.fb[t] = 0; sh.g[t] = 0.0; }
+  double* rr = w;  // per-frame r~ (weights no longer needed)
+  for (int t = tid; t < T; t += NT) { sh.fb[t] = 0; rr[t] = 0.0; }
   __syncthreads();
-  for (int i = tid; i < L; i += kThreads) {
+  for (int i = tid; i < L; i += NT) {
     const int t = sh.idx[i];
     sh.fb[t] = sh.n[i];
-    sh.g[t] = sh.a[i];
+    rr[t] = rt[i];
   }
   __syncthreads();
-  for (int t = tid; t < T; t += kThreads) {
+  for (int t = tid; t < T; t += NT) {
     budget[t] = sh.fb[t];
-    if (rel_rect) rel_rect[t] = float(sh.g[t]);
+    if (rel_rect) rel_rect[t] = float(rr[t]);
   }
-  int nv[kPer], tsum = 0;
+  int tsum = 0;
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     const int t = tid * kPer + k;
-    nv[k] = t < T ? sh.fb[t] : 0;
-    tsum += nv[k];
+    tsum += t < T ? sh.fb[t] : 0;
   }
   int total = 0;
-  int run = block_exclusive_scan(tsum, total, sh);
+  int run = bscan_excl<NT>(tsum, total, sh);
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     const int t = tid * kPer + k;
     if (t < T) offset[t] = run;
-    run += nv[k];
+    if (t < T) run += sh.fb[t];
   }
   if (tid == 0) offset[T] = total;
 }
@@ -301,8 +301,16 @@ __global__ __launch_bounds__(kThreads) void k_temporal_budget(const float* __res
 
 hipError_t launch_temporal_budget(const wz_config& c, const float* frame_rel, const float* frame_delta,
                                   int32_t* budget, int32_t* offset, float* rel_rect, hipStream_t s) {
-  hipLaunchKernelGGL(k_temporal_budget, dim3(1), dim3(kThreads), 0, s, frame_rel, frame_delta, c.T,
-                     c.H * c.W, (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
+  const int N = c.H * c.W;
+  if (c.T <= 64)
+    hipLaunchKernelGGL((k_temporal_budget<64, 64>), dim3(1), dim3(64), 0, s, frame_rel, frame_delta, c.T, N,
+                       (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
+  else if (c.T <= 256)
+    hipLaunchKernelGGL((k_temporal_budget<256, 256>), dim3(1), dim3(256), 0, s, frame_rel, frame_delta, c.T, N,
+                       (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
+  else
+    hipLaunchKernelGGL((k_temporal_budget<1024, kTMax>), dim3(1), dim3(1024), 0, s, frame_rel, frame_delta, c.T, N,
+                       (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
   return hipGetLastError();
 }
 

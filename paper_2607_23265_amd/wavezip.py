@@ -110,10 +110,11 @@ def workspace_bytes(p: Problem):
 
 
 def new_workspace(p: Problem, device):
+    """A zero-filled workspace (the library keeps its counters at zero between calls)."""
     n = workspace_bytes(p)
     if n == 0:
         raise WZError(3, "wz_workspace_bytes")
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def relevance(p: Problem, X, query, ws=None):

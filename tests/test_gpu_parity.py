@@ -19,6 +19,7 @@ from paper_2607_23265_amd import wavezip as wz
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
+COUNTER_BYTES = 4 * (2048 + 2049)  # leading counters of the workspace
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -70,9 +71,11 @@ def test_benchmarked_launch_bf16_out_and_determinism():
     X, q = wz.to_device(inp, DEV)
     ws = wz.new_workspace(p, DEV)
     first = [t.clone() for t in wz.condense(p, X, q, ws=ws)]
-    ws.fill_(0xA5)  # stale workspace contents must not matter
+    # everything but the leading counters may be stale: scribble over it
+    ws[COUNTER_BYTES:].fill_(0xA5)
     second = wz.condense(p, X, q, ws=ws)
     torch.cuda.synchronize()
+    assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0  # counters are back at zero
     for x, y in zip(first, second):
         assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
                            y.view(torch.int16) if y.dtype == torch.bfloat16 else y)
@@ -102,6 +105,19 @@ def test_stage_temporal_budget(name):
     want_rr = np.zeros(wl.T)
     want_rr[kept] = rt
     assert G.rel_err(_np(rr), want_rr) <= 1e-6
+
+
+def test_workspace_reuse_across_shapes():
+    """One workspace serves calls of different shapes in turn (the counters return to zero)."""
+    big = G.workload_case("t64_14x14_c3584")
+    small = G.workload_case("tiny")
+    ws = wz.new_workspace(wz.problem_of(big[0]), DEV)
+    for wl, inp, out in (big, small, big, small):
+        X, q = wz.to_device(inp, DEV)
+        tok, idx, b, o = wz.condense(wz.problem_of(wl), X, q, ws=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(_np(b), out["budget"]) and np.array_equal(_np(idx), out["index"])
+        assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("T", [1, 2, 3, 1023, 1024, 1025, 2048])
