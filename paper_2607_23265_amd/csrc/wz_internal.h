@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "wavezip.h"
 
 namespace wz {
@@ -36,36 +38,78 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 }
 
 // ---------------------------------------------------------------------------
-// Tiling of the relevance pass: every workgroup owns one tile of up to 32
-// consecutive tokens of one frame and reads all C channels of them.
+// Decomposition of the relevance pass.
+//
+// MFMA path: a workgroup owns one token tile of a frame (up to 256 tokens,
+// one wave per 16-row MFMA tile) and one slice of channels.  Tiles cover whole
+// frames when H*W <= 256, so the query, which every workgroup must read for its
+// channels, is read about once per frame; channel slices give the grid enough
+// workgroups.  Vector-ALU path: tiles of up to 32 tokens, all channels.
 // ---------------------------------------------------------------------------
-constexpr int kXcds = 8;  // MI355X: workgroups are dealt to the 8 XCDs round robin
+constexpr int kXcds = 8;          // MI355X: workgroups are dealt to the 8 XCDs round robin
+constexpr int kCUs = 256;
+constexpr int kMaxWaves = 16;     // 16-row MFMA tiles per token tile
+constexpr int kTilesPerWave = 2;  // 16-row MFMA tiles per wave on the MFMA path
+constexpr int kSliceSteps = 32;   // 32-channel steps per slice at most (the query slice sits in LDS)
+constexpr int kTokMax = 4096;     // validated bound on tokens per frame
 
-struct Tiling {
-  int tiles_per_frame;  // ceil(N / tile_tokens)
-  int tile_tokens;      // tokens per tile (the last tile of a frame may be shorter)
-  int mtiles;           // 16-row MFMA tiles per workgroup tile
-  int grid;             // workgroups: frames rounded up to a multiple of kXcds, times tiles
+// Query columns of the per-slice partial scores, padded for 16-byte rows.
+inline int qpad(int Q) { return (Q + 3) & ~3; }
+
+bool relevance_uses_mfma(const wz_config& c);
+
+struct RelPlan {
+  int tiles;        // token tiles per frame
+  int tile_tokens;  // tokens per tile (the last tile of a frame may be shorter)
+  int mt;           // 16-row MFMA tiles per token tile
+  int slices;       // channel slices
+  int kc;           // channels per slice (a multiple of 32 on the MFMA path)
+  int grid;         // workgroups: frames rounded up to a multiple of kXcds, x tiles x slices
+  int threads;      // threads per workgroup
 };
 
-inline Tiling relevance_tiling(const wz_config& c) {
+inline RelPlan relevance_plan(const wz_config& c) {
   const int N = c.H * c.W;
-  const int cap = 32;  // two 16-row MFMA tiles
-  Tiling t;
-  t.tiles_per_frame = (N + cap - 1) / cap;
-  t.tile_tokens = (N + t.tiles_per_frame - 1) / t.tiles_per_frame;
-  t.mtiles = (t.tile_tokens + 15) / 16;
-  t.grid = (c.T + kXcds - 1) / kXcds * kXcds * t.tiles_per_frame;
-  return t;
+  RelPlan p;
+  if (relevance_uses_mfma(c)) {
+    const int cap = 16 * kMaxWaves;
+    p.tiles = (N + cap - 1) / cap;
+    p.tile_tokens = (N + p.tiles - 1) / p.tiles;
+    p.mt = (p.tile_tokens + 15) / 16;
+    const int ksteps = (c.C + 31) / 32;
+    // slices of at most kSliceSteps steps; more while the grid is short of
+    // one workgroup per CU, keeping slices of at least 8 channel steps and
+    // per-slice partial scores (4*Q bytes a token) under a quarter of X (2*C)
+    const int smin = (ksteps + kSliceSteps - 1) / kSliceSteps;
+    const int smax = std::max(smin, std::min(ksteps / 8, c.C / (8 * c.Q)));
+    int S = smin;
+    while (S < smax && (long long)c.T * p.tiles * S < kCUs) ++S;
+    const int kper = (ksteps + S - 1) / S;
+    p.kc = kper * 32;
+    p.slices = (ksteps + kper - 1) / kper;
+    p.threads = (p.mt + kTilesPerWave - 1) / kTilesPerWave * 64;
+  } else {
+    const int cap = 32;
+    p.tiles = (N + cap - 1) / cap;
+    p.tile_tokens = (N + p.tiles - 1) / p.tiles;
+    p.mt = (p.tile_tokens + 15) / 16;
+    p.slices = 1;
+    p.kc = c.C;
+    p.threads = 256;
+  }
+  p.grid = (c.T + kXcds - 1) / kXcds * kXcds * p.tiles * p.slices;
+  return p;
 }
 
-// Workgroup b handles frame t = (b / kXcds / tiles) * kXcds + b % kXcds and
-// tile (b / kXcds) % tiles, so every tile of a frame runs on the same XCD
-// (its L2 then holds the partial sums the frame's last workgroup combines).
-__device__ __forceinline__ void tile_of_block(int b, int tiles, int& t, int& tile) {
+// Workgroup b works on frame t = (b / kXcds / (tiles*slices)) * kXcds + b % kXcds,
+// so every workgroup of a frame runs on the same XCD.
+__device__ __forceinline__ void unit_of_block(int b, int tiles, int slices, int& t, int& tile, int& slice) {
   const int xcd = b % kXcds, slot = b / kXcds;
-  tile = slot % tiles;
-  t = (slot / tiles) * kXcds + xcd;
+  const int per_frame = tiles * slices;
+  const int r = slot % per_frame;
+  t = (slot / per_frame) * kXcds + xcd;
+  tile = r / slices;
+  slice = r % slices;
 }
 
 // Counters the relevance pass uses to find the last workgroup of a frame and
@@ -73,18 +117,19 @@ __device__ __forceinline__ void tile_of_block(int b, int tiles, int& t, int& til
 // left at zero by every call, and must be zero before the first call.
 constexpr int kMaxFrames = 2048;
 struct Counters {
-  int frame[kMaxFrames];     // tiles of frame t finished
+  int frame[kMaxFrames];     // workgroups of frame t finished
   int pair[kMaxFrames + 1];  // frames t-1, t finished (for delta_t)
 };
 
 // Workspace carve-up (all offsets 256-byte aligned).
 struct Workspace {
   Counters* ctr;       // zero between calls
-  float* pool_part;    // [T][tiles][C]  per-tile channel sums
-  float* sig_part;     // [T][tiles][Q]  per-tile sums of x . q_j
-  float* pooled;       // [T][C]         per-frame channel sums p_t
-  double* pnorm2;      // [T]            |p_t|^2
-  float* rq;           // [Q]            1 / |q_j| (0 for a zero query token)
+  float* s_part;       // [T][slices][N][qpad(Q)] per-slice x . q_j (only with several slices)
+  float* g_part;       // [T][slices][N]          per-slice |x|^2 (only with several slices)
+  float* qg_part;      // [T][slices][Q]          per-slice |q_j|^2
+  float* sig_part;     // [T][tiles][slices][Q]   per-unit sums over tokens of x . q_j
+  float* pool_part;    // [T][tiles][C]           per-tile channel sums
+  double* pn2_part;    // [T][slices]             per-slice |p_t|^2 (one tile per frame)
   float* tok_score;    // [T*N]
   float* frame_rel;    // [T]
   float* frame_delta;  // [T]
@@ -96,17 +141,19 @@ struct Workspace {
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 inline Workspace workspace_layout(const wz_config& c, char* base) {
-  const Tiling tl = relevance_tiling(c);
-  const size_t T = c.T, N = size_t(c.H) * c.W, C = c.C, Q = c.Q, tiles = tl.tiles_per_frame;
+  const RelPlan pl = relevance_plan(c);
+  const size_t T = c.T, N = size_t(c.H) * c.W, C = c.C, Q = c.Q, QP = qpad(c.Q), tiles = pl.tiles,
+               S = pl.slices;
   Workspace w;
   size_t off = 0;
   auto take = [&](size_t bytes) { char* p = base ? base + off : nullptr; off += align256(bytes); return p; };
   w.ctr = reinterpret_cast<Counters*>(take(sizeof(Counters)));
+  w.s_part = reinterpret_cast<float*>(take(S > 1 ? T * S * N * QP * 4 : 0));
+  w.g_part = reinterpret_cast<float*>(take(S > 1 ? T * S * N * 4 : 0));
+  w.qg_part = reinterpret_cast<float*>(take(T * S * Q * 4));
+  w.sig_part = reinterpret_cast<float*>(take(T * tiles * S * Q * 4));
   w.pool_part = reinterpret_cast<float*>(take(T * tiles * C * 4));
-  w.sig_part = reinterpret_cast<float*>(take(T * tiles * Q * 4));
-  w.pooled = reinterpret_cast<float*>(take(T * C * 4));
-  w.pnorm2 = reinterpret_cast<double*>(take(T * 8));
-  w.rq = reinterpret_cast<float*>(take(Q * 4));
+  w.pn2_part = reinterpret_cast<double*>(take(T * S * 8));
   w.tok_score = reinterpret_cast<float*>(take(T * N * 4));
   w.frame_rel = reinterpret_cast<float*>(take(T * 4));
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
