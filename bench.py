@@ -111,7 +111,8 @@ def main():
     wall = time.perf_counter() - t0
     ms_step = ev0.elapsed_time(ev1) / args.steps
 
-    # dominant kernel: the relevance pass, launched alone back to back on the same stream
+    # dominant stage: wz_relevance (the pass over X and the per-frame kernel), called alone
+    # back to back on the same stream
     a = torch.empty(wl.T * wl.N, dtype=torch.float32, device=dev)
     r = torch.empty(wl.T, dtype=torch.float32, device=dev)
     d = torch.empty(wl.T, dtype=torch.float32, device=dev)
@@ -162,7 +163,8 @@ def main():
         "hbm_frac": call_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": call_bytes,
         "wall_s": wall,
-        "roofline": {"kernel": "relevance pass (wz_relevance)", "bound": "hbm", "achieved": k1_gbps,
+        "roofline": {"kernel": "stage 1, wz_relevance: streaming pass k_relevance_mfma + per-frame k_frame",
+                     "bound": "hbm", "achieved": k1_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k1_gbps / HBM_PEAK_GBPS,
                      "traffic": None, "bytes_per_launch": k1_bytes, "us_per_launch": k1_ms * 1e3},
     }

@@ -81,14 +81,11 @@ typedef struct {
   float tau;          /* frame-filter threshold on delta; 0 keeps every frame  */
 } wz_config;
 
-/* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`
- * (0 if cfg is invalid).  The workspace holds per-tile partial sums, the
- * intermediate scores and, in its first bytes, the counters with which the
- * relevance kernel finds the last workgroup of each frame.  Zero-fill a
- * workspace once before its first use; every call leaves those counters at
- * zero again, so the same workspace can be reused by later calls of any cfg
- * (one call at a time per workspace).  Apart from the counters, contents on
- * entry are ignored.                                                          */
+/* Bytes of device workspace that wz_relevance, wz_spatial_dwt_condense and
+ * wz_condense need for `cfg` (0 if cfg is invalid): per-unit partial sums of
+ * the streaming pass, the intermediate scores, selection ranks, saliency maps
+ * and budgets.  Contents on entry are ignored; one call at a time per
+ * workspace.                                                                  */
 size_t wz_workspace_bytes(const wz_config* cfg);
 
 /* Stage 1 -- Cross-Modal Scorer (similarity branch, Sec. 3.2.1) and Visual
@@ -97,9 +94,10 @@ size_t wz_workspace_bytes(const wz_config* cfg);
  *   frame_rel[t]         = r_t = max_j cos(v_t, q_j)                  [T]
  *   frame_delta[t]       = delta_t = clamp(1 - cos(v_t, v_{t-1}), 0, 2),
  *                          delta_0 = 0                                  [T]
- * where v_t is the spatial mean of frame t's tokens.  Accumulation is fp32.
- * ws: at least wz_workspace_bytes(cfg) bytes of device memory, zero-filled
- * before its first use (see wz_workspace_bytes).  One kernel launch.       */
+ * where v_t is the spatial mean of frame t's tokens.  Accumulation is fp32,
+ * the frame-level cosines fp64.  ws: at least wz_workspace_bytes(cfg) bytes
+ * of device memory.  Two kernel launches: one pass over X writing per-unit
+ * partials, then one workgroup per frame adding them in a fixed order.      */
 wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
                        float* tok_score, float* frame_rel, float* frame_delta,
                        void* ws, size_t ws_bytes, void* stream);
@@ -119,24 +117,26 @@ wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel,
                              int32_t* offset, float* rel_rect, void* stream);
 
 /* Stage 3 -- Wavelet Spatial Modulator and Token Assigner (Eq. (7),
- * Eq. (12)-(15), Eq. (19)).  For every frame with budget[t] > 0: M_t =
- * min-max(tok_score of frame t); keep the budget[t] tokens of largest score
- * (ties -> smaller index); for each kept token take its 2x2 Haar block of the
- * grid (last row/column repeated when H or W is odd), compute LL/LH/HL/HH,
- * multiply the three detail bands by g = lambda_ * mean(M over the block),
- * invert, and write the token's reconstructed features to row offset[t] + k
- * of out_tokens ([offset[T]][C], cfg->out_dtype), k = the token's rank in
- * raster order among the frame's kept tokens; out_index gets its flat index.
- * Rows from offset[T] on are not written.  budget/offset must satisfy
- * 0 <= budget[t] <= H*W and offset = exclusive prefix sum of budget (as
- * produced by wz_temporal_budget); out_tokens must hold offset[T] <= B rows.  */
+ * Eq. (12)-(15), Eq. (19)).  Frame t keeps n_t = offset[t+1] - offset[t]
+ * tokens: M_t = min-max(tok_score of frame t); keep the n_t tokens of largest
+ * score (ties -> smaller index); for each kept token take its 2x2 Haar block
+ * of the grid (last row/column repeated when H or W is odd), compute
+ * LL/LH/HL/HH, multiply the three detail bands by g = lambda_ * mean(M over
+ * the block), invert, and write the token's reconstructed features to row
+ * offset[t] + k of out_tokens ([B][C], cfg->out_dtype), k = the token's rank
+ * in raster order among the frame's kept tokens; out_index gets its flat
+ * index.  offset ([T+1], as produced by wz_temporal_budget) must start at 0,
+ * be nondecreasing with steps of at most H*W and end at offset[T] <= B; rows
+ * from offset[T] on are not written.  ws: at least wz_workspace_bytes(cfg)
+ * bytes (holds the selection ranks and saliency maps; contents on entry
+ * ignored).  Two kernel launches.                                            */
 wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X,
-                                  const float* tok_score, const int32_t* budget,
-                                  const int32_t* offset, void* out_tokens,
-                                  int32_t* out_index, void* stream);
+                                  const float* tok_score, const int32_t* offset,
+                                  void* out_tokens, int32_t* out_index,
+                                  void* ws, size_t ws_bytes, void* stream);
 
 /* The whole pass C(X, Q) of Eq. (4)/(6): stage 1, 2 and 3 in sequence on one
- * stream, intermediates kept in `ws`.  out_tokens [B][C] (cfg->out_dtype) and
+ * stream (four kernel launches), intermediates kept in `ws`.  out_tokens [B][C] (cfg->out_dtype) and
  * out_index [B] receive offset[T] rows (= B unless the frame filter leaves
  * fewer than B tokens).  budget [T] and offset [T+1] are optional outputs
  * (NULL: kept in the workspace).                                              */

@@ -74,8 +74,9 @@ wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query, f
   if (!ws) return WZ_ERR_NULL;
   const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
   if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
-  return from_hip(launch_relevance(*cfg, X, query, tok_score, frame_rel, frame_delta, w,
-                                   static_cast<hipStream_t>(stream)));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, tok_score, w, s)));
+  return from_hip(launch_frame(*cfg, w, tok_score, frame_rel, frame_delta, true, s));
 }
 
 wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const float* frame_delta,
@@ -91,19 +92,22 @@ wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const
 }
 
 wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const float* tok_score,
-                                  const int32_t* budget, const int32_t* offset, void* out_tokens,
-                                  int32_t* out_index, void* stream) {
+                                  const int32_t* offset, void* out_tokens, int32_t* out_index, void* ws,
+                                  size_t ws_bytes, void* stream) {
   WZ_TRY(check_config(cfg));
   WZ_TRY(check_ptr(X, 16));
   WZ_TRY(check_ptr(tok_score, 4));
-  WZ_TRY(check_ptr(budget, 4));
   WZ_TRY(check_ptr(offset, 4));
   if (cfg->B > 0) {
     WZ_TRY(check_ptr(out_tokens, 16));
     WZ_TRY(check_ptr(out_index, 4));
   }
-  return from_hip(launch_spatial_condense(*cfg, X, tok_score, budget, offset, out_tokens, out_index,
-                                          static_cast<hipStream_t>(stream)));
+  if (!ws) return WZ_ERR_NULL;
+  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
+  if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  WZ_TRY(from_hip(launch_frame(*cfg, w, const_cast<float*>(tok_score), nullptr, nullptr, false, s)));
+  return from_hip(launch_spatial_gather(*cfg, X, w.rank, w.sal, offset, out_tokens, out_index, s));
 }
 
 wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
@@ -124,9 +128,10 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, vo
   hipStream_t s = static_cast<hipStream_t>(stream);
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
-  WZ_TRY(from_hip(launch_relevance(*cfg, X, query, w.tok_score, w.frame_rel, w.frame_delta, w, s)));
+  WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s)));
+  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s)));
   WZ_TRY(from_hip(launch_temporal_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s)));
-  return from_hip(launch_spatial_condense(*cfg, X, w.tok_score, bud, off, out_tokens, out_index, s));
+  return from_hip(launch_spatial_gather(*cfg, X, w.rank, w.sal, off, out_tokens, out_index, s));
 }
 
 }  // extern "C"

@@ -1,0 +1,62 @@
+// Device helpers shared by the gfx950 kernels: raw buffer-resource accesses.
+#pragma once
+
+#include "wz_internal.h"
+
+namespace wz {
+
+// Buffer-resource accesses: an offset at or past the resource's size reads
+// zeros / drops the write without touching memory, so pad rows and ragged
+// edges need no branch (a branch around a load makes the compiler wait for
+// every load in flight before the branch joins).
+constexpr int kOOB = 0x40000000;       // byte offset beyond any resource here
+constexpr int kBufWord3 = 0x00020000;  // gfx9-family raw buffer descriptor word 3
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), kBufWord3);
+}
+__device__ __forceinline__ bf16x8 buf_load_bf16x8(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ u32x4 buf_load_u32x4(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+__device__ __forceinline__ f32x4 buf_load_f32x4(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float buf_load_f32(__amdgpu_buffer_rsrc_t r, int off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ int buf_load_i32(__amdgpu_buffer_rsrc_t r, int off) {
+  return int(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ void buf_store_f32(float v, __amdgpu_buffer_rsrc_t r, int off) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, off, 0, 0);
+}
+
+// Sum over the four 16-lane rows of a wave, every lane getting the total of
+// its column (lane & 15): ((row0 + row1) + (row2 + row3)).  gfx950's lane
+// swaps do it in the vector ALU, without the LDS crossbar.
+__device__ __forceinline__ float row_sum4(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);  // rows (0+1, 0+1, 2+3, 2+3)
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Selection key of token n with score a: larger a ranks first, then the
+// smaller index, so distinct tokens never tie.  The score maps onto the upper
+// 32 bits order-preservingly, the complemented index onto the lower 12 bits
+// (n < 4096).
+__device__ __forceinline__ uint32_t order_key(float a) {
+  const uint32_t u = __float_as_uint(a);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float order_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+__device__ __forceinline__ uint64_t sel_key(float a, int n) {
+  return (uint64_t(order_key(a)) << 12) | uint64_t(kTokMax - 1 - n);
+}
+
+}  // namespace wz

@@ -112,25 +112,18 @@ __device__ __forceinline__ void unit_of_block(int b, int tiles, int slices, int&
   slice = r % slices;
 }
 
-// Counters the relevance pass uses to find the last workgroup of a frame and
-// of a pair of adjacent frames.  They sit at the start of the workspace, are
-// left at zero by every call, and must be zero before the first call.
 constexpr int kMaxFrames = 2048;
-struct Counters {
-  int frame[kMaxFrames];     // workgroups of frame t finished
-  int pair[kMaxFrames + 1];  // frames t-1, t finished (for delta_t)
-};
 
 // Workspace carve-up (all offsets 256-byte aligned).
 struct Workspace {
-  Counters* ctr;       // zero between calls
   float* s_part;       // [T][slices][N][qpad(Q)] per-slice x . q_j (only with several slices)
   float* g_part;       // [T][slices][N]          per-slice |x|^2 (only with several slices)
   float* qg_part;      // [T][slices][Q]          per-slice |q_j|^2
   float* sig_part;     // [T][tiles][slices][Q]   per-unit sums over tokens of x . q_j
   float* pool_part;    // [T][tiles][C]           per-tile channel sums
-  double* pn2_part;    // [T][slices]             per-slice |p_t|^2 (one tile per frame)
   float* tok_score;    // [T*N]
+  int32_t* rank;       // [T*N]                   selection rank of each token in its frame
+  float* sal;          // [T*N]                   saliency map M
   float* frame_rel;    // [T]
   float* frame_delta;  // [T]
   int32_t* budget;     // [T]
@@ -147,14 +140,14 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   Workspace w;
   size_t off = 0;
   auto take = [&](size_t bytes) { char* p = base ? base + off : nullptr; off += align256(bytes); return p; };
-  w.ctr = reinterpret_cast<Counters*>(take(sizeof(Counters)));
   w.s_part = reinterpret_cast<float*>(take(S > 1 ? T * S * N * QP * 4 : 0));
   w.g_part = reinterpret_cast<float*>(take(S > 1 ? T * S * N * 4 : 0));
   w.qg_part = reinterpret_cast<float*>(take(T * S * Q * 4));
   w.sig_part = reinterpret_cast<float*>(take(T * tiles * S * Q * 4));
   w.pool_part = reinterpret_cast<float*>(take(T * tiles * C * 4));
-  w.pn2_part = reinterpret_cast<double*>(take(T * S * 8));
   w.tok_score = reinterpret_cast<float*>(take(T * N * 4));
+  w.rank = reinterpret_cast<int32_t*>(take(T * N * 4));
+  w.sal = reinterpret_cast<float*>(take(T * N * 4));
   w.frame_rel = reinterpret_cast<float*>(take(T * 4));
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
   w.budget = reinterpret_cast<int32_t*>(take(T * 4));
@@ -164,12 +157,17 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
 }
 
 // Kernel launchers (each returns hipGetLastError() of its launches).
-hipError_t launch_relevance(const wz_config& c, const void* X, const void* query, float* tok_score,
-                            float* frame_rel, float* frame_delta, const Workspace& ws, hipStream_t s);
+// Streaming pass of stage 1: per-unit partials into ws (and a_{t,n} into
+// tok_score when there is one channel slice).
+hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void* query, float* tok_score,
+                                   const Workspace& ws, hipStream_t s);
+// Per-frame kernel: with finish, a_{t,n} (several slices), r_t and delta_t
+// from the partials; always the selection ranks and saliency maps of tok_score.
+hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
+                        float* frame_delta, bool finish, hipStream_t s);
 hipError_t launch_temporal_budget(const wz_config& c, const float* frame_rel, const float* frame_delta,
                                   int32_t* budget, int32_t* offset, float* rel_rect, hipStream_t s);
-hipError_t launch_spatial_condense(const wz_config& c, const void* X, const float* tok_score,
-                                   const int32_t* budget, const int32_t* offset, void* out_tokens,
-                                   int32_t* out_index, hipStream_t s);
+hipError_t launch_spatial_gather(const wz_config& c, const void* X, const int32_t* rank, const float* sal,
+                                 const int32_t* offset, void* out_tokens, int32_t* out_index, hipStream_t s);
 
 }  // namespace wz

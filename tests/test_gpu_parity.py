@@ -19,7 +19,6 @@ from paper_2607_23265_amd import wavezip as wz
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-COUNTER_BYTES = 4 * (2048 + 2049)  # leading counters of the workspace
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -70,12 +69,11 @@ def test_benchmarked_launch_bf16_out_and_determinism():
     p = wz.problem_of(wl, wz.WZ_BF16)
     X, q = wz.to_device(inp, DEV)
     ws = wz.new_workspace(p, DEV)
+    ws.fill_(0x5A)  # workspace contents on entry are ignored
     first = [t.clone() for t in wz.condense(p, X, q, ws=ws)]
-    # everything but the leading counters may be stale: scribble over it
-    ws[COUNTER_BYTES:].fill_(0xA5)
+    ws.fill_(0xA5)
     second = wz.condense(p, X, q, ws=ws)
     torch.cuda.synchronize()
-    assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0  # counters are back at zero
     for x, y in zip(first, second):
         assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
                            y.view(torch.int16) if y.dtype == torch.bfloat16 else y)
@@ -108,7 +106,7 @@ def test_stage_temporal_budget(name):
 
 
 def test_workspace_reuse_across_shapes():
-    """One workspace serves calls of different shapes in turn (the counters return to zero)."""
+    """One workspace serves calls of different shapes in turn."""
     big = G.workload_case("t64_14x14_c3584")
     small = G.workload_case("tiny")
     ws = wz.new_workspace(wz.problem_of(big[0]), DEV)
@@ -117,7 +115,6 @@ def test_workspace_reuse_across_shapes():
         tok, idx, b, o = wz.condense(wz.problem_of(wl), X, q, ws=ws)
         torch.cuda.synchronize()
         assert np.array_equal(_np(b), out["budget"]) and np.array_equal(_np(idx), out["index"])
-        assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("T", [1, 2, 3, 1023, 1024, 1025, 2048])
@@ -172,9 +169,8 @@ def test_stage_spatial_condense(name, out_dtype):
         toks.append(mod[sel])
         idxs.append(t * wl.N + sel)
     want_tok, want_idx = np.concatenate(toks), np.concatenate(idxs)
-    budget = torch.from_numpy(out["budget"].astype(np.int32)).to(DEV)
     offset = torch.from_numpy(out["offset"].astype(np.int32)).to(DEV)
-    tok, idx = wz.spatial_dwt_condense(p, X, torch.from_numpy(a32.ravel()).to(DEV), budget, offset)
+    tok, idx = wz.spatial_dwt_condense(p, X, torch.from_numpy(a32.ravel()).to(DEV), offset)
     torch.cuda.synchronize()
     n = len(want_idx)
     assert np.array_equal(_np(idx)[:n], want_idx)
