@@ -14,6 +14,7 @@ algorithmic HBM rate of the whole call, the roofline of the dominant kernel
 rate on the host as a reported baseline.
 """
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -37,6 +38,9 @@ def parse():
     ap.add_argument("--out-dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle (0 disables)")
+    ap.add_argument("--copy-calib", type=int, default=0,
+                    help="only run this many plain device copies of a frame tensor (the known-size kernel that "
+                         "scales HBM byte counters) and exit")
     return ap.parse_args()
 
 
@@ -44,6 +48,32 @@ def algorithmic_bytes(wl, out_bytes):
     """Bytes the pass must move per call: frames read once, query, condensed rows, indices, budgets."""
     s_in = 2 if wl.dtype == "bf16" else 4
     return (wl.T * wl.N * wl.C * s_in + wl.Q * wl.C * s_in + wl.B * wl.C * out_bytes + 4 * wl.B + 4 * wl.T)
+
+
+def kernel_sources_sha256():
+    """Digest of the kernel and C-ABI sources, to tell whether recorded counters still describe them."""
+    h = hashlib.sha256()
+    csrc = os.path.join("paper_2607_23265_amd", "csrc")
+    files = sorted([os.path.join(csrc, f) for f in os.listdir(os.path.join(HERE, csrc)) if f.endswith((".hip", ".h"))] +
+                   [os.path.join("include", f) for f in os.listdir(os.path.join(HERE, "include")) if f.endswith(".h")])
+    for f in files:
+        h.update(f.encode())
+        with open(os.path.join(HERE, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload):
+    """HBM bytes per wz_relevance call measured with rocprofv3 byte counters (profiles/), or None when
+    there is no record for the workload or the kernels changed since it was taken."""
+    path = os.path.join(HERE, "profiles", f"stage1_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("kernel_sources_sha256") != kernel_sources_sha256():
+        return None
+    return rec["traffic_bytes_per_launch"]
 
 
 def relevance_bytes(wl):
@@ -94,6 +124,14 @@ def main():
     nsets = max(1, math.ceil(2 * MALL_BYTES / X0.numel() / X0.element_size()))
     Xs = [X0] + [X0.clone() for _ in range(nsets - 1)]
     qs = [q0] + [q0.clone() for _ in range(nsets - 1)]
+    if args.copy_calib:
+        dst = [torch.empty_like(X0) for _ in range(2)]
+        for i in range(args.copy_calib):
+            dst[i % 2].copy_(Xs[i % nsets])
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_read": X0.numel() * X0.element_size(),
+                          "bytes_written": X0.numel() * X0.element_size(), "copies": args.copy_calib}), flush=True)
+        return
     ws = wz.new_workspace(p, dev)
     out = wz._out_tokens(p, dev)
     stream = torch.cuda.current_stream(dev)
@@ -166,7 +204,8 @@ def main():
         "roofline": {"kernel": "stage 1, wz_relevance: streaming pass k_relevance_mfma + per-frame k_frame",
                      "bound": "hbm", "achieved": k1_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k1_gbps / HBM_PEAK_GBPS,
-                     "traffic": None, "bytes_per_launch": k1_bytes, "us_per_launch": k1_ms * 1e3},
+                     "traffic": recorded_traffic(wl.name), "bytes_per_launch": k1_bytes,
+                     "us_per_launch": k1_ms * 1e3},
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_seconds)
