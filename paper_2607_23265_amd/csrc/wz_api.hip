@@ -76,7 +76,7 @@ wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query, f
   if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, tok_score, w, s)));
-  return from_hip(launch_frame(*cfg, w, tok_score, frame_rel, frame_delta, true, s));
+  return from_hip(launch_frame_scores(*cfg, w, tok_score, frame_rel, frame_delta, s));
 }
 
 wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const float* frame_delta,
@@ -87,8 +87,8 @@ wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const
   WZ_TRY(check_ptr(budget, 4));
   WZ_TRY(check_ptr(offset, 4));
   if (rel_rect && !aligned(rel_rect, 4)) return WZ_ERR_ALIGN;
-  return from_hip(launch_temporal_budget(*cfg, frame_rel, frame_delta, budget, offset, rel_rect,
-                                         static_cast<hipStream_t>(stream)));
+  return from_hip(launch_budget_select(*cfg, frame_rel, frame_delta, budget, offset, rel_rect, nullptr, nullptr,
+                                       nullptr, static_cast<hipStream_t>(stream)));
 }
 
 wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const float* tok_score,
@@ -106,7 +106,8 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
   const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
   if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  WZ_TRY(from_hip(launch_frame(*cfg, w, const_cast<float*>(tok_score), nullptr, nullptr, false, s)));
+  WZ_TRY(from_hip(launch_budget_select(*cfg, nullptr, nullptr, nullptr, nullptr, nullptr, tok_score, w.rank, w.sal,
+                                       s)));
   return from_hip(launch_spatial_gather(*cfg, X, w.rank, w.sal, offset, out_tokens, out_index, s));
 }
 
@@ -129,8 +130,9 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, vo
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s)));
-  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s)));
-  WZ_TRY(from_hip(launch_temporal_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s)));
+  WZ_TRY(from_hip(launch_frame_scores(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, s)));
+  WZ_TRY(from_hip(launch_budget_select(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, w.tok_score, w.rank,
+                                       w.sal, s)));
   return from_hip(launch_spatial_gather(*cfg, X, w.rank, w.sal, off, out_tokens, out_index, s));
 }
 

@@ -161,12 +161,14 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
 // tok_score when there is one channel slice).
 hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void* query, float* tok_score,
                                    const Workspace& ws, hipStream_t s);
-// Per-frame kernel: with finish, a_{t,n} (several slices), r_t and delta_t
-// from the partials; always the selection ranks and saliency maps of tok_score.
-hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
-                        float* frame_delta, bool finish, hipStream_t s);
-hipError_t launch_temporal_budget(const wz_config& c, const float* frame_rel, const float* frame_delta,
-                                  int32_t* budget, int32_t* offset, float* rel_rect, hipStream_t s);
+// Per-frame finish of stage 1: a_{t,n} (several slices), r_t and delta_t.
+hipError_t launch_frame_scores(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
+                               float* frame_delta, hipStream_t s);
+// Budgets (when frame_rel is given) and the per-frame selection ranks and
+// saliency maps (when tok_score is given), in one launch.
+hipError_t launch_budget_select(const wz_config& c, const float* frame_rel, const float* frame_delta,
+                                int32_t* budget, int32_t* offset, float* rel_rect, const float* tok_score,
+                                int32_t* rank, float* sal, hipStream_t s);
 hipError_t launch_spatial_gather(const wz_config& c, const void* X, const int32_t* rank, const float* sal,
                                  const int32_t* offset, void* out_tokens, int32_t* out_index, hipStream_t s);
 

@@ -179,13 +179,20 @@ __global__ __launch_bounds__(kMaxWaves / kTilesPerWave * 64) void k_relevance_mf
         if (lane < 32) s_poolw[wave][ks * kKStep + lane] = lane < 16 ? v0 : v1;
       }
     };
+    // Steps 2s and 2s+1 read the two 64-byte halves of the same 128-byte
+    // line of each row, so they are consumed and re-issued as a pair: the
+    // second request of a line then finds the first one's miss in flight
+    // instead of a line the cache may have evicted meanwhile.
+    static_assert(R % 2 == 0, "the ring advances in pairs of steps");
     auto run = [&](auto pool) {
       for (int ks0 = 0; ks0 < kper; ks0 += R) {
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < R; r += 2) {
           const int ks = ks0 + r;
           if (ks < kper) compute(ks, a[r], pool);
+          if (ks + 1 < kper) compute(ks + 1, a[r + 1], pool);
           issue(ks + R, a[r]);
+          issue(ks + 1 + R, a[r + 1]);
         }
       }
     };

@@ -1,6 +1,6 @@
 // Stage 2: Wavelet Temporal Allocator (Sec. 3.2.2 gate and frame filter,
-// Eq. (9)-(11)) and the integer frame budgets (Eq. (16) under Eq. (5)), plus
-// the per-frame preparation of the token selection.
+// Eq. (9)-(11)) and the integer frame budgets (Eq. (16) under Eq. (5)).  The
+// same launch also prepares stage 3's per-frame selection (below).
 //
 // The budget is a few fp64 operations per frame, so it runs in ONE workgroup
 // with every array in LDS: one wave when T <= 64 (no cross-wave
@@ -16,7 +16,7 @@
 //            fractional parts (ties: smaller frame index); uniform weights if
 //            every w is 0; every frame full when B >= |M| * H * W.
 
-#include "wz_internal.h"
+#include "wz_device.h"
 
 namespace wz {
 namespace {
@@ -318,13 +318,6 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
   if (tid == 0) offset[T] = total;
 }
 
-template <int NT, int TV>
-__global__ __launch_bounds__(NT) void k_temporal_budget(const float* __restrict__ rel, const float* __restrict__ delta,
-                                                        int T, int N, long long B, int levels, float tau,
-                                                        int32_t* __restrict__ budget, int32_t* __restrict__ offset,
-                                                        float* __restrict__ rel_rect) {
-  budget_body<NT, TV>(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
-}
 
 // ---------------------------------------------------------------------------
 // T <= 64: one wave, frame t (then retained position i) in lane t (lane i),
@@ -380,12 +373,9 @@ __device__ __forceinline__ int wave_reduce_sum_i32(int v) {
          (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
 }
 
-__global__ __launch_bounds__(kWave) void k_temporal_budget_wave(const float* __restrict__ rel,
-                                                                const float* __restrict__ delta, int T, int N,
-                                                                long long B, int levels, float tau,
-                                                                int32_t* __restrict__ budget,
-                                                                int32_t* __restrict__ offset,
-                                                                float* __restrict__ rel_rect) {
+__device__ void budget_wave_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
+                                 long long B, int levels, float tau, int32_t* __restrict__ budget,
+                                 int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
   const double inv_sqrt2 = 0.70710678118654752440;
   auto dmin = [](double a, double b) { return fmin(a, b); };
   auto dmax = [](double a, double b) { return fmax(a, b); };
@@ -459,18 +449,33 @@ __global__ __launch_bounds__(kWave) void k_temporal_budget_wave(const float* __r
       }
       const double b = floor(q);
       if (act) n = int(b);
-      const double frac = act ? q - b : -1.0;  // below every fractional part when not active
-      const int left = int(R) - wave_reduce_sum_i32(act ? int(b) : 0);
-      // +1 for the `left` active positions ranked first by (fraction desc,
-      // index asc): each lane compares itself with the 63 others in turn
-      int rank = 0;
-#pragma unroll 8
-      for (int s = 1; s < kWave; ++s) {
-        const int j = (lane + s) & (kWave - 1);
-        const double fj = __shfl(frac, j, kWave);
-        rank += (fj > frac) || (fj == frac && j < lane);
+      const double frac = act ? q - b : 0.0;  // in [0, 1) for active positions
+      int need = int(R) - wave_reduce_sum_i32(act ? int(b) : 0);
+      // +1 for the `need` active positions ranked first by (fraction desc,
+      // index asc).  Non-negative doubles order like their bit patterns, so a
+      // descent over the bits (fractions below 1 leave bits 63 and 62 clear)
+      // finds them: positions with the current bit set are taken whole while
+      // they fit, else the search continues among them; positions still tied
+      // after the last bit go by index.
+      const uint64_t fb = __builtin_bit_cast(uint64_t, frac);
+      uint64_t cand = active, chosen = 0;
+      for (int bit = 61; bit >= 0 && need > 0; --bit) {
+        if (__popcll(cand) <= need) break;
+        const uint64_t ones = cand & __ballot((fb >> bit) & 1ull);
+        const int c1 = __popcll(ones);
+        if (c1 <= need) {
+          chosen |= ones;
+          need -= c1;
+          cand &= ~ones;
+        } else {
+          cand = ones;
+        }
       }
-      if (act && rank < left) n += 1;
+      for (; need > 0 && cand; --need) {  // the remaining candidates all fit, or are exact ties
+        chosen |= cand & (~cand + 1ull);
+        cand &= cand - 1ull;
+      }
+      if ((chosen >> lane) & 1ull) n += 1;
       R = 0;
     }
   }
@@ -493,20 +498,125 @@ __global__ __launch_bounds__(kWave) void k_temporal_budget_wave(const float* __r
   if (lane == T - 1) offset[T] = incl;
 }
 
+// ---------------------------------------------------------------------------
+// Selection preparation of frame t (stage 3, Eq. (7) and the selection that
+// replaces Eq. (17)):
+//   rank[t][n] = number of the frame's tokens with a larger score a (ties:
+//                the smaller index ranks first), so that a frame's n_t kept
+//                tokens are those of rank < n_t whatever n_t turns out to be;
+//   sal[t][n]  = M_t = min-max of the frame's scores (0 if all are equal).
+// ---------------------------------------------------------------------------
+template <int NTH>
+__device__ void frame_select(int t, int N, const float* __restrict__ tok_score, int32_t* __restrict__ rank,
+                             float* __restrict__ sal) {
+  constexpr int NW = NTH / kWave, AV = kTokMax / NTH;
+  __shared__ uint64_t s_key[kTokMax];
+  __shared__ float s_mm[2][NW];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const __amdgpu_buffer_rsrc_t ares = make_rsrc(tok_score + size_t(t) * N, uint32_t(N) * 4);
+  float av[AV];
+#pragma unroll
+  for (int i = 0; i < AV; ++i) {
+    const int n = tid + i * NTH;
+    av[i] = buf_load_f32(ares, n < N ? n * 4 : kOOB);
+  }
+  float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < AV; ++i) {
+    const int n = tid + i * NTH;
+    if (n < N) {
+      s_key[n] = sel_key(av[i], n);
+      lo = fminf(lo, av[i]);
+      hi = fmaxf(hi, av[i]);
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    lo = fminf(lo, __shfl_xor(lo, m, kWave));
+    hi = fmaxf(hi, __shfl_xor(hi, m, kWave));
+  }
+  if (lane == 0) {
+    s_mm[0][wave] = lo;
+    s_mm[1][wave] = hi;
+  }
+  __syncthreads();
+  lo = s_mm[0][0];
+  hi = s_mm[1][0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) {
+    lo = fminf(lo, s_mm[0][w]);
+    hi = fmaxf(hi, s_mm[1][w]);
+  }
+  const float range = hi - lo;
+  // tpt consecutive lanes share a token, each counting the keys of one part
+  // of the frame (read as near-broadcasts, 16 per step)
+  const int tpt = N * 8 <= NTH ? 8 : N * 4 <= NTH ? 4 : N * 2 <= NTH ? 2 : 1;
+  const int part = tid % tpt, per_round = NTH / tpt;
+  const int jlen = (N + tpt - 1) / tpt, jb = min(N, part * jlen), je = min(N, jb + jlen);
+  for (int n0 = 0; n0 < N; n0 += per_round) {
+    const int n = n0 + tid / tpt;
+    int r = 0;
+    uint64_t kn = 0;
+    if (n < N) {
+      kn = s_key[n];
+      int j = jb;
+      for (; j + 16 <= je; j += 16) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) r += s_key[j + e] > kn;
+      }
+      for (; j < je; ++j) r += s_key[j] > kn;
+    }
+    for (int m = 1; m < tpt; m <<= 1) r += __shfl_xor(r, m, kWave);
+    if (n < N && part == 0) {
+      rank[size_t(t) * N + n] = r;
+      const float a = order_value(uint32_t(kn >> 12));
+      sal[size_t(t) * N + n] = range > 0.f ? (a - lo) / range : 0.f;
+    }
+  }
+}
+
+// Workgroup 0 computes the budgets when do_budget (a one-wave body on wave
+// 0, which never waits at a barrier); the others prepare the selection of
+// frame blockIdx.x - do_budget.  Both only read stage 1's outputs, so they
+// run side by side.
+template <int NT, int TV, int NTH>
+__global__ __launch_bounds__(NTH) void k_budget_select(const float* __restrict__ rel,
+                                                       const float* __restrict__ delta, int T, int N, long long B,
+                                                       int levels, float tau, int32_t* __restrict__ budget,
+                                                       int32_t* __restrict__ offset, float* __restrict__ rel_rect,
+                                                       const float* __restrict__ tok_score,
+                                                       int32_t* __restrict__ rank, float* __restrict__ sal,
+                                                       int do_budget) {
+  if (do_budget && blockIdx.x == 0) {
+    if (int(threadIdx.x) < NT) {
+      if constexpr (NT == kWave) budget_wave_body(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
+      else budget_body<NT, TV>(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
+    }
+    return;
+  }
+  frame_select<NTH>(int(blockIdx.x) - do_budget, N, tok_score, rank, sal);
+}
+
+template <int NT, int TV, int NTH>
+void launch_bs(const wz_config& c, const float* rel, const float* delta, int32_t* budget, int32_t* offset,
+               float* rel_rect, const float* tok_score, int32_t* rank, float* sal, hipStream_t s) {
+  const int do_budget = rel != nullptr;
+  const int grid = do_budget + (tok_score ? c.T : 0);
+  hipLaunchKernelGGL((k_budget_select<NT, TV, NTH>), dim3(grid), dim3(NTH), 0, s, rel, delta, c.T, c.H * c.W,
+                     (long long)c.B, c.levels, c.tau, budget, offset, rel_rect, tok_score, rank, sal, do_budget);
+}
+
 }  // namespace
 
-hipError_t launch_temporal_budget(const wz_config& c, const float* frame_rel, const float* frame_delta,
-                                  int32_t* budget, int32_t* offset, float* rel_rect, hipStream_t s) {
-  const int N = c.H * c.W;
-  if (c.T <= 64)
-    hipLaunchKernelGGL(k_temporal_budget_wave, dim3(1), dim3(kWave), 0, s, frame_rel, frame_delta, c.T, N,
-                       (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
+hipError_t launch_budget_select(const wz_config& c, const float* frame_rel, const float* frame_delta,
+                                int32_t* budget, int32_t* offset, float* rel_rect, const float* tok_score,
+                                int32_t* rank, float* sal, hipStream_t s) {
+  if (c.T <= 64)  // one-wave budget: the selection workgroups can use 1024 threads
+    launch_bs<kWave, 64, 1024>(c, frame_rel, frame_delta, budget, offset, rel_rect, tok_score, rank, sal, s);
   else if (c.T <= 256)
-    hipLaunchKernelGGL((k_temporal_budget<256, 256>), dim3(1), dim3(256), 0, s, frame_rel, frame_delta, c.T, N,
-                       (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
+    launch_bs<256, 256, 256>(c, frame_rel, frame_delta, budget, offset, rel_rect, tok_score, rank, sal, s);
   else
-    hipLaunchKernelGGL((k_temporal_budget<1024, kTMax>), dim3(1), dim3(1024), 0, s, frame_rel, frame_delta, c.T, N,
-                       (long long)c.B, c.levels, c.tau, budget, offset, rel_rect);
+    launch_bs<1024, kTMax, 1024>(c, frame_rel, frame_delta, budget, offset, rel_rect, tok_score, rank, sal, s);
   return hipGetLastError();
 }
 
