@@ -1,9 +1,9 @@
-// Per-frame finish of stage 1, T x kChunks workgroups.  Workgroup (t, q)
-// adds the channel slices' partial dot products of the q-th quarter of frame
-// t's tokens in slice order and forms
+// Per-frame finish of stage 1, T x (kChunks + 1) workgroups.  Workgroup
+// (t, q < kChunks) adds the channel slices' partial dot products of the q-th
+// quarter of frame t's tokens in slice order and forms
 //   a_{t,n} = max_j (sum_s S_s[n][j]) / (|q_j| |x_n|)     (several slices;
 //             with one slice the streaming pass wrote a_{t,n} itself),
-// and workgroup (t, 0) also forms
+// and workgroup (t, kChunks) forms
 //   r_t     = max_j sigma_j / (|q_j| |p_t|),  sigma_j = p_t . q_j   (Sec. 3.2.1)
 //   delta_t = clamp(1 - p_t . p_{t-1} / (|p_t| |p_{t-1}|), 0, 2), delta_0 = 0
 //             (Sec. 3.2.2, Eq. (8); the mean's cosine is the sum's)
@@ -42,11 +42,11 @@ __global__ __launch_bounds__(kThreads) void k_frame_scores(const FrameArgs f) {
   __shared__ uint32_t s_best[kTokMax / kChunks];
   __shared__ double s_red[4][NW];
 
-  const int t = blockIdx.x / kChunks, q = blockIdx.x % kChunks;
+  const int t = blockIdx.x / (kChunks + 1), q = blockIdx.x % (kChunks + 1);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int N = f.N, C = f.C, Q = f.Q, QP = f.QP, S = f.slices, tiles = f.tiles, K = tiles * S, C4 = C / 4;
-  const int per = (N + kChunks - 1) / kChunks, n0 = min(N, q * per), NQ = min(N, n0 + per) - n0;
-  const bool lead = q == 0;  // this workgroup also forms r_t and delta_t
+  const bool lead = q == kChunks;  // this workgroup forms r_t and delta_t (and no scores)
+  const int per = (N + kChunks - 1) / kChunks, n0 = lead ? 0 : min(N, q * per), NQ = lead ? 0 : min(N, n0 + per) - n0;
   const bool scores = S > 1;
   const int G4 = QP / 4, units = NQ * G4;
 
@@ -204,7 +204,7 @@ hipError_t launch_frame_scores(const wz_config& c, const Workspace& ws, float* t
   const RelPlan pl = relevance_plan(c);
   const FrameArgs fa{ws.s_part, ws.g_part, ws.qg_part, ws.sig_part, ws.pool_part, tok_score, frame_rel, frame_delta,
                      c.T,       c.H * c.W, c.C,        c.Q,         qpad(c.Q),    pl.tiles,  pl.slices};
-  hipLaunchKernelGGL(k_frame_scores, dim3(c.T * kChunks), dim3(kThreads), 0, s, fa);
+  hipLaunchKernelGGL(k_frame_scores, dim3(c.T * (kChunks + 1)), dim3(kThreads), 0, s, fa);
   return hipGetLastError();
 }
 

@@ -201,10 +201,11 @@ void launch_typed(const wz_config& c, const void* X, const int32_t* rank, const 
 #define WZ_GATHER(U)                                                                                       \
   hipLaunchKernelGGL((k_spatial_gather<In, Out, U, FC>), grid, block, 0, s, x, rank, sal, offset, c.T, c.H, \
                      c.W, c.C, (long long)c.B, c.lambda_, o, out_index)
+  // at most 4 vectors per lane and row in flight: deeper batches of every
+  // wave's four rows overfill the CU's L1 with misses and run slower
   if (vec_per_lane <= 1) WZ_GATHER(1);
   else if (vec_per_lane <= 2) WZ_GATHER(2);
-  else if (vec_per_lane <= 4) WZ_GATHER(4);
-  else WZ_GATHER(8);
+  else WZ_GATHER(4);
 #undef WZ_GATHER
 }
 
