@@ -201,7 +201,7 @@ def main():
         "hbm_frac": call_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": call_bytes,
         "wall_s": wall,
-        "roofline": {"kernel": "stage 1, wz_relevance: streaming pass k_relevance_mfma + per-frame k_frame",
+        "roofline": {"kernel": "stage 1, wz_relevance: streaming pass k_relevance_mfma + per-frame k_frame_scores",
                      "bound": "hbm", "achieved": k1_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k1_gbps / HBM_PEAK_GBPS,
                      "traffic": recorded_traffic(wl.name), "bytes_per_launch": k1_bytes,

@@ -97,7 +97,7 @@ size_t wz_workspace_bytes(const wz_config* cfg);
  * where v_t is the spatial mean of frame t's tokens.  Accumulation is fp32,
  * the frame-level cosines fp64.  ws: at least wz_workspace_bytes(cfg) bytes
  * of device memory.  Two kernel launches: one pass over X writing per-unit
- * partials, then four workgroups per frame adding them in a fixed order.    */
+ * partials, then five workgroups per frame adding them in a fixed order.    */
 wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
                        float* tok_score, float* frame_rel, float* frame_delta,
                        void* ws, size_t ws_bytes, void* stream);

@@ -223,6 +223,8 @@ EDGE = {
     "lambda_zero": dict(T=4, H=4, W=4, C=64, Q=16, B=20, lam=0.0),
     "large_grid": dict(T=2, H=64, W=64, C=8, Q=16, B=3000),
     "many_frames": dict(T=512, H=2, W=2, C=16, Q=16, B=1900),
+    "max_channels": dict(T=2, H=7, W=7, C=65536, Q=16, B=20),
+    "max_query": dict(T=3, H=7, W=7, C=256, Q=1024, B=30),
 }
 
 
