@@ -15,6 +15,15 @@ constexpr int kBufWord3 = 0x00020000;  // gfx9-family raw buffer descriptor word
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), kBufWord3);
 }
+// Same, with base and size passed through readfirstlane: for values the
+// compiler cannot prove wave-uniform, a descriptor in VGPRs would turn every
+// access into a waterfall loop.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_uniform(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(a)), hi = __builtin_amdgcn_readfirstlane(uint32_t(a >> 32));
+  const void* p = reinterpret_cast<const void*>((uint64_t(hi) << 32) | lo);
+  return make_rsrc(p, __builtin_amdgcn_readfirstlane(bytes));
+}
 __device__ __forceinline__ bf16x8 buf_load_bf16x8(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
@@ -42,6 +51,26 @@ __device__ __forceinline__ float row_sum4(float v) {
   v = __uint_as_float(a[0]) + __uint_as_float(a[1]);  // rows (0+1, 0+1, 2+3, 2+3)
   const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Workgroup barrier that orders LDS only.  __syncthreads() also waits for
+// every outstanding global load and store of the wave (vmcnt(0)); this one
+// leaves them in flight, which a streaming kernel needs to keep its prefetch
+// ring going across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Sum over the 16 lanes of each row of a wave (every lane gets its row's
+// total), in a fixed order, by DPP: quad swaps, then the two row mirrors.
+__device__ __forceinline__ float row_sum16(float v) {
+  v += __uint_as_float(__builtin_amdgcn_update_dpp(0, __float_as_uint(v), 0xB1, 0xF, 0xF, false));   // lane ^ 1
+  v += __uint_as_float(__builtin_amdgcn_update_dpp(0, __float_as_uint(v), 0x4E, 0xF, 0xF, false));   // lane ^ 2
+  v += __uint_as_float(__builtin_amdgcn_update_dpp(0, __float_as_uint(v), 0x141, 0xF, 0xF, false));  // 7 - i in 8
+  v += __uint_as_float(__builtin_amdgcn_update_dpp(0, __float_as_uint(v), 0x140, 0xF, 0xF, false));  // 15 - i in 16
+  return v;
 }
 
 // Selection key of token n with score a: larger a ranks first, then the

@@ -40,11 +40,11 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 // ---------------------------------------------------------------------------
 // Decomposition of the relevance pass.
 //
-// MFMA path: a workgroup owns one token tile of a frame (up to 256 tokens,
-// one wave per 16-row MFMA tile) and one slice of channels.  Tiles cover whole
-// frames when H*W <= 256, so the query, which every workgroup must read for its
-// channels, is read about once per frame; channel slices give the grid enough
-// workgroups.  Vector-ALU path: tiles of up to 32 tokens, all channels.
+// MFMA paths: a workgroup owns one token tile of a frame (up to 256 tokens)
+// and one slice of channels.  Tiles cover whole frames when H*W <= 256, so the
+// query, which every workgroup must read for its channels, is read about once
+// per frame; channel slices give the grid enough workgroups.  Vector-ALU path:
+// tiles of up to 32 tokens, all channels.
 // ---------------------------------------------------------------------------
 constexpr int kXcds = 8;          // MI355X: workgroups are dealt to the 8 XCDs round robin
 constexpr int kCUs = 256;
@@ -56,22 +56,61 @@ constexpr int kTokMax = 4096;     // validated bound on tokens per frame
 // Query columns of the per-slice partial scores, padded for 16-byte rows.
 inline int qpad(int Q) { return (Q + 3) & ~3; }
 
-bool relevance_uses_mfma(const wz_config& c);
+// Streaming kernels of the relevance pass, chosen by shape:
+//   kRelLds  bf16, Q <= 32: coalesced loads transposed through LDS, MFMA;
+//   kRelMfma bf16, Q > 32, frames of >= 49 tokens: MFMA-layout loads;
+//   kRelValu everything else (fp32 inputs, small frames with many queries).
+enum RelKind { kRelValu = 0, kRelMfma = 1, kRelLds = 2 };
+RelKind relevance_kind(const wz_config& c);
+
+// LDS-transpose kernel limits: up to 8 waves of 32 tokens per tile; a slice
+// is whole 128-channel chunks, with the query slice (Q padded to 16 or 32)
+// resident in LDS.
+constexpr int kLdsChunk = 128;        // channels per chunk (256 bytes of a bf16 row)
+constexpr int kLdsWavesMax = 8;
+constexpr int kLdsSliceMax1 = 1024;   // slice channels at most, queries of <= 16 tokens
+constexpr int kLdsSliceMax2 = 896;    // ... of 17..32 tokens
 
 struct RelPlan {
+  RelKind kind;
   int tiles;        // token tiles per frame
   int tile_tokens;  // tokens per tile (the last tile of a frame may be shorter)
-  int mt;           // 16-row MFMA tiles per token tile
+  int mt;           // 16-row MFMA tiles per token tile (kRelMfma)
   int slices;       // channel slices
-  int kc;           // channels per slice (a multiple of 32 on the MFMA path)
+  int kc;           // channels per slice
   int grid;         // workgroups: frames rounded up to a multiple of kXcds, x tiles x slices
   int threads;      // threads per workgroup
+  int ipc;          // kRelLds: load instructions per chunk and wave (rows per wave / 4)
+  int ntg;          // kRelLds: 16-column query tiles
 };
 
 inline RelPlan relevance_plan(const wz_config& c) {
   const int N = c.H * c.W;
-  RelPlan p;
-  if (relevance_uses_mfma(c)) {
+  RelPlan p{};
+  p.kind = relevance_kind(c);
+  if (p.kind == kRelLds) {
+    const int cap = 32 * kLdsWavesMax;
+    p.tiles = (N + cap - 1) / cap;
+    p.tile_tokens = (N + p.tiles - 1) / p.tiles;
+    const int nw = (p.tile_tokens + 31) / 32;
+    const int per = (p.tile_tokens + nw - 1) / nw;
+    p.ipc = per <= 28 ? 7 : 8;
+    p.threads = nw * 64;
+    p.ntg = c.Q <= 16 ? 1 : 2;
+    p.mt = 0;
+    const int chunks = (c.C + kLdsChunk - 1) / kLdsChunk;
+    const int cmax = (p.ntg == 1 ? kLdsSliceMax1 : kLdsSliceMax2) / kLdsChunk;
+    // fewest slices the LDS allows; more while the grid is short of one
+    // workgroup per CU, keeping per-slice partial scores (4*Q bytes a
+    // token) under a quarter of X (2*C bytes a token)
+    const int qp = (c.Q + 3) & ~3;
+    const int smax = std::max(1, c.C / (8 * qp));
+    int S = (chunks + cmax - 1) / cmax;
+    while (S < chunks && S < smax && (long long)c.T * p.tiles * S < kCUs) ++S;
+    const int cps = (chunks + S - 1) / S;
+    p.kc = cps * kLdsChunk;
+    p.slices = (chunks + cps - 1) / cps;
+  } else if (p.kind == kRelMfma) {
     const int cap = 16 * kMaxWaves;
     p.tiles = (N + cap - 1) / cap;
     p.tile_tokens = (N + p.tiles - 1) / p.tiles;
