@@ -81,10 +81,9 @@ typedef struct {
   float tau;          /* frame-filter threshold on delta; 0 keeps every frame  */
 } wz_config;
 
-/* Bytes of device workspace that wz_relevance, wz_spatial_dwt_condense and
- * wz_condense need for `cfg` (0 if cfg is invalid): per-unit partial sums of
- * the streaming pass, the intermediate scores, selection ranks, saliency maps
- * and budgets.  Contents on entry are ignored; one call at a time per
+/* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`
+ * (0 if cfg is invalid): per-unit partial sums of the streaming pass, the
+ * intermediate scores and frame values, and budgets.  Contents on entry are ignored; one call at a time per
  * workspace.                                                                  */
 size_t wz_workspace_bytes(const wz_config* cfg);
 
@@ -127,16 +126,18 @@ wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel,
  * in raster order among the frame's kept tokens; out_index gets its flat
  * index.  offset ([T+1], as produced by wz_temporal_budget) must start at 0,
  * be nondecreasing with steps of at most H*W and end at offset[T] <= B; rows
- * from offset[T] on are not written.  ws: at least wz_workspace_bytes(cfg)
- * bytes (holds the selection ranks and saliency maps; contents on entry
- * ignored).  Two kernel launches.                                            */
+ * from offset[T] on are not written, and no row outside [0, B) is ever
+ * written whatever offset holds.  Needs no workspace.  One kernel launch.    */
 wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X,
                                   const float* tok_score, const int32_t* offset,
                                   void* out_tokens, int32_t* out_index,
-                                  void* ws, size_t ws_bytes, void* stream);
+                                  void* stream);
 
 /* The whole pass C(X, Q) of Eq. (4)/(6): stage 1, 2 and 3 in sequence on one
- * stream (four kernel launches), intermediates kept in `ws`.  out_tokens [B][C] (cfg->out_dtype) and
+ * stream, intermediates kept in `ws`.  Three kernel launches: the pass over
+ * X, the per-frame scores, and one kernel that computes the budgets (every
+ * workgroup alike) and performs stage 3; for T > 256 the budgets get a
+ * launch of their own.  out_tokens [B][C] (cfg->out_dtype) and
  * out_index [B] receive offset[T] rows (= B unless the frame filter leaves
  * fewer than B tokens).  budget [T] and offset [T+1] are optional outputs
  * (NULL: kept in the workspace).                                              */

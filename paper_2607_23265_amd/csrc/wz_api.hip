@@ -87,13 +87,12 @@ wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const
   WZ_TRY(check_ptr(budget, 4));
   WZ_TRY(check_ptr(offset, 4));
   if (rel_rect && !aligned(rel_rect, 4)) return WZ_ERR_ALIGN;
-  return from_hip(launch_budget_select(*cfg, frame_rel, frame_delta, budget, offset, rel_rect, nullptr, nullptr,
-                                       nullptr, static_cast<hipStream_t>(stream)));
+  return from_hip(launch_budget(*cfg, frame_rel, frame_delta, budget, offset, rel_rect,
+                                static_cast<hipStream_t>(stream)));
 }
 
 wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const float* tok_score,
-                                  const int32_t* offset, void* out_tokens, int32_t* out_index, void* ws,
-                                  size_t ws_bytes, void* stream) {
+                                  const int32_t* offset, void* out_tokens, int32_t* out_index, void* stream) {
   WZ_TRY(check_config(cfg));
   WZ_TRY(check_ptr(X, 16));
   WZ_TRY(check_ptr(tok_score, 4));
@@ -102,13 +101,8 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
     WZ_TRY(check_ptr(out_tokens, 16));
     WZ_TRY(check_ptr(out_index, 4));
   }
-  if (!ws) return WZ_ERR_NULL;
-  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
-  if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  WZ_TRY(from_hip(launch_budget_select(*cfg, nullptr, nullptr, nullptr, nullptr, nullptr, tok_score, w.rank, w.sal,
-                                       s)));
-  return from_hip(launch_spatial_gather(*cfg, X, w.rank, w.sal, offset, out_tokens, out_index, s));
+  return from_hip(launch_assign_gather(*cfg, X, tok_score, nullptr, nullptr, offset, nullptr, nullptr, out_tokens,
+                                       out_index, static_cast<hipStream_t>(stream)));
 }
 
 wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
@@ -127,13 +121,16 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, vo
   const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
   if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  int32_t* bud = budget ? budget : w.budget;
-  int32_t* off = offset ? offset : w.offset;
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s)));
   WZ_TRY(from_hip(launch_frame_scores(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, s)));
-  WZ_TRY(from_hip(launch_budget_select(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, w.tok_score, w.rank,
-                                       w.sal, s)));
-  return from_hip(launch_spatial_gather(*cfg, X, w.rank, w.sal, off, out_tokens, out_index, s));
+  if (cfg->T <= kFusedTMax)  // budgets computed inside the selection kernel
+    return from_hip(launch_assign_gather(*cfg, X, w.tok_score, w.frame_rel, w.frame_delta, nullptr, budget, offset,
+                                         out_tokens, out_index, s));
+  int32_t* bud = budget ? budget : w.budget;
+  int32_t* off = offset ? offset : w.offset;
+  WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s)));
+  return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, nullptr, nullptr, out_tokens,
+                                       out_index, s));
 }
 
 }  // extern "C"

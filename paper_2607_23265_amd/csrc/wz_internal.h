@@ -152,6 +152,7 @@ __device__ __forceinline__ void unit_of_block(int b, int tiles, int slices, int&
 }
 
 constexpr int kMaxFrames = 2048;
+constexpr int kFusedTMax = 256;  // frames up to which the budget is folded into the selection kernel
 
 // Workspace carve-up (all offsets 256-byte aligned).
 struct Workspace {
@@ -161,8 +162,6 @@ struct Workspace {
   float* sig_part;     // [T][tiles][slices][Q]   per-unit sums over tokens of x . q_j
   float* pool_part;    // [T][tiles][C]           per-tile channel sums
   float* tok_score;    // [T*N]
-  int32_t* rank;       // [T*N]                   selection rank of each token in its frame
-  float* sal;          // [T*N]                   saliency map M
   float* frame_rel;    // [T]
   float* frame_delta;  // [T]
   int32_t* budget;     // [T]
@@ -185,8 +184,6 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   w.sig_part = reinterpret_cast<float*>(take(T * tiles * S * Q * 4));
   w.pool_part = reinterpret_cast<float*>(take(T * tiles * C * 4));
   w.tok_score = reinterpret_cast<float*>(take(T * N * 4));
-  w.rank = reinterpret_cast<int32_t*>(take(T * N * 4));
-  w.sal = reinterpret_cast<float*>(take(T * N * 4));
   w.frame_rel = reinterpret_cast<float*>(take(T * 4));
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
   w.budget = reinterpret_cast<int32_t*>(take(T * 4));
@@ -203,12 +200,18 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
 // Per-frame finish of stage 1: a_{t,n} (several slices), r_t and delta_t.
 hipError_t launch_frame_scores(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
                                float* frame_delta, hipStream_t s);
-// Budgets (when frame_rel is given) and the per-frame selection ranks and
-// saliency maps (when tok_score is given), in one launch.
-hipError_t launch_budget_select(const wz_config& c, const float* frame_rel, const float* frame_delta,
-                                int32_t* budget, int32_t* offset, float* rel_rect, const float* tok_score,
-                                int32_t* rank, float* sal, hipStream_t s);
-hipError_t launch_spatial_gather(const wz_config& c, const void* X, const int32_t* rank, const float* sal,
-                                 const int32_t* offset, void* out_tokens, int32_t* out_index, hipStream_t s);
+// Budgets alone, in one workgroup (wz_temporal_budget, and wz_condense when
+// T > kFusedTMax).
+hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float* frame_delta, int32_t* budget,
+                         int32_t* offset, float* rel_rect, hipStream_t s);
+// Selection, spatial modulation and compaction.  With offset_in the frames'
+// row offsets are given; without it (T <= kFusedTMax) every workgroup computes
+// the budgets from frame_rel and frame_delta itself and workgroup 0 writes
+// them to budget_out / offset_out when those are not null.
+hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* tok_score, const float* frame_rel,
+                                const float* frame_delta, const int32_t* offset_in, int32_t* budget_out,
+                                int32_t* offset_out, void* out_tokens, int32_t* out_index, hipStream_t s);
+// Workgroups per frame of launch_assign_gather.
+int assign_groups_per_frame(const wz_config& c);
 
 }  // namespace wz

@@ -1,622 +1,36 @@
-// Stage 2: Wavelet Temporal Allocator (Sec. 3.2.2 gate and frame filter,
-// Eq. (9)-(11)) and the integer frame budgets (Eq. (16) under Eq. (5)).  The
-// same launch also prepares stage 3's per-frame selection (below).
-//
-// The budget is a few fp64 operations per frame, so it runs in ONE workgroup
-// with every array in LDS: one wave when T <= 64 (no cross-wave
-// synchronisation at all), 256 threads up to T = 256, 1024 beyond.  Steps:
-//   gamma  = min-max(delta) over all T frames (0 if all equal);
-//   M      = {0} U {t >= 1 : delta_t >= tau}, compacted in temporal order;
-//   WTA    = J levels of orthonormal Haar analysis of r over M (odd lengths
-//            repeat the last sample), detail level j multiplied by gamma
-//            pair-averaged j times, then synthesis back to length |M|;
-//   budget = capped largest remainder on w = max(r~, 0): quotas
-//            R * w_m / sum(w); frames reaching H*W are fixed there and the
-//            rest re-apportioned; leftover tokens go to the largest
-//            fractional parts (ties: smaller frame index); uniform weights if
-//            every w is 0; every frame full when B >= |M| * H * W.
-
-#include "wz_device.h"
+// Stage 2 on its own: the Wavelet Temporal Allocator (Sec. 3.2.2 gate and
+// frame filter, Eq. (9)-(11)) and the integer frame budgets (Eq. (16) under
+// Eq. (5)) in ONE workgroup: one wave when T <= 64, 256 threads up to
+// T = 256, 1024 beyond.  The arithmetic lives in wz_budget.h, which the fused
+// selection and gather kernel runs too.
+#include "wz_budget.h"
 
 namespace wz {
 namespace {
 
-constexpr int kTMax = kMaxFrames;
-constexpr int kMaxLevels = 16;
-
-enum : unsigned char { kIdle = 0, kActive = 1, kFull = 2 };
-
-template <int TV>
-struct Shared {
-  double a[2][TV];              // approximation (ping-pong), then r~ in a[0]
-  double g[2][TV];              // gate pooled alongside (ping-pong); g[0] reused for weights
-  double det[TV + kMaxLevels];  // gated detail coefficients of every level
-  int idx[TV];                  // frame index of each retained position
-  int n[TV];                    // budget of each retained position
-  int fb[TV];                   // budget of each frame
-  unsigned char state[TV];
-  double dred[16];
-  int ired[16];
-  int lens[kMaxLevels];
-  int doffs[kMaxLevels];
-};
-
-// Block-wide ordering point of the budget body: a barrier for several waves;
-// one wave only needs its LDS accesses kept in program order.
-template <int NT>
-__device__ __forceinline__ void bsync() {
-  if constexpr (NT > kWave) {
-    __syncthreads();
-  } else {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-  }
-}
-
-template <int NT, typename Sh>
-__device__ double bsum(double v, Sh& sh) {
-  v = wave_sum_f64(v);
-  if (NT == kWave) return v;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sh.dred[wave] = v;
-  __syncthreads();
-  double s = 0.0;
-#pragma unroll
-  for (int i = 0; i < NT / kWave; ++i) s += sh.dred[i];
-  return s;
-}
-
-template <int NT, typename Sh>
-__device__ double bminmax(double v, bool want_max, Sh& sh) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const double o = __shfl_xor(v, m, kWave);
-    v = want_max ? fmax(v, o) : fmin(v, o);
-  }
-  if (NT == kWave) return v;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sh.dred[wave] = v;
-  __syncthreads();
-  double r = sh.dred[0];
-#pragma unroll
-  for (int i = 1; i < NT / kWave; ++i) r = want_max ? fmax(r, sh.dred[i]) : fmin(r, sh.dred[i]);
-  return r;
-}
-
-template <int NT, typename Sh>
-__device__ int bsum_int(int v, Sh& sh) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
-  if (NT == kWave) return v;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) sh.ired[wave] = v;
-  __syncthreads();
-  int s = 0;
-#pragma unroll
-  for (int i = 0; i < NT / kWave; ++i) s += sh.ired[i];
-  return s;
-}
-
-// Exclusive prefix sum over the block in thread order; `total` gets the sum.
-template <int NT, typename Sh>
-__device__ int bscan_excl(int v, int& total, Sh& sh) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int inc = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int o = __shfl_up(inc, d, kWave);
-    if (lane >= d) inc += o;
-  }
-  if (NT == kWave) {
-    total = __shfl(inc, 63, kWave);
-    return inc - v;
-  }
-  __syncthreads();
-  if (lane == 63) sh.ired[wave] = inc;
-  __syncthreads();
-  int before = 0;
-  total = 0;
-#pragma unroll
-  for (int i = 0; i < NT / kWave; ++i) {
-    if (i < wave) before += sh.ired[i];
-    total += sh.ired[i];
-  }
-  return before + inc - v;
-}
-
-// NT threads handle up to TV frames; thread tid owns frames tid*kPer .. tid*kPer+kPer-1.
 template <int NT, int TV>
-__device__ void budget_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
-                            long long B, int levels, float tau, int32_t* __restrict__ budget,
-                            int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
-  constexpr int kPer = (TV + NT - 1) / NT;  // frames per thread (contiguous run)
-  static_assert(kPer <= 32 && TV <= kTMax, "frame mask holds 32 frames per thread");
-  __shared__ Shared<TV> sh;
-  const int tid = threadIdx.x;
-  const double inv_sqrt2 = 0.70710678118654752440;
-
-  // ---- gamma = min-max(delta); retained set M (thread tid owns frames tid*kPer ..) ----
-  double dv[kPer], rv[kPer], lo = INFINITY, hi = -INFINITY;
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int t = tid * kPer + k;
-    dv[k] = t < T ? double(delta[t]) : 0.0;
-    rv[k] = t < T ? double(rel[t]) : 0.0;
-    if (t < T) { lo = fmin(lo, dv[k]); hi = fmax(hi, dv[k]); }
-  }
-  lo = bminmax<NT>(lo, false, sh);
-  hi = bminmax<NT>(hi, true, sh);
-  int cnt = 0;
-  unsigned keep = 0;
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int t = tid * kPer + k;
-    if (t < T && (t == 0 || dv[k] >= double(tau))) { keep |= 1u << k; ++cnt; }
-  }
-  int L = 0;
-  int pos = bscan_excl<NT>(cnt, L, sh);
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    if (keep & (1u << k)) {
-      const int t = tid * kPer + k;
-      sh.idx[pos] = t;
-      sh.a[0][pos] = rv[k];
-      sh.g[0][pos] = hi > lo ? (dv[k] - lo) / (hi - lo) : 0.0;
-      ++pos;
-    }
-  }
-  bsync<NT>();
-
-  // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)) ------------------------
-  int len = L, doff = 0, cur = 0;
-  for (int lev = 0; lev < levels; ++lev) {
-    const int half = (len + 1) / 2;
-    if (tid == 0) { sh.lens[lev] = len; sh.doffs[lev] = doff; }
-    const double* A0 = sh.a[cur];
-    const double* G0 = sh.g[cur];
-    for (int k = tid; k < half; k += NT) {
-      const int i0 = 2 * k, i1 = min(2 * k + 1, len - 1);
-      const double x0 = A0[i0], x1 = A0[i1];
-      const double gp = 0.5 * (G0[i0] + G0[i1]);
-      sh.a[cur ^ 1][k] = (x0 + x1) * inv_sqrt2;
-      sh.g[cur ^ 1][k] = gp;
-      sh.det[doff + k] = gp * ((x0 - x1) * inv_sqrt2);
-    }
-    bsync<NT>();
-    cur ^= 1;
-    doff += half;
-    len = half;
-  }
-  // ---- inverse DWT (Eq. (11)) ---------------------------------------------------
-  for (int lev = levels - 1; lev >= 0; --lev) {
-    const int plen = sh.lens[lev];
-    const int half = (plen + 1) / 2;
-    const double* A0 = sh.a[cur];
-    double* A1 = sh.a[cur ^ 1];
-    for (int k = tid; k < half; k += NT) {
-      const double A = A0[k], D = sh.det[sh.doffs[lev] + k];
-      A1[2 * k] = (A + D) * inv_sqrt2;
-      if (2 * k + 1 < plen) A1[2 * k + 1] = (A - D) * inv_sqrt2;
-    }
-    bsync<NT>();
-    cur ^= 1;
-  }
-  const double* rt = sh.a[cur];  // r~ over the retained positions
-  double* w = sh.g[cur ^ 1];      // free buffer: weights, then fractional parts
-
-  // ---- budgets (Eq. (16), Eq. (5)) ------------------------------------------------
-  const long long cap_total = (long long)L * N;
-  if (B >= cap_total) {
-    for (int i = tid; i < L; i += NT) sh.n[i] = N;
-  } else {
-    double wsum = 0.0;
-    for (int i = tid; i < L; i += NT) {
-      const double wi = fmax(rt[i], 0.0);
-      w[i] = wi;
-      wsum += wi;
-    }
-    wsum = bsum<NT>(wsum, sh);
-    for (int i = tid; i < L; i += NT) {
-      if (wsum == 0.0) w[i] = 1.0;
-      sh.state[i] = w[i] > 0.0 ? kActive : kIdle;
-      sh.n[i] = 0;
-    }
-    bsync<NT>();
-    long long R = B;
-    while (R > 0) {
-      int na = 0;
-      for (int i = tid; i < L; i += NT) na += sh.state[i] == kActive;
-      na = bsum_int<NT>(na, sh);
-      if (na == 0) {  // every weighted frame is full: spread the rest evenly
-        for (int i = tid; i < L; i += NT)
-          if (sh.state[i] != kFull) { sh.state[i] = kActive; w[i] = 1.0; }
-        bsync<NT>();
-      }
-      double S = 0.0;
-      for (int i = tid; i < L; i += NT)
-        if (sh.state[i] == kActive) S += w[i];
-      S = bsum<NT>(S, sh);
-      const double Rd = double(R);
-      int full = 0;
-      for (int i = tid; i < L; i += NT)
-        if (sh.state[i] == kActive && Rd * w[i] / S >= double(N)) ++full;
-      full = bsum_int<NT>(full, sh);
-      if (full > 0) {
-        for (int i = tid; i < L; i += NT)
-          if (sh.state[i] == kActive && Rd * w[i] / S >= double(N)) { sh.state[i] = kFull; sh.n[i] = N; }
-        bsync<NT>();
-        R -= (long long)full * N;
-        continue;
-      }
-      int base_sum = 0;
-      for (int i = tid; i < L; i += NT) {
-        if (sh.state[i] == kActive) {
-          const double q = Rd * w[i] / S;
-          const double b = floor(q);
-          sh.n[i] = int(b);
-          base_sum += int(b);
-          w[i] = q - b;  // fractional part from here on (in [0, 1))
-        } else {
-          w[i] = -1.0;  // below every fractional part: never ranks ahead
-        }
-      }
-      const int left = int(R) - bsum_int<NT>(base_sum, sh);
-      // +1 for the `left` active frames ranked first by (fraction desc, index asc)
-      for (int i = tid; i < L; i += NT) {
-        if (sh.state[i] != kActive) continue;
-        const double f = w[i];
-        int rank = 0, j = 0;
-        for (; j + 8 <= L; j += 8) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const double fj = w[j + e];
-            rank += (fj > f) || (fj == f && j + e < i);
-          }
-        }
-        for (; j < L; ++j) {
-          const double fj = w[j];
-          rank += (fj > f) || (fj == f && j < i);
-        }
-        if (rank < left) sh.n[i] += 1;
-      }
-      R = 0;
-    }
-  }
-  bsync<NT>();
-
-  // ---- scatter to frames, offsets, rectified relevance ----------------------------
-  double* rr = w;  // per-frame r~ (weights no longer needed)
-  for (int t = tid; t < T; t += NT) { sh.fb[t] = 0; rr[t] = 0.0; }
-  bsync<NT>();
-  for (int i = tid; i < L; i += NT) {
-    const int t = sh.idx[i];
-    sh.fb[t] = sh.n[i];
-    rr[t] = rt[i];
-  }
-  bsync<NT>();
-  for (int t = tid; t < T; t += NT) {
-    budget[t] = sh.fb[t];
-    if (rel_rect) rel_rect[t] = float(rr[t]);
-  }
-  int tsum = 0;
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int t = tid * kPer + k;
-    tsum += t < T ? sh.fb[t] : 0;
-  }
-  int total = 0;
-  int run = bscan_excl<NT>(tsum, total, sh);
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int t = tid * kPer + k;
-    if (t < T) offset[t] = run;
-    if (t < T) run += sh.fb[t];
-  }
-  if (tid == 0) offset[T] = total;
+__global__ __launch_bounds__(NT) void k_budget(const float* __restrict__ rel, const float* __restrict__ delta,
+                                               int T, int N, long long B, int levels, float tau,
+                                               int32_t* __restrict__ budget, int32_t* __restrict__ offset,
+                                               float* __restrict__ rel_rect) {
+  if constexpr (NT == kWave) budget_wave_body(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
+  else budget_body<NT, TV>(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
 }
 
-
-// ---------------------------------------------------------------------------
-// T <= 64: one wave, frame t (then retained position i) in lane t (lane i),
-// every value in registers.  Reductions use DPP row permutations and lane
-// reads instead of LDS round trips; compaction uses a ballot; the Haar levels
-// move data with lane shuffles.  Same arithmetic as budget_body.
-// ---------------------------------------------------------------------------
-constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
-constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
-constexpr int kDppHalfMirror = 0x141;  // lane i <-> 7 - i within each half row
-constexpr int kDppMirror = 0x140;      // lane i <-> 15 - i within each row
-
-template <int CTRL>
-__device__ __forceinline__ double dpp_f64(double v) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(u)), CTRL, 0xF, 0xF, false));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(u >> 32)), CTRL, 0xF, 0xF, false));
-  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
-}
-template <int CTRL>
-__device__ __forceinline__ int dpp_i32(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
-}
-__device__ __forceinline__ double readlane_f64(double v, int l) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u)), l));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u >> 32)), l));
-  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
-}
-__device__ __forceinline__ double permute_f64(int dst_lane, double v) {  // value of lane l goes to lane dst(l)
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_ds_permute(dst_lane * 4, int(uint32_t(u))));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_ds_permute(dst_lane * 4, int(uint32_t(u >> 32))));
-  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
-}
-
-// op over all 64 lanes (every lane gets the result): within each row of 16
-// lanes by DPP, then the four row results in a fixed order.
-template <typename Op>
-__device__ __forceinline__ double wave_reduce_f64(double v, Op op) {
-  v = op(v, dpp_f64<kDppXor1>(v));
-  v = op(v, dpp_f64<kDppXor2>(v));
-  v = op(v, dpp_f64<kDppHalfMirror>(v));
-  v = op(v, dpp_f64<kDppMirror>(v));
-  return op(op(readlane_f64(v, 0), readlane_f64(v, 16)), op(readlane_f64(v, 32), readlane_f64(v, 48)));
-}
-__device__ __forceinline__ int wave_reduce_sum_i32(int v) {
-  v += dpp_i32<kDppXor1>(v);
-  v += dpp_i32<kDppXor2>(v);
-  v += dpp_i32<kDppHalfMirror>(v);
-  v += dpp_i32<kDppMirror>(v);
-  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
-         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
-}
-
-__device__ void budget_wave_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
-                                 long long B, int levels, float tau, int32_t* __restrict__ budget,
-                                 int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
-  const double inv_sqrt2 = 0.70710678118654752440;
-  auto dmin = [](double a, double b) { return fmin(a, b); };
-  auto dmax = [](double a, double b) { return fmax(a, b); };
-  auto dadd = [](double a, double b) { return a + b; };
-  const int lane = threadIdx.x;
-  const bool valid = lane < T;
-  const double d = valid ? double(delta[lane]) : 0.0;
-  const double r = valid ? double(rel[lane]) : 0.0;
-
-  // ---- gamma = min-max(delta); retained set M in temporal order ----
-  const double lo = wave_reduce_f64(valid ? d : INFINITY, dmin);
-  const double hi = wave_reduce_f64(valid ? d : -INFINITY, dmax);
-  const double gam = hi > lo ? (d - lo) / (hi - lo) : 0.0;
-  const bool keep = valid && (lane == 0 || d >= double(tau));
-  const uint64_t kmask = __ballot(keep);
-  const int L = __popcll(kmask);
-  const int pos = __popcll(kmask & ((1ull << lane) - 1ull));
-  // a permutation of the lanes: retained frames to positions 0..L-1, the rest after them
-  const int dst = keep ? pos : L + (lane - pos);
-  double x = permute_f64(dst, r);  // position i: r of the i-th retained frame
-  double g = permute_f64(dst, gam);
-
-  // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)); lanes beyond a
-  // level's length hold values nobody reads ----
-  __shared__ double s_det[kMaxLevels][kWave];
-  int len = L;
-  for (int lev = 0; lev < levels; ++lev) {
-    const int i0 = min(2 * lane, kWave - 1), i1 = min(min(2 * lane + 1, len - 1), kWave - 1);
-    const double x0 = __shfl(x, i0, kWave), x1 = __shfl(x, i1, kWave);
-    const double gp = 0.5 * (__shfl(g, i0, kWave) + __shfl(g, i1, kWave));
-    s_det[lev][lane] = gp * ((x0 - x1) * inv_sqrt2);
-    x = (x0 + x1) * inv_sqrt2;
-    g = gp;
-    len = (len + 1) / 2;
-  }
-  // ---- inverse DWT (Eq. (11)) ----
-  for (int lev = levels - 1; lev >= 0; --lev) {
-    const int k = lane >> 1;
-    const double A = __shfl(x, k, kWave), Dk = s_det[lev][k];
-    x = (lane & 1) ? (A - Dk) * inv_sqrt2 : (A + Dk) * inv_sqrt2;
-  }
-  // x in lane i < L: r~ of retained position i
-
-  // ---- budgets (Eq. (16), Eq. (5)) ----
-  const bool inM = lane < L;
-  int n = 0;
-  if (B >= (long long)L * N) {
-    n = inM ? N : 0;
-  } else {
-    double w = inM ? fmax(x, 0.0) : 0.0;
-    const double wsum = wave_reduce_f64(w, dadd);
-    if (wsum == 0.0 && inM) w = 1.0;
-    uint64_t active = __ballot(inM && w > 0.0), full = 0;
-    long long R = B;
-    while (R > 0) {
-      if (active == 0) {  // every weighted frame is full: spread the rest evenly
-        active = __ballot(inM) & ~full;
-        if ((active >> lane) & 1) w = 1.0;
-      }
-      const bool act = (active >> lane) & 1;
-      const double S = wave_reduce_f64(act ? w : 0.0, dadd);
-      const double Rd = double(R);
-      const double q = act ? Rd * w / S : 0.0;
-      const uint64_t cap = __ballot(act && q >= double(N));
-      if (cap) {
-        if ((cap >> lane) & 1) n = N;
-        full |= cap;
-        active &= ~cap;
-        R -= (long long)__popcll(cap) * N;
-        continue;
-      }
-      const double b = floor(q);
-      if (act) n = int(b);
-      const double frac = act ? q - b : 0.0;  // in [0, 1) for active positions
-      int need = int(R) - wave_reduce_sum_i32(act ? int(b) : 0);
-      // +1 for the `need` active positions ranked first by (fraction desc,
-      // index asc).  Non-negative doubles order like their bit patterns, so a
-      // descent over the bits (fractions below 1 leave bits 63 and 62 clear)
-      // finds them: positions with the current bit set are taken whole while
-      // they fit, else the search continues among them; positions still tied
-      // after the last bit go by index.
-      const uint64_t fb = __builtin_bit_cast(uint64_t, frac);
-      uint64_t cand = active, chosen = 0;
-      for (int bit = 61; bit >= 0 && need > 0; --bit) {
-        if (__popcll(cand) <= need) break;
-        const uint64_t ones = cand & __ballot((fb >> bit) & 1ull);
-        const int c1 = __popcll(ones);
-        if (c1 <= need) {
-          chosen |= ones;
-          need -= c1;
-          cand &= ~ones;
-        } else {
-          cand = ones;
-        }
-      }
-      for (; need > 0 && cand; --need) {  // the remaining candidates all fit, or are exact ties
-        chosen |= cand & (~cand + 1ull);
-        cand &= cand - 1ull;
-      }
-      if ((chosen >> lane) & 1ull) n += 1;
-      R = 0;
-    }
-  }
-
-  // ---- back to frames, offsets, rectified relevance ----
-  const int nb = __shfl(n, pos, kWave);
-  const double rt = __shfl(x, pos, kWave);
-  const int bt = keep ? nb : 0;
-  int incl = bt;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int v = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += v;
-  }
-  if (valid) {
-    budget[lane] = bt;
-    offset[lane] = incl - bt;
-    if (rel_rect) rel_rect[lane] = keep ? float(rt) : 0.f;
-  }
-  if (lane == T - 1) offset[T] = incl;
-}
-
-// ---------------------------------------------------------------------------
-// Selection preparation of frame t (stage 3, Eq. (7) and the selection that
-// replaces Eq. (17)):
-//   rank[t][n] = number of the frame's tokens with a larger score a (ties:
-//                the smaller index ranks first), so that a frame's n_t kept
-//                tokens are those of rank < n_t whatever n_t turns out to be;
-//   sal[t][n]  = M_t = min-max of the frame's scores (0 if all are equal).
-// ---------------------------------------------------------------------------
-template <int NTH>
-__device__ void frame_select(int t, int N, const float* __restrict__ tok_score, int32_t* __restrict__ rank,
-                             float* __restrict__ sal) {
-  constexpr int NW = NTH / kWave, AV = kTokMax / NTH;
-  __shared__ uint64_t s_key[kTokMax];
-  __shared__ float s_mm[2][NW];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const __amdgpu_buffer_rsrc_t ares = make_rsrc(tok_score + size_t(t) * N, uint32_t(N) * 4);
-  float av[AV];
-#pragma unroll
-  for (int i = 0; i < AV; ++i) {
-    const int n = tid + i * NTH;
-    av[i] = buf_load_f32(ares, n < N ? n * 4 : kOOB);
-  }
-  float lo = INFINITY, hi = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < AV; ++i) {
-    const int n = tid + i * NTH;
-    if (n < N) {
-      s_key[n] = sel_key(av[i], n);
-      lo = fminf(lo, av[i]);
-      hi = fmaxf(hi, av[i]);
-    }
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    lo = fminf(lo, __shfl_xor(lo, m, kWave));
-    hi = fmaxf(hi, __shfl_xor(hi, m, kWave));
-  }
-  if (lane == 0) {
-    s_mm[0][wave] = lo;
-    s_mm[1][wave] = hi;
-  }
-  __syncthreads();
-  lo = s_mm[0][0];
-  hi = s_mm[1][0];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) {
-    lo = fminf(lo, s_mm[0][w]);
-    hi = fmaxf(hi, s_mm[1][w]);
-  }
-  const float range = hi - lo;
-  // tpt consecutive lanes share a token, each counting the keys of one part
-  // of the frame (read as near-broadcasts, 16 per step)
-  const int tpt = N * 8 <= NTH ? 8 : N * 4 <= NTH ? 4 : N * 2 <= NTH ? 2 : 1;
-  const int part = tid % tpt, per_round = NTH / tpt;
-  const int jlen = (N + tpt - 1) / tpt, jb = min(N, part * jlen), je = min(N, jb + jlen);
-  for (int n0 = 0; n0 < N; n0 += per_round) {
-    const int n = n0 + tid / tpt;
-    int r = 0;
-    uint64_t kn = 0;
-    if (n < N) {
-      kn = s_key[n];
-      int j = jb;
-      for (; j + 16 <= je; j += 16) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) r += s_key[j + e] > kn;
-      }
-      for (; j < je; ++j) r += s_key[j] > kn;
-    }
-    for (int m = 1; m < tpt; m <<= 1) r += __shfl_xor(r, m, kWave);
-    if (n < N && part == 0) {
-      rank[size_t(t) * N + n] = r;
-      const float a = order_value(uint32_t(kn >> 12));
-      sal[size_t(t) * N + n] = range > 0.f ? (a - lo) / range : 0.f;
-    }
-  }
-}
-
-// Workgroup 0 computes the budgets when do_budget (a one-wave body on wave
-// 0, which never waits at a barrier); the others prepare the selection of
-// frame blockIdx.x - do_budget.  Both only read stage 1's outputs, so they
-// run side by side.
-template <int NT, int TV, int NTH>
-__global__ __launch_bounds__(NTH) void k_budget_select(const float* __restrict__ rel,
-                                                       const float* __restrict__ delta, int T, int N, long long B,
-                                                       int levels, float tau, int32_t* __restrict__ budget,
-                                                       int32_t* __restrict__ offset, float* __restrict__ rel_rect,
-                                                       const float* __restrict__ tok_score,
-                                                       int32_t* __restrict__ rank, float* __restrict__ sal,
-                                                       int do_budget) {
-  if (do_budget && blockIdx.x == 0) {
-    if (int(threadIdx.x) < NT) {
-      if constexpr (NT == kWave) budget_wave_body(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
-      else budget_body<NT, TV>(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
-    }
-    return;
-  }
-  frame_select<NTH>(int(blockIdx.x) - do_budget, N, tok_score, rank, sal);
-}
-
-template <int NT, int TV, int NTH>
-void launch_bs(const wz_config& c, const float* rel, const float* delta, int32_t* budget, int32_t* offset,
-               float* rel_rect, const float* tok_score, int32_t* rank, float* sal, hipStream_t s) {
-  const int do_budget = rel != nullptr;
-  const int grid = do_budget + (tok_score ? c.T : 0);
-  hipLaunchKernelGGL((k_budget_select<NT, TV, NTH>), dim3(grid), dim3(NTH), 0, s, rel, delta, c.T, c.H * c.W,
-                     (long long)c.B, c.levels, c.tau, budget, offset, rel_rect, tok_score, rank, sal, do_budget);
+template <int NT, int TV>
+void launch_k(const wz_config& c, const float* rel, const float* delta, int32_t* budget, int32_t* offset,
+              float* rel_rect, hipStream_t s) {
+  hipLaunchKernelGGL((k_budget<NT, TV>), dim3(1), dim3(NT), 0, s, rel, delta, c.T, c.H * c.W, (long long)c.B,
+                     c.levels, c.tau, budget, offset, rel_rect);
 }
 
 }  // namespace
 
-hipError_t launch_budget_select(const wz_config& c, const float* frame_rel, const float* frame_delta,
-                                int32_t* budget, int32_t* offset, float* rel_rect, const float* tok_score,
-                                int32_t* rank, float* sal, hipStream_t s) {
-  if (c.T <= 64)  // one-wave budget: the selection workgroups can use 1024 threads
-    launch_bs<kWave, 64, 1024>(c, frame_rel, frame_delta, budget, offset, rel_rect, tok_score, rank, sal, s);
-  else if (c.T <= 256)
-    launch_bs<256, 256, 256>(c, frame_rel, frame_delta, budget, offset, rel_rect, tok_score, rank, sal, s);
-  else
-    launch_bs<1024, kTMax, 1024>(c, frame_rel, frame_delta, budget, offset, rel_rect, tok_score, rank, sal, s);
+hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float* frame_delta, int32_t* budget,
+                         int32_t* offset, float* rel_rect, hipStream_t s) {
+  if (c.T <= 64) launch_k<kWave, 64>(c, frame_rel, frame_delta, budget, offset, rel_rect, s);
+  else if (c.T <= 256) launch_k<256, 256>(c, frame_rel, frame_delta, budget, offset, rel_rect, s);
+  else launch_k<1024, kTMax>(c, frame_rel, frame_delta, budget, offset, rel_rect, s);
   return hipGetLastError();
 }
 

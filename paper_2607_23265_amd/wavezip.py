@@ -53,7 +53,7 @@ def lib():
     L.wz_workspace_bytes.restype = S
     L.wz_relevance.argtypes = [cfgp, P, P, P, P, P, P, S, P]
     L.wz_temporal_budget.argtypes = [cfgp, P, P, P, P, P, P]
-    L.wz_spatial_dwt_condense.argtypes = [cfgp, P, P, P, P, P, P, S, P]
+    L.wz_spatial_dwt_condense.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_condense.argtypes = [cfgp, P, P, P, P, P, P, P, S, P]
     for f in ("wz_relevance", "wz_temporal_budget", "wz_spatial_dwt_condense", "wz_condense"):
         getattr(L, f).restype = ctypes.c_int
@@ -150,15 +150,14 @@ def _out_tokens(p: Problem, dev):
                                                                                device=dev)
 
 
-def spatial_dwt_condense(p: Problem, X, tok_score, offset, ws=None):
+def spatial_dwt_condense(p: Problem, X, tok_score, offset):
     """wz_spatial_dwt_condense -> (tokens [B, C], index [B]); rows from offset[T] on are unwritten."""
     _require_device(X, tok_score, offset)
     dev = X.device
-    ws = new_workspace(p, dev) if ws is None else ws
     tok, idx = _out_tokens(p, dev)
     cfg = p.config()
     _check(lib().wz_spatial_dwt_condense(ctypes.byref(cfg), _ptr(X), _ptr(tok_score), _ptr(offset), _ptr(tok),
-                                         _ptr(idx), _ptr(ws), ws.numel(), _stream(dev)),
+                                         _ptr(idx), _stream(dev)),
            "wz_spatial_dwt_condense")
     return tok, idx
 
