@@ -76,7 +76,7 @@ wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query, f
   if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, tok_score, w, s)));
-  return from_hip(launch_frame_scores(*cfg, w, tok_score, frame_rel, frame_delta, s));
+  return from_hip(launch_frame(*cfg, w, tok_score, frame_rel, frame_delta, false, s));
 }
 
 wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const float* frame_delta,
@@ -101,8 +101,8 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
     WZ_TRY(check_ptr(out_tokens, 16));
     WZ_TRY(check_ptr(out_index, 4));
   }
-  return from_hip(launch_assign_gather(*cfg, X, tok_score, nullptr, nullptr, offset, nullptr, nullptr, out_tokens,
-                                       out_index, static_cast<hipStream_t>(stream)));
+  return from_hip(launch_assign_gather(*cfg, X, tok_score, nullptr, nullptr, offset, nullptr, nullptr, nullptr,
+                                       out_tokens, out_index, static_cast<hipStream_t>(stream)));
 }
 
 wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
@@ -122,14 +122,14 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, vo
   if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
   hipStream_t s = static_cast<hipStream_t>(stream);
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s)));
-  WZ_TRY(from_hip(launch_frame_scores(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, s)));
+  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s)));
   if (cfg->T <= kFusedTMax)  // budgets computed inside the selection kernel
-    return from_hip(launch_assign_gather(*cfg, X, w.tok_score, w.frame_rel, w.frame_delta, nullptr, budget, offset,
-                                         out_tokens, out_index, s));
+    return from_hip(launch_assign_gather(*cfg, X, w.tok_score, w.frame_rel, w.frame_delta, nullptr, &w, budget,
+                                         offset, out_tokens, out_index, s));
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
   WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s)));
-  return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, nullptr, nullptr, out_tokens,
+  return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, &w, nullptr, nullptr, out_tokens,
                                        out_index, s));
 }
 

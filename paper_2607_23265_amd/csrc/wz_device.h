@@ -1,6 +1,8 @@
 // Device helpers shared by the gfx950 kernels: raw buffer-resource accesses.
 #pragma once
 
+#include <type_traits>
+
 #include "wz_internal.h"
 
 namespace wz {
@@ -86,6 +88,46 @@ __device__ __forceinline__ float order_value(uint32_t k) {
 }
 __device__ __forceinline__ uint64_t sel_key(float a, int n) {
   return (uint64_t(order_key(a)) << 12) | uint64_t(kTokMax - 1 - n);
+}
+
+}  // namespace wz
+
+namespace wz {
+
+// Extremes over the 64 lanes of a wave (every lane gets the result), by DPP
+// within each 16-lane row and gfx950's lane swaps across rows: no LDS.
+template <typename Op>
+__device__ __forceinline__ float wave_reduce_f32(float v, Op op) {
+  auto dpp = [](float x, auto ctrl) {
+    return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), decltype(ctrl)::value, 0xF, 0xF, false));
+  };
+  v = op(v, dpp(v, std::integral_constant<int, 0xB1>{}));   // lane ^ 1
+  v = op(v, dpp(v, std::integral_constant<int, 0x4E>{}));   // lane ^ 2
+  v = op(v, dpp(v, std::integral_constant<int, 0x141>{}));  // 7 - i in 8
+  v = op(v, dpp(v, std::integral_constant<int, 0x140>{}));  // 15 - i in 16
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = op(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return op(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float wave_min_f32(float v) {
+  return wave_reduce_f32(v, [](float a, float b) { return fminf(a, b); });
+}
+__device__ __forceinline__ float wave_max_f32(float v) {
+  return wave_reduce_f32(v, [](float a, float b) { return fmaxf(a, b); });
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: shifts within each
+// 16-lane row by DPP, then the totals of the rows below from three lane reads.
+__device__ __forceinline__ int wave_incl_scan_i32(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+            r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return v + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
 }
 
 }  // namespace wz

@@ -60,7 +60,7 @@ inline int qpad(int Q) { return (Q + 3) & ~3; }
 //   kRelLds  bf16, Q <= 32: coalesced loads transposed through LDS, MFMA;
 //   kRelMfma bf16, Q > 32, frames of >= 49 tokens: MFMA-layout loads;
 //   kRelValu everything else (fp32 inputs, small frames with many queries).
-enum RelKind { kRelValu = 0, kRelMfma = 1, kRelLds = 2 };
+enum RelKind { kRelValu = 0, kRelMfma = 1, kRelLds = 2, kRelTok = 3 };
 RelKind relevance_kind(const wz_config& c);
 
 // LDS-transpose kernel limits: up to 8 waves of 32 tokens per tile; a slice
@@ -88,7 +88,17 @@ inline RelPlan relevance_plan(const wz_config& c) {
   const int N = c.H * c.W;
   RelPlan p{};
   p.kind = relevance_kind(c);
-  if (p.kind == kRelLds) {
+  if (p.kind == kRelTok) {
+    // tiles of at most 64 tokens with every channel, one slice
+    p.tiles = (N + 63) / 64;
+    p.tile_tokens = (N + p.tiles - 1) / p.tiles;
+    p.ipc = (p.tile_tokens + 7) / 8;
+    p.ntg = c.Q <= 16 ? 1 : 2;
+    p.mt = 0;
+    p.slices = 1;
+    p.kc = c.C;
+    p.threads = 8 * 64;
+  } else if (p.kind == kRelLds) {
     const int cap = 32 * kLdsWavesMax;
     p.tiles = (N + cap - 1) / cap;
     p.tile_tokens = (N + p.tiles - 1) / p.tiles;
@@ -162,6 +172,9 @@ struct Workspace {
   float* sig_part;     // [T][tiles][slices][Q]   per-unit sums over tokens of x . q_j
   float* pool_part;    // [T][tiles][C]           per-tile channel sums
   float* tok_score;    // [T*N]
+  int32_t* rank;       // [T*N]                   selection rank of each token in its frame
+  int32_t* byrank;     // [T*N]                   token of each rank
+  float* gate;         // [T*N]                   saliency gate of each token's 2x2 block
   float* frame_rel;    // [T]
   float* frame_delta;  // [T]
   int32_t* budget;     // [T]
@@ -184,6 +197,9 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   w.sig_part = reinterpret_cast<float*>(take(T * tiles * S * Q * 4));
   w.pool_part = reinterpret_cast<float*>(take(T * tiles * C * 4));
   w.tok_score = reinterpret_cast<float*>(take(T * N * 4));
+  w.rank = reinterpret_cast<int32_t*>(take(T * N * 4));
+  w.byrank = reinterpret_cast<int32_t*>(take(T * N * 4));
+  w.gate = reinterpret_cast<float*>(take(T * N * 4));
   w.frame_rel = reinterpret_cast<float*>(take(T * 4));
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
   w.budget = reinterpret_cast<int32_t*>(take(T * 4));
@@ -197,9 +213,11 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
 // tok_score when there is one channel slice).
 hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void* query, float* tok_score,
                                    const Workspace& ws, hipStream_t s);
-// Per-frame finish of stage 1: a_{t,n} (several slices), r_t and delta_t.
-hipError_t launch_frame_scores(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
-                               float* frame_delta, hipStream_t s);
+// Per-frame finish of stage 1: a_{t,n} (several slices), r_t and delta_t;
+// with `order` also every frame's selection ranks and block gates (into
+// ws.rank, ws.byrank, ws.gate) for launch_assign_gather.
+hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
+                        float* frame_delta, bool order, hipStream_t s);
 // Budgets alone, in one workgroup (wz_temporal_budget, and wz_condense when
 // T > kFusedTMax).
 hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float* frame_delta, int32_t* budget,
@@ -207,10 +225,13 @@ hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float
 // Selection, spatial modulation and compaction.  With offset_in the frames'
 // row offsets are given; without it (T <= kFusedTMax) every workgroup computes
 // the budgets from frame_rel and frame_delta itself and workgroup 0 writes
-// them to budget_out / offset_out when those are not null.
+// them to budget_out / offset_out when those are not null.  With ws the
+// frames' ranks and gates come from launch_frame; without it each workgroup
+// forms its frame's from tok_score.
 hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* tok_score, const float* frame_rel,
-                                const float* frame_delta, const int32_t* offset_in, int32_t* budget_out,
-                                int32_t* offset_out, void* out_tokens, int32_t* out_index, hipStream_t s);
+                                const float* frame_delta, const int32_t* offset_in, const Workspace* ws,
+                                int32_t* budget_out, int32_t* offset_out, void* out_tokens, int32_t* out_index,
+                                hipStream_t s);
 // Workgroups per frame of launch_assign_gather.
 int assign_groups_per_frame(const wz_config& c);
 

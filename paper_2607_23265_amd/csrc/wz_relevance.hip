@@ -607,6 +607,263 @@ __global__ __launch_bounds__(kLdsWavesMax * 64) void k_relevance_lds(const uint1
 }
 
 // ---------------------------------------------------------------------------
+// Token-tiled path (bf16, Q <= 32)
+// ---------------------------------------------------------------------------
+// A workgroup owns one tile of at most 64 tokens of one frame with ALL its
+// channels, so a_{t,n} is final here and no per-slice partial scores are
+// written; its tokens are one contiguous stretch of X.  The eight waves split
+// the channels into 64-channel chunks (wave w takes chunks w, w + 8, ...) and
+// never wait for each other until the epilogue.  Per chunk a wave
+//   1. loads the tile's rows (8 rows x 128 bytes per instruction, whole cache
+//      lines) and the query's 64 channels directly in the MFMA B layout (16
+//      query rows x 64 bytes per instruction; the query is L2-resident);
+//   2. stores the rows to its own LDS buffer (16-byte units XOR-swizzled by
+//      row) and, from the same registers, accumulates |x|^2 and the chunk's
+//      channel sums with bf16 dot2 instructions; the channel sums of the
+//      chunk are reduced across the wave by DPP and lane swaps and stored;
+//   3. re-issues the ring slot for the chunk after next;
+//   4. runs two 32-channel steps of S += X Q^T (v_mfma_f32_16x16x32_bf16) on
+//      four 16-row tiles, reading A from its buffer.
+// The epilogue adds the waves' partial S, |x|^2 and |q_j|^2 in wave order
+// through LDS and forms a_{t,n} = max_j S_nj / (|q_j| |x_n|) and the tile's
+// sigma_j = sum_n S_nj.
+constexpr int kTokWaves = 8;
+constexpr int kTokChunk = 64;   // channels per chunk (128 bytes of a bf16 row)
+constexpr int kTokRows = 64;    // tokens per tile at most (four 16-row MFMA tiles)
+
+constexpr int kTokPoolMax = 8192;  // channels whose sums are gathered in LDS before one coalesced store
+
+// POOL: the tile's channel sums are gathered in LDS (C <= kTokPoolMax) and
+// stored once at the end, instead of a few lanes per chunk storing them
+// between the stream's loads.
+template <int NTG, int IPC, bool POOL>
+__global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t* __restrict__ X,
+                                                                 const uint16_t* __restrict__ query,
+                                                                 int tile_tokens, StreamArgs f) {
+  constexpr int NQ = NTG * 16;       // query columns of the accumulators
+  // per-wave chunk buffer (16-byte units swizzled by row); after a wave's
+  // loop its buffer holds its partial S [64 rows][NQ] (fits: NQ <= 32)
+  __shared__ __align__(16) u32x4 s_x[kTokWaves][kTokRows][8];
+  __shared__ __align__(16) float s_pool[POOL ? kTokPoolMax : 4];
+  __shared__ float s_xx[kTokWaves][kTokRows];
+  __shared__ float s_qq[kTokWaves][NQ];
+  __shared__ float s_rq[NQ];
+  __shared__ float s_sig[kTokWaves][NQ];             // per-wave column sums of S
+
+  int t, tile, sl;
+  unit_of_block(blockIdx.x, f.tiles, 1, t, tile, sl);
+  if (t >= f.T) return;
+  const int N = f.N, C = f.C, Q = f.Q;
+  const int tok0 = tile * tile_tokens;
+  const int TM = min(tile_tokens, N - tok0);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, grp = lane >> 4;  // MFMA layout
+  const int lr = lane >> 3, lu = lane & 7;     // coalesced layout: row lr of each 8-row group, 16-byte unit lu
+  const int nch = (C + kTokChunk - 1) / kTokChunk;
+
+  const __amdgpu_buffer_rsrc_t xres = make_rsrc_uniform(X + (size_t(t) * N + tok0) * C, uint32_t(TM) * C * 2);
+  const __amdgpu_buffer_rsrc_t qres = make_rsrc_uniform(query, uint32_t(Q) * C * 2);
+
+  // ring slot: IPC row instructions (rows 8k + lr, unit lu) and the query
+  // operands of the chunk's two steps (tile n, step s: query row 16n + r16,
+  // channels 32s + 8 grp); chunks past the end and channels past C read zeros
+  struct Slot {
+    bf16x8 x[IPC];
+    bf16x8 q[NTG][2];
+  };
+  auto issue = [&](int c, Slot& d) {
+    const int ch = c * kTokChunk;
+    const bool okc = c < nch;
+#pragma unroll
+    for (int k = 0; k < IPC; ++k) {
+      const int cc = ch + 8 * lu;
+      d.x[k] = buf_load_bf16x8(xres, (okc && cc < C) ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
+    }
+#pragma unroll
+    for (int n = 0; n < NTG; ++n)
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const int j = 16 * n + r16, cc = ch + 32 * st + 8 * grp;
+        d.q[n][st] = buf_load_bf16x8(qres, (okc && j < Q && cc < C) ? (j * C + cc) * 2 : kOOB);
+      }
+  };
+
+  f32x4 Sacc[4][NTG];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int n = 0; n < NTG; ++n) Sacc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float xx[IPC], qq[NTG];
+#pragma unroll
+  for (int k = 0; k < IPC; ++k) xx[k] = 0.f;
+#pragma unroll
+  for (int n = 0; n < NTG; ++n) qq[n] = 0.f;
+  uint32_t one_lo = kBf16OneLo, one_hi = kBf16OneHi;
+  asm volatile("" : "+v"(one_lo), "+v"(one_hi));  // opaque: keeps them out of inline constants
+  float* pool = POOL ? s_pool : f.pool_part + (size_t(t) * f.tiles + tile) * C;
+
+  auto consume = [&](int c, const Slot& d) {
+    // rows to LDS, |x|^2 and channel sums from the registers
+    float cs[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cs[e] = 0.f;
+#pragma unroll
+    for (int k = 0; k < IPC; ++k) {
+      const int row = 8 * k + lr;
+      const u32x4 v = __builtin_bit_cast(u32x4, d.x[k]);
+      s_x[wave][row][lu ^ (row & 7)] = v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        xx[k] = dot2(v[e], v[e], xx[k]);
+        cs[2 * e] = dot2(v[e], one_lo, cs[2 * e]);
+        cs[2 * e + 1] = dot2(v[e], one_hi, cs[2 * e + 1]);
+      }
+    }
+    // |q_j|^2 shares of this lane's query operands
+#pragma unroll
+    for (int n = 0; n < NTG; ++n)
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const u32x4 v = __builtin_bit_cast(u32x4, d.q[n][st]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qq[n] = dot2(v[e], v[e], qq[n]);
+      }
+    // channel sums over the wave's rows: lanes lu, lu + 8, ..., lu + 56 in a fixed order
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v = cs[e];
+      v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
+      const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+      v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+      const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+      cs[e] = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+    }
+    const int c0 = c * kTokChunk + 8 * lu;
+    if (lane < 8 && c0 < C) {
+      *reinterpret_cast<f32x4*>(pool + c0) = f32x4{cs[0], cs[1], cs[2], cs[3]};
+      *reinterpret_cast<f32x4*>(pool + c0 + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
+    }
+  };
+  auto contract = [&](const Slot& d) {
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      bf16x8 A[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * i + r16;
+        A[i] = __builtin_bit_cast(bf16x8, s_x[wave][row][(4 * st + grp) ^ (row & 7)]);
+      }
+#pragma unroll
+      for (int n = 0; n < NTG; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[i], d.q[n][st], Sacc[i][n], 0, 0, 0);
+    }
+  };
+
+  // rows this wave never loads (8 * IPC .. 63) are zero in its buffer
+  for (int u = 8 * IPC * 8 + lane; u < kTokRows * 8; u += kWave) (&s_x[wave][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
+
+  Slot A, B;
+  issue(wave, A);
+  issue(wave + kTokWaves, B);
+  for (int c = wave; c < nch; c += 2 * kTokWaves) {
+    __builtin_amdgcn_sched_barrier(0);
+    consume(c, A);
+    contract(A);
+    issue(c + 2 * kTokWaves, A);
+    __builtin_amdgcn_sched_barrier(0);
+    if (c + kTokWaves < nch) {
+      consume(c + kTokWaves, B);
+      contract(B);
+    }
+    issue(c + 3 * kTokWaves, B);
+  }
+
+  // ---- epilogue: waves added in order ----
+  // |x|^2 of row 8k + lr: the 8 lanes of the row
+#pragma unroll
+  for (int k = 0; k < IPC; ++k) {
+    float v = xx[k];
+    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0xB1, 0xF, 0xF, false));   // lane ^ 1
+    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x4E, 0xF, 0xF, false));   // lane ^ 2
+    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x141, 0xF, 0xF, false));  // 7 - i in 8
+    if (lu == 0) s_xx[wave][8 * k + lr] = v;
+  }
+  for (int r = 8 * IPC + lane; r < kTokRows; r += kWave) s_xx[wave][r] = 0.f;
+#pragma unroll
+  for (int n = 0; n < NTG; ++n) {
+    const float v = row_sum4(qq[n]);
+    if (lane < 16) s_qq[wave][16 * n + lane] = v;
+  }
+  // wave w's partial S sits in its own chunk buffer: [row][NQ] floats from &s_x[w][0][0]
+  auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_x[w][0][0])[r * NQ + j]; };
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int n = 0; n < NTG; ++n)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s_part(wave, 16 * i + 4 * grp + e, 16 * n + r16) = Sacc[i][n][e];
+  __syncthreads();
+  if (POOL) {
+    f32x4* gpool = reinterpret_cast<f32x4*>(f.pool_part + (size_t(t) * f.tiles + tile) * C);
+    for (int c4 = tid; c4 < C / 4; c4 += kTokWaves * kWave) gpool[c4] = reinterpret_cast<const f32x4*>(s_pool)[c4];
+  }
+  if (tid < NQ) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < kTokWaves; ++w) v += s_qq[w][tid];
+    s_rq[tid] = v > 0.f ? 1.0f / sqrtf(v) : 0.f;
+    if (tile == 0 && tid < Q) f.qg_part[size_t(t) * Q + tid] = v;
+  }
+  // thread -> row tid / 8, columns 4 * (tid % 8) .. + 3 (NTG = 2) or 2 * (tid % 8) .. + 1 (NTG = 1)
+  constexpr int CPT = NQ / 8;
+  const int row = tid >> 3, cg = (tid & 7) * CPT;
+  float sv[CPT];
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < kTokWaves; ++w) v += s_part(w, row, cg + e);
+    sv[e] = v;
+  }
+  float x2 = 0.f;
+#pragma unroll
+  for (int w = 0; w < kTokWaves; ++w) x2 += s_xx[w][row];
+  __syncthreads();
+  float best = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < CPT; ++e)
+    if (cg + e < Q) best = fmaxf(best, sv[e] * s_rq[cg + e]);
+  best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
+  best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
+  best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
+  if ((tid & 7) == 0 && row < TM) {
+    const float xn = sqrtf(x2);
+    f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+  }
+  // sigma_j of the tile: the wave's eight rows by lane swaps, then the waves in order
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) {
+    float v = row < TM ? sv[e] : 0.f;
+    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+    if (lane < 8) s_sig[wave][cg + e] = v;
+  }
+  __syncthreads();
+  if (tid < Q) {
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < kTokWaves; ++w) v += s_sig[w][tid];
+    f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Vector-ALU path
 // ---------------------------------------------------------------------------
 template <typename In>
@@ -744,6 +1001,16 @@ void launch_mfma(const RelPlan& pl, const void* X, const void* query, const Stre
 }
 
 template <int NTG, int IPC>
+void launch_tok(const RelPlan& pl, const void* X, const void* query, const StreamArgs& fa, hipStream_t s) {
+  if (fa.C <= kTokPoolMax)
+    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true>), dim3(pl.grid), dim3(pl.threads), 0, s,
+                       static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, fa);
+  else
+    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false>), dim3(pl.grid), dim3(pl.threads), 0, s,
+                       static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, fa);
+}
+
+template <int NTG, int IPC>
 void launch_lds(const RelPlan& pl, const void* X, const void* query, const StreamArgs& fa, hipStream_t s) {
   hipLaunchKernelGGL((k_relevance_lds<NTG, IPC, WZ_LDS_RING>), dim3(pl.grid), dim3(pl.threads), 0, s,
                      static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, pl.kc,
@@ -754,7 +1021,11 @@ void launch_lds(const RelPlan& pl, const void* X, const void* query, const Strea
 
 RelKind relevance_kind(const wz_config& c) {
   if (c.in_dtype != WZ_BF16) return kRelValu;
+#ifdef WZ_REL_SLICES
   if (c.Q <= 32) return kRelLds;
+#else
+  if (c.Q <= 32) return kRelTok;
+#endif
   // two 16-row MFMA tiles per wave, at least 2 waves: frames of at least 49 tokens
   return c.H * c.W >= 49 ? kRelMfma : kRelValu;
 }
@@ -764,7 +1035,21 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
   const RelPlan pl = relevance_plan(c);
   const StreamArgs fa{ws.s_part, ws.g_part, ws.qg_part, ws.sig_part, ws.pool_part, tok_score, c.T, c.H * c.W,
                       c.C,       c.Q,       qpad(c.Q),  pl.tiles,    pl.slices};
-  if (pl.kind == kRelLds) {
+  if (pl.kind == kRelTok) {
+#define WZ_TOK(NTG)                                    \
+  switch (pl.ipc) {                                    \
+    case 1: launch_tok<NTG, 1>(pl, X, query, fa, s); break; \
+    case 2: launch_tok<NTG, 2>(pl, X, query, fa, s); break; \
+    case 3: launch_tok<NTG, 3>(pl, X, query, fa, s); break; \
+    case 4: launch_tok<NTG, 4>(pl, X, query, fa, s); break; \
+    case 5: launch_tok<NTG, 5>(pl, X, query, fa, s); break; \
+    case 6: launch_tok<NTG, 6>(pl, X, query, fa, s); break; \
+    case 7: launch_tok<NTG, 7>(pl, X, query, fa, s); break; \
+    default: launch_tok<NTG, 8>(pl, X, query, fa, s); break; \
+  }
+    if (pl.ntg == 1) { WZ_TOK(1) } else { WZ_TOK(2) }
+#undef WZ_TOK
+  } else if (pl.kind == kRelLds) {
     if (pl.ntg == 1) {
       if (pl.ipc == 7) launch_lds<1, 7>(pl, X, query, fa, s);
       else launch_lds<1, 8>(pl, X, query, fa, s);

@@ -7,25 +7,27 @@
 // bit and no kernel boundary separates the budget from its use.
 //
 // Workgroup (t, p), p < P, 1024 threads, works on frame t:
-//   A. its threads load the frame's scores a_{t,n} as selection keys (larger
-//      score first, then the smaller index) and take their min and max;
-//      then wave 0 computes the budgets (T <= 64; all waves up to T = 256)
-//      while the other waves rank every token of the frame by counting the
-//      larger keys (four threads share a token);
-//   B. the frame keeps its n_t tokens of rank < n_t; a block-wide count in
-//      raster order lists them, with the gate g = lambda * mean(M) of each
-//      kept token's 2x2 block, M = min-max of the frame's scores;
-//   C. kept tokens p, p + P, ... are reconstructed, each split into channel
-//      parts of at most two 16-byte vectors per lane, one part per wave at a
-//      time: the 2x2 Haar block of the grid (the last row / column repeated
-//      when H or W is odd) is read, LL, LH, HL, HH formed with the
-//      orthonormal butterflies (Eq. (12)), the three detail bands multiplied
-//      by g (Eq. (13)-(14)) and the token's position inverted (Eq. (15)); the
-//      row goes to out_tokens[offset_t + i], its flat index t*H*W + n to
-//      out_index.
-// Only the blocks of kept tokens are read: at most 4 * B token rows, usually
-// partly from the Infinity Cache right after the pass over the frames.
+//   A. wave 0 computes the budgets (T <= 64; all waves up to T = 256) while
+//      the other waves take the frame's selection ranks and block gates
+//      (from the per-frame kernel, or formed here from the scores when the
+//      stage runs on its own, wz_rank.h) and read the 2x2 blocks of the first
+//      tokens this workgroup will reconstruct: most frames keep at least
+//      three quarters of the mean budget, so those reads are rarely wasted
+//      and overlap the budget;
+//   B. the frame keeps its n_t tokens of rank < n_t, numbered in raster
+//      order by ballots;
+//   C. kept tokens of rank p, p + P, ... are reconstructed, each split into
+//      channel parts of at most two 16-byte vectors per lane, one part per
+//      wave at a time: LL, LH, HL, HH of the token's 2x2 Haar block (the last
+//      row / column repeated when H or W is odd) by the orthonormal
+//      butterflies (Eq. (12)), the three detail bands multiplied by the
+//      block's gate (Eq. (13)-(14)) and the token's position inverted
+//      (Eq. (15)); the row goes to out_tokens[offset_t + position], its flat
+//      index t*H*W + n to out_index.
+// Only the blocks of kept tokens are read: at most 4 * B token rows, partly
+// from the Infinity Cache right after the pass over the frames.
 #include "wz_budget.h"
+#include "wz_rank.h"
 
 namespace wz {
 namespace {
@@ -42,6 +44,9 @@ struct AssignArgs {
   const float* rel;         // [T] r_t        (budget modes)
   const float* delta;       // [T] delta_t    (budget modes)
   const int32_t* offset_in; // [T+1]          (kOffsets)
+  const int32_t* rank;      // [T][H*W] or null: selection ranks from the per-frame kernel
+  const int32_t* byrank;    // [T][H*W]
+  const float* gate;        // [T][H*W]
   int32_t* budget_out;      // [T] or null    (budget modes; written by workgroup (0, 0))
   int32_t* offset_out;      // [T+1] or null  (budget modes)
   void* out_tokens;         // [B][C]
@@ -100,67 +105,35 @@ __device__ __forceinline__ void store_row<uint16_t, 4>(uint16_t* p, const float*
   *reinterpret_cast<u32x2*>(p) = o;
 }
 
-constexpr int kBins = 256;  // score bins of the ranking
-
 template <typename In, typename Out, int U, int MODE>
 __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) {
   constexpr int V = Vec16<In>::kV;
-  // The ranking group: every wave but wave 0 when wave 0 computes the
-  // budgets meanwhile (kWaveBudget), else all waves.
+  // waves that read ranks and blocks while wave 0 computes the budgets
   constexpr int G0 = MODE == kWaveBudget ? 1 : 0;
   constexpr int GW = kNW - G0;
   extern __shared__ __align__(16) char s_dyn[];
   __shared__ int32_t s_nb[kFusedTMax];       // budgets (budget modes)
   __shared__ int32_t s_off[kFusedTMax + 1];  // offsets (budget modes)
-  __shared__ float s_mm[2][kNW];             // per-wave min / max of the scores
   __shared__ int s_cnt[kNW];
-  __shared__ int s_start[kBins];             // first sorted position of each bin (bins in descending order)
-  __shared__ int s_fill[kBins];              // tokens per bin
-  __shared__ int s_sync;                     // arrivals at the ranking group's barriers
+  __shared__ float s_mm[2 * kNW];
+  __shared__ int s_start[kBins], s_fill[kBins];
 
   const int N = f.H * f.W, T = f.T;
   const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
   const int t = (slot / f.P) * kXcds + xcd, p = slot % f.P;
   if (t >= T) return;  // whole workgroup
-  uint64_t* s_key = reinterpret_cast<uint64_t*>(s_dyn);     // [N] selection keys
-  int32_t* s_rank = reinterpret_cast<int32_t*>(s_key + N);  // [N] rank of each token
-  int32_t* s_byrank = s_rank + N;                           // [N] token of each rank
-  int32_t* s_posr = s_byrank + N;                           // [N] raster position among the kept, by rank
-  float* s_gate = reinterpret_cast<float*>(s_posr + N);     // [N] gate of each token's block
-  int32_t* s_sorted = s_posr;                               // [N] tokens by bin (before the positions)
+  RankLds rl;
+  rl.key = reinterpret_cast<uint64_t*>(s_dyn);
+  rl.rank = reinterpret_cast<int32_t*>(rl.key + N);
+  rl.byrank = rl.rank + N;
+  rl.gate = reinterpret_cast<float*>(rl.byrank + N);
+  rl.order = reinterpret_cast<int32_t*>(rl.gate + N);
+  rl.start = s_start;
+  rl.fill = s_fill;
+  rl.mm = s_mm;
+  int32_t* s_posr = rl.order;  // raster position among the kept, by rank (after the ranking)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int gi = tid - G0 * kWave, gn = GW * kWave;         // thread index and count in the group
-
-  // budget inputs first: wave 0 computes the budgets as soon as they arrive
-  double bd = 0.0, br = 0.0;
-  int o_base = 0, o_next = 0, o_last = 0;
-  if constexpr (MODE == kWaveBudget) {
-    if (wave == 0 && lane < T) {
-      bd = double(f.delta[lane]);
-      br = double(f.rel[lane]);
-    }
-  } else if constexpr (MODE == kOffsets) {
-    o_base = f.offset_in[t];
-    o_next = f.offset_in[t + 1];
-    o_last = f.offset_in[T];
-  }
-  if (tid == 0) s_sync = 0;
-  lds_barrier();
-
-  // Barrier of the ranking group alone (wave 0 may be inside the budget): an
-  // arrival counter in LDS that every group wave increments once per barrier
-  // and waits on; every group wave reaches every such barrier.
-  int gen = 0;
-  auto group_sync = [&]() {
-    if constexpr (MODE == kWaveBudget) {
-      ++gen;
-      if (lane == 0) __hip_atomic_fetch_add(&s_sync, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-      while (__hip_atomic_load(&s_sync, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < gen * GW)
-        __builtin_amdgcn_s_sleep(1);
-    } else {
-      lds_barrier();
-    }
-  };
+  const bool given = f.rank != nullptr;
 
   // Channel parts of a kept token: at most U vectors per lane each.
   const int nvec = f.C / V;
@@ -170,13 +143,11 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   const __amdgpu_buffer_rsrc_t xres = make_rsrc(static_cast<const In*>(f.X) + size_t(t) * N * f.C, uint32_t(N) * rb);
   // This workgroup reconstructs the kept tokens of rank p, p + P, ...; item j
   // is part j % parts of the token of rank p + P * (j / parts).  The first
-  // items, up to one per group wave and for ranks below kpre (where most
-  // frames' budgets reach), are read before the budget is known.
+  // items, one per reading wave and for ranks below kpre, are read before the
+  // budget is known.
   const int kp = min(f.kpre, N);
-  const int npre = MODE == kWaveBudget && kp > p ? min(GW, (kp - p + f.P - 1) / f.P * parts) : 0;
-  u32x4 xp[U][4];
-  auto load_item = [&](int j, u32x4 (&x)[U][4]) {
-    const int n = s_byrank[p + f.P * (j / parts)];
+  const int npre = given && kp > p ? min(GW, (kp - p + f.P - 1) / f.P * parts) : 0;
+  auto load_item = [&](int j, int n, u32x4 (&x)[U][4]) {
     const int h = n / f.W, w = n - h * f.W;
     const int i0 = h & ~1, j0 = w & ~1;
     const int i1 = min(i0 + 1, f.H - 1), j1 = min(j0 + 1, f.W - 1);
@@ -194,122 +165,61 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
     }
   };
 
+  // ---- A. budgets; ranks and gates; the first blocks ----
+  double bd = 0.0, br = 0.0;
+  int o_base = 0, o_next = 0, o_last = 0;
   if constexpr (MODE == kWaveBudget) {
-    if (wave == 0) budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
-  } else if constexpr (MODE == kBlockBudget) {
+    if (wave == 0 && lane < T) {
+      bd = double(f.delta[lane]);
+      br = double(f.rel[lane]);
+    }
+  } else if constexpr (MODE == kOffsets) {
+    o_base = f.offset_in[t];
+    o_next = f.offset_in[t + 1];
+    o_last = f.offset_in[T];
+  } else {
     budget_body<kThreads, kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
   }
-
-  if (wave >= G0) {
-    // ---- A. the frame's scores as selection keys (larger score first, then
-    // the smaller index), their extremes, and the ranks by bins of score ----
+  u32x4 xp[U][4];
+  if (given) {
+    if (wave >= G0) {
+      const int jp = wave - G0;
+      if (jp < npre) load_item(jp, f.byrank[size_t(t) * N + p + f.P * (jp / parts)], xp);
+      for (int n = tid - G0 * kWave; n < N; n += GW * kWave) {
+        rl.rank[n] = f.rank[size_t(t) * N + n];
+        rl.byrank[n] = f.byrank[size_t(t) * N + n];
+        rl.gate[n] = f.gate[size_t(t) * N + n];
+      }
+    } else {
+      budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+    }
+  } else {
+    // the frame's order from its scores, all waves (after the budgets)
+    if constexpr (MODE == kWaveBudget) {
+      if (wave == 0) budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+    }
     const __amdgpu_buffer_rsrc_t ares = make_rsrc(f.tok_score + size_t(t) * N, uint32_t(N) * 4);
     float lo = INFINITY, hi = -INFINITY;
-    for (int n0 = 0; n0 < N; n0 += 4 * gn) {
+    for (int n0 = 0; n0 < N; n0 += 4 * kThreads) {
       float av[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int n = n0 + u * gn + gi;
+        const int n = n0 + u * kThreads + tid;
         av[u] = buf_load_f32(ares, n < N ? n * 4 : kOOB);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int n = n0 + u * gn + gi;
+        const int n = n0 + u * kThreads + tid;
         if (n < N) {
-          s_key[n] = sel_key(av[u], n);
+          rl.key[n] = sel_key(av[u], n);
           lo = fminf(lo, av[u]);
           hi = fmaxf(hi, av[u]);
         }
       }
     }
-    for (int q = gi; q < kBins; q += gn) s_fill[q] = 0;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      lo = fminf(lo, __shfl_xor(lo, m, kWave));
-      hi = fmaxf(hi, __shfl_xor(hi, m, kWave));
-    }
-    if (lane == 0) {
-      s_mm[0][wave] = lo;
-      s_mm[1][wave] = hi;
-    }
-    group_sync();
-    lo = s_mm[0][G0];
-    hi = s_mm[1][G0];
-#pragma unroll
-    for (int w = G0 + 1; w < kNW; ++w) {
-      lo = fminf(lo, s_mm[0][w]);
-      hi = fmaxf(hi, s_mm[1][w]);
-    }
-    const float range = hi - lo;
-    // bin of a score: linear in the score between the extremes, so never
-    // lower for a larger selection key (NaN keys sort outside every number
-    // and go to the end bins; without a finite positive range every number
-    // shares bin 0)
-    const float bscale = range > 0.f && range < INFINITY ? float(kBins) / range : 0.f;
-    auto bin_of = [&](uint64_t key) {
-      const float a = order_value(uint32_t(key >> 12));
-      if (a != a) return (key >> 43) ? kBins - 1 : 0;
-      return min(kBins - 1, max(0, int((a - lo) * bscale)));
-    };
-    for (int n = gi; n < N; n += gn) atomicAdd(&s_fill[bin_of(s_key[n])], 1);
-    group_sync();
-    if (wave == G0) {
-      // start of bin q = tokens in bins above q: a scan over the bins from the top
-      int c[kBins / kWave], sum = 0;
-#pragma unroll
-      for (int e = 0; e < kBins / kWave; ++e) {
-        c[e] = s_fill[kBins - 1 - (lane * (kBins / kWave) + e)];
-        sum += c[e];
-      }
-      int incl = sum;
-#pragma unroll
-      for (int d = 1; d < kWave; d <<= 1) {
-        const int o = __shfl_up(incl, d, kWave);
-        if (lane >= d) incl += o;
-      }
-      int run = incl - sum;
-#pragma unroll
-      for (int e = 0; e < kBins / kWave; ++e) {
-        const int q = kBins - 1 - (lane * (kBins / kWave) + e);
-        s_start[q] = run;
-        run += c[e];
-        s_fill[q] = 0;
-      }
-    }
-    group_sync();
-    for (int n = gi; n < N; n += gn) {
-      const int q = bin_of(s_key[n]);
-      s_sorted[s_start[q] + atomicAdd(&s_fill[q], 1)] = n;
-    }
-    group_sync();
-    // rank = tokens in higher bins + larger keys in the same bin
-    for (int n = gi; n < N; n += gn) {
-      const uint64_t kn = s_key[n];
-      const int q = bin_of(kn);
-      const int j0 = s_start[q], j1 = j0 + s_fill[q];
-      int r = j0;
-      for (int j = j0; j < j1; ++j) r += s_key[s_sorted[j]] > kn;
-      s_rank[n] = r;
-      s_byrank[r] = n;
-    }
-    // gate g = lambda * mean(M) of the 2x2 block of each token (Eq. (13)),
-    // M = min-max of the frame's scores (Eq. (7))
-    auto sal = [&](int n) {
-      const float a = order_value(uint32_t(s_key[n] >> 12));
-      return range > 0.f ? (a - lo) / range : 0.f;
-    };
-    for (int n = gi; n < N; n += gn) {
-      const int h = n / f.W, w = n - h * f.W;
-      const int i0 = h & ~1, j0 = w & ~1;
-      const int i1 = min(i0 + 1, f.H - 1), j1 = min(j0 + 1, f.W - 1);
-      const float m00 = sal(i0 * f.W + j0), m01 = sal(i0 * f.W + j1), m10 = sal(i1 * f.W + j0),
-                  m11 = sal(i1 * f.W + j1);
-      s_gate[n] = f.lam * (0.25f * (((m00 + m01) + m10) + m11));
-    }
-    group_sync();  // every rank known: the first items' reads go out
-    if (wave - G0 < npre) load_item(wave - G0, xp);
+    rank_frame<kThreads>(N, f.H, f.W, f.lam, lo, hi, rl);
   }
-  // LDS-only barriers from here on: the prefetch reads stay in flight
+  // LDS-only barriers from here on: the block reads stay in flight
   lds_barrier();  // ranks, gates and budgets published
 
   long long base, total;
@@ -335,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   int run = 0;  // kept tokens of earlier rounds
   for (int n0 = 0; n0 < N; n0 += kThreads) {
     const int n = n0 + tid;
-    const int r = n < N ? s_rank[n] : 0;
+    const int r = n < N ? rl.rank[n] : 0;
     const bool kept = n < N && r < nt;
     const uint64_t m = __ballot(kept);
     if (lane == 0) s_cnt[wave] = __popcll(m);
@@ -358,8 +268,8 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
     const int r = p + f.P * (j / parts);
     const long long k = base + s_posr[r];
     if (k < 0 || k >= total) return;
-    const int n = s_byrank[r];
-    const float g = s_gate[n];
+    const int n = rl.byrank[r];
+    const float g = rl.gate[n];
     const int h = n / f.W, w = n - h * f.W;
     const float sw = (w & 1) ? -1.f : 1.f;
     const float sh = (h & 1) ? -1.f : 1.f;
@@ -387,11 +297,11 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
     }
     if (j % parts == 0 && lane == 0) f.out_index[k] = t * N + n;
   };
-  // prefetched items whose token is kept, then the rest
+  // blocks read ahead whose token is kept, then the rest
   if (wave >= G0 && wave - G0 < npre && wave - G0 < mine * parts) finish_item(wave - G0, xp);
   for (int j = npre + wave; j < mine * parts; j += kNW) {
     u32x4 x[U][4];
-    load_item(j, x);
+    load_item(j, rl.byrank[p + f.P * (j / parts)], x);
     finish_item(j, x);
   }
 }
@@ -400,7 +310,7 @@ template <typename In, typename Out, int MODE>
 void launch_typed(const wz_config& c, const AssignArgs& a, hipStream_t s) {
   const int nvec = c.C / Vec16<In>::kV;
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * a.P)), block(kThreads);
-  const size_t lds = size_t(c.H) * c.W * 24;  // keys (8 B); rank, token by rank, position, gate (4 B each)
+  const size_t lds = size_t(c.H) * c.W * 24;  // key 8 B; rank, byrank, gate, order / position 4 B
   // one batch of loads per part: two vectors per lane, or one for short rows
   if (nvec <= kWave) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE>), grid, block, lds, s, a);
   else hipLaunchKernelGGL((k_assign_gather<In, Out, kVecPerLane, MODE>), grid, block, lds, s, a);
@@ -429,13 +339,34 @@ int assign_groups_per_frame(const wz_config& c) {
 }
 
 hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* tok_score, const float* frame_rel,
-                                const float* frame_delta, const int32_t* offset_in, int32_t* budget_out,
-                                int32_t* offset_out, void* out_tokens, int32_t* out_index, hipStream_t s) {
+                                const float* frame_delta, const int32_t* offset_in, const Workspace* ws,
+                                int32_t* budget_out, int32_t* offset_out, void* out_tokens, int32_t* out_index,
+                                hipStream_t s) {
   // three quarters of the mean budget: most frames keep at least that many
   const int kpre = int(std::min<long long>(c.H * c.W, 3 * c.B / (4LL * c.T)));
-  AssignArgs a{X,         tok_score, frame_rel, frame_delta, offset_in, budget_out, offset_out, out_tokens,
-               out_index, c.B,       c.T,       c.H,         c.W,       c.C,        assign_groups_per_frame(c),
-               c.levels,  kpre,      c.lambda_, c.tau};
+  AssignArgs a{};
+  a.X = X;
+  a.tok_score = tok_score;
+  a.rel = frame_rel;
+  a.delta = frame_delta;
+  a.offset_in = offset_in;
+  a.rank = ws ? ws->rank : nullptr;
+  a.byrank = ws ? ws->byrank : nullptr;
+  a.gate = ws ? ws->gate : nullptr;
+  a.budget_out = budget_out;
+  a.offset_out = offset_out;
+  a.out_tokens = out_tokens;
+  a.out_index = out_index;
+  a.B = c.B;
+  a.T = c.T;
+  a.H = c.H;
+  a.W = c.W;
+  a.C = c.C;
+  a.P = assign_groups_per_frame(c);
+  a.levels = c.levels;
+  a.kpre = kpre;
+  a.lam = c.lambda_;
+  a.tau = c.tau;
   if (offset_in) launch_mode<kOffsets>(c, a, s);
   else if (c.T <= kWave) launch_mode<kWaveBudget>(c, a, s);
   else if (c.T <= kFusedTMax) launch_mode<kBlockBudget>(c, a, s);
