@@ -1,5 +1,5 @@
 // Per-frame finish of stage 1, and the selection order of stage 3, in one
-// launch of 1024-thread workgroups with up to three roles per frame t:
+// launch with up to two workgroups per frame t:
 //   scores  a_{t,n} = max_j (sum_s S_s[n][j]) / (|q_j| |x_n|)   (several
 //           channel slices; with one slice the streaming pass wrote a_{t,n}
 //           itself), the slices' partials added in slice order;
@@ -12,17 +12,19 @@
 //           is the sum's), cos := 0 (a = 0, r = 0, delta = 1) when a vector
 //           is zero.
 // The scores and the order share a workgroup (the order needs every score of
-// the frame); the lead has its own.  Every partial is added in a fixed order,
-// so results do not depend on timing, and first loads are issued before the
-// first one is used.
+// the frame; 1024 threads when the scores come from several slices' partials,
+// else 256).  The lead has its own workgroup, placed on the
+// XCD whose workgroups wrote the frame's partial channel sums.  Every partial
+// is added in a fixed order, so results do not depend on timing, and first
+// loads are issued before the first one is used.
 #include "wz_rank.h"
 
 namespace wz {
 namespace {
 
 constexpr int kQMax = 1024;
-constexpr int kThreads = 1024;
-constexpr int kNW = kThreads / kWave;
+constexpr int kPartThreads = 1024;  // workgroup size when scores come from slice partials
+constexpr int kThreads = 256;       // otherwise
 
 struct FrameArgs {
   const float* s_part;     // [T][S][N][QP]   (several slices)
@@ -43,7 +45,9 @@ struct FrameArgs {
 };
 
 // scores (and order) of frame t
+template <int NTH>
 __device__ void scores_role(const FrameArgs& f, int t) {
+  constexpr int kNW = NTH / kWave;
   constexpr int TPT = 4;   // threads per token
   constexpr int LB = 8;    // partial-score vectors in flight per thread
   __shared__ float s_rq[kQMax];
@@ -64,17 +68,18 @@ __device__ void scores_role(const FrameArgs& f, int t) {
   float lo = INFINITY, hi = -INFINITY;
 
   if (S == 1) {
+    if (!f.order) return;
     const __amdgpu_buffer_rsrc_t ares = make_rsrc(f.tok_score + size_t(t) * N, uint32_t(N) * 4);
-    for (int n0 = 0; n0 < N; n0 += 4 * kThreads) {
+    for (int n0 = 0; n0 < N; n0 += 4 * NTH) {
       float av[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int n = n0 + u * kThreads + tid;
+        const int n = n0 + u * NTH + tid;
         av[u] = buf_load_f32(ares, n < N ? n * 4 : kOOB);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int n = n0 + u * kThreads + tid;
+        const int n = n0 + u * NTH + tid;
         if (n < N) {
           rl.key[n] = sel_key(av[u], n);
           lo = fminf(lo, av[u]);
@@ -110,7 +115,7 @@ __device__ void scores_role(const FrameArgs& f, int t) {
         gx[k] = buf_load_f32(gres, (part == 0 && n < N && s0 + k < S) ? ((s0 + k) * N + n) * 4 : kOOB);
     };
     load_g(tid / TPT, 0);
-    for (int j = tid; j < Q; j += kThreads) {
+    for (int j = tid; j < Q; j += NTH) {
       float qq = 0.f;
       for (int s0 = 0; s0 < S; s0 += SB) {
         float qv[SB];
@@ -123,7 +128,7 @@ __device__ void scores_role(const FrameArgs& f, int t) {
       s_rq[j] = qq > 0.f ? 1.0f / sqrtf(qq) : 0.f;
     }
     lds_barrier();
-    for (int n0 = 0; n0 < N; n0 += kThreads / TPT) {
+    for (int n0 = 0; n0 < N; n0 += NTH / TPT) {
       const int n = n0 + tid / TPT;
       if (n0 > 0) {
 #pragma unroll
@@ -174,9 +179,9 @@ __device__ void scores_role(const FrameArgs& f, int t) {
     }
   }
   if (!f.order) return;
-  rank_frame<kThreads>(N, f.H, f.W, f.lam, lo, hi, rl);
+  rank_frame<NTH>(N, f.H, f.W, f.lam, lo, hi, rl);
   lds_barrier();
-  for (int n = tid; n < N; n += kThreads) {
+  for (int n = tid; n < N; n += NTH) {
     f.rank[size_t(t) * N + n] = rl.rank[n];
     f.byrank[size_t(t) * N + n] = rl.byrank[n];
     f.gate[size_t(t) * N + n] = rl.gate[n];
@@ -184,8 +189,10 @@ __device__ void scores_role(const FrameArgs& f, int t) {
 }
 
 // r_t and delta_t of frame t
+template <int NTH>
 __device__ void lead_role(const FrameArgs& f, int t) {
-  constexpr int PF = 1;  // channel-sum vectors per thread issued up front
+  constexpr int kNW = NTH / kWave;
+  constexpr int TB = 4;  // tiles of the channel sums loaded at once
   __shared__ double s_red[4][kNW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int C = f.C, Q = f.Q, S = f.slices, tiles = f.tiles, K = tiles * S, C4 = C / 4;
@@ -195,16 +202,37 @@ __device__ void lead_role(const FrameArgs& f, int t) {
   const __amdgpu_buffer_rsrc_t qgres = make_rsrc(f.qg_part + size_t(t) * S * Q, uint32_t(S) * Q * 4);
   const __amdgpu_buffer_rsrc_t sgres = make_rsrc(f.sig_part + size_t(t) * K * Q, uint32_t(K) * Q * 4);
 
-  f32x4 pa[PF], pb[PF];  // tile 0 of p_{t-1} and p_t
+  // channel sums p_{t-1} (a) and p_t (b) of channel vectors c4 + NTH * i, i < PF:
+  // tiles added in order, the loads of TB tiles of all PF vectors in flight at once
+  constexpr int PF = NTH <= 256 ? 4 : 1;
+  auto sums = [&](int c4, f32x4 (&x)[PF], f32x4 (&y)[PF]) {
 #pragma unroll
-  for (int i = 0; i < PF; ++i) {
-    const int c4 = tid + i * kThreads;
-    pa[i] = buf_load_f32x4(pares, c4 < C4 ? c4 * 16 : kOOB);
-    pb[i] = buf_load_f32x4(pbres, c4 < C4 ? c4 * 16 : kOOB);
-  }
-  // sigma_j / |q_j| for query j = tid
+    for (int i = 0; i < PF; ++i) x[i] = y[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < tiles; k0 += TB) {
+      f32x4 xa[PF][TB], yb[PF][TB];
+#pragma unroll
+      for (int i = 0; i < PF; ++i)
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+          const int c = c4 + NTH * i;
+          const int off = (c < C4 && k0 + k < tiles) ? ((k0 + k) * C + c * 4) * 4 : kOOB;
+          xa[i][k] = buf_load_f32x4(pares, off);
+          yb[i][k] = buf_load_f32x4(pbres, off);
+        }
+#pragma unroll
+      for (int i = 0; i < PF; ++i)
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+          if (k0 + k < tiles) {
+            x[i] += xa[i][k];
+            y[i] += yb[i][k];
+          }
+        }
+    }
+  };
+  // sigma_j / |q_j| for query j
   double rbest = -INFINITY;
-  for (int j = tid; j < Q; j += kThreads) {
+  for (int j = tid; j < Q; j += NTH) {
     float qq = 0.f, sg = 0.f;
     for (int k0 = 0; k0 < K; k0 += 4) {
       float a[4], b[4];
@@ -223,28 +251,18 @@ __device__ void lead_role(const FrameArgs& f, int t) {
     const float rq = qq > 0.f ? 1.0f / sqrtf(qq) : 0.f;
     rbest = fmax(rbest, double(sg) * rq);
   }
-  // channel sums p_{t-1} (a) and p_t (b), tiles added in order
   double ab = 0.0, aa = 0.0, bb = 0.0;
-  for (int c0 = 0; c0 < C4; c0 += PF * kThreads) {
+  for (int c4 = tid; c4 < C4; c4 += PF * NTH) {
+    f32x4 x[PF], y[PF];
+    sums(c4, x, y);
 #pragma unroll
-    for (int i = 0; i < PF; ++i) {
-      const int c4 = c0 + tid + i * kThreads;
-      f32x4 x = pa[i], y = pb[i];
-      if (c0 > 0) {
-        x = buf_load_f32x4(pares, c4 < C4 ? c4 * 16 : kOOB);
-        y = buf_load_f32x4(pbres, c4 < C4 ? c4 * 16 : kOOB);
-      }
-      for (int k = 1; k < tiles; ++k) {
-        x += buf_load_f32x4(pares, c4 < C4 ? (k * C + c4 * 4) * 4 : kOOB);
-        y += buf_load_f32x4(pbres, c4 < C4 ? (k * C + c4 * 4) * 4 : kOOB);
-      }
+    for (int i = 0; i < PF; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        ab += double(x[e]) * y[e];
-        aa += double(x[e]) * x[e];
-        bb += double(y[e]) * y[e];
+        ab += double(x[i][e]) * y[i][e];
+        aa += double(x[i][e]) * x[i][e];
+        bb += double(y[i][e]) * y[i][e];
       }
-    }
   }
   ab = wave_sum_f64(ab);
   aa = wave_sum_f64(aa);
@@ -273,10 +291,16 @@ __device__ void lead_role(const FrameArgs& f, int t) {
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_frame(const FrameArgs f) {
-  const int t = blockIdx.x / f.roles, role = blockIdx.x % f.roles;
-  if (role == f.roles - 1) lead_role(f, t);
-  else scores_role(f, t);
+// Workgroup b: frame t = (b / 8 / roles) * 8 + b % 8 (so every workgroup of a
+// frame runs on the XCD that streamed it), role (b / 8) % roles; the last role
+// is the lead.
+template <int NTH>
+__global__ __launch_bounds__(NTH) void k_frame(const FrameArgs f) {
+  const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
+  const int t = (slot / f.roles) * kXcds + xcd, role = slot % f.roles;
+  if (t >= f.T) return;
+  if (role == f.roles - 1) lead_role<NTH>(f, t);
+  else scores_role<NTH>(f, t);
 }
 
 }  // namespace
@@ -291,7 +315,9 @@ hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_scor
                c.W,       c.C,        c.Q,          qpad(c.Q),   pl.tiles,     pl.slices, order ? 1 : 0,
                roles,     c.lambda_};
   const size_t lds = roles == 2 ? size_t(N) * 24 : 0;  // key 8 B; rank, byrank, gate, bin order 4 B
-  hipLaunchKernelGGL(k_frame, dim3(c.T * roles), dim3(kThreads), lds, s, fa);
+  const dim3 grid((c.T + kXcds - 1) / kXcds * kXcds * roles);
+  if (pl.slices > 1) hipLaunchKernelGGL((k_frame<kPartThreads>), grid, dim3(kPartThreads), lds, s, fa);
+  else hipLaunchKernelGGL((k_frame<kThreads>), grid, dim3(kThreads), lds, s, fa);
   return hipGetLastError();
 }
 
