@@ -38,13 +38,13 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 }
 
 // ---------------------------------------------------------------------------
-// Decomposition of the relevance pass.
-//
-// MFMA paths: a workgroup owns one token tile of a frame (up to 256 tokens)
-// and one slice of channels.  Tiles cover whole frames when H*W <= 256, so the
-// query, which every workgroup must read for its channels, is read about once
-// per frame; channel slices give the grid enough workgroups.  Vector-ALU path:
-// tiles of up to 32 tokens, all channels.
+// Decomposition of the relevance pass (shapes and limits; the kernels'
+// comments give the details).  Token-tiled path: tiles of at most 64 tokens
+// with every channel.  MFMA-layout path: a token tile of a frame (up to 256
+// tokens) and one slice of channels; tiles cover whole frames when H*W <= 256,
+// so the query, which every workgroup must read for its channels, is read
+// about once per frame, and channel slices give the grid enough workgroups.
+// Vector-ALU path: tiles of up to 32 tokens, all channels.
 // ---------------------------------------------------------------------------
 constexpr int kXcds = 8;          // MI355X: workgroups are dealt to the 8 XCDs round robin
 constexpr int kCUs = 256;
@@ -57,19 +57,11 @@ constexpr int kTokMax = 4096;     // validated bound on tokens per frame
 inline int qpad(int Q) { return (Q + 3) & ~3; }
 
 // Streaming kernels of the relevance pass, chosen by shape:
-//   kRelLds  bf16, Q <= 32: coalesced loads transposed through LDS, MFMA;
+//   kRelTok  bf16, Q <= 32: token tiles with every channel, LDS-transposed MFMA;
 //   kRelMfma bf16, Q > 32, frames of >= 49 tokens: MFMA-layout loads;
 //   kRelValu everything else (fp32 inputs, small frames with many queries).
-enum RelKind { kRelValu = 0, kRelMfma = 1, kRelLds = 2, kRelTok = 3 };
+enum RelKind { kRelValu = 0, kRelMfma = 1, kRelTok = 2 };
 RelKind relevance_kind(const wz_config& c);
-
-// LDS-transpose kernel limits: up to 8 waves of 32 tokens per tile; a slice
-// is whole 128-channel chunks, with the query slice (Q padded to 16 or 32)
-// resident in LDS.
-constexpr int kLdsChunk = 128;        // channels per chunk (256 bytes of a bf16 row)
-constexpr int kLdsWavesMax = 8;
-constexpr int kLdsSliceMax1 = 1024;   // slice channels at most, queries of <= 16 tokens
-constexpr int kLdsSliceMax2 = 896;    // ... of 17..32 tokens
 
 struct RelPlan {
   RelKind kind;
@@ -80,8 +72,8 @@ struct RelPlan {
   int kc;           // channels per slice
   int grid;         // workgroups: frames rounded up to a multiple of kXcds, x tiles x slices
   int threads;      // threads per workgroup
-  int ipc;          // kRelLds: load instructions per chunk and wave (rows per wave / 4)
-  int ntg;          // kRelLds: 16-column query tiles
+  int ipc;          // kRelTok: row load instructions per chunk (tile rows / 8)
+  int ntg;          // kRelTok: 16-column query tiles
 };
 
 inline RelPlan relevance_plan(const wz_config& c) {
@@ -98,28 +90,6 @@ inline RelPlan relevance_plan(const wz_config& c) {
     p.slices = 1;
     p.kc = c.C;
     p.threads = 8 * 64;
-  } else if (p.kind == kRelLds) {
-    const int cap = 32 * kLdsWavesMax;
-    p.tiles = (N + cap - 1) / cap;
-    p.tile_tokens = (N + p.tiles - 1) / p.tiles;
-    const int nw = (p.tile_tokens + 31) / 32;
-    const int per = (p.tile_tokens + nw - 1) / nw;
-    p.ipc = per <= 28 ? 7 : 8;
-    p.threads = nw * 64;
-    p.ntg = c.Q <= 16 ? 1 : 2;
-    p.mt = 0;
-    const int chunks = (c.C + kLdsChunk - 1) / kLdsChunk;
-    const int cmax = (p.ntg == 1 ? kLdsSliceMax1 : kLdsSliceMax2) / kLdsChunk;
-    // fewest slices the LDS allows; more while the grid is short of one
-    // workgroup per CU, keeping per-slice partial scores (4*Q bytes a
-    // token) under a quarter of X (2*C bytes a token)
-    const int qp = (c.Q + 3) & ~3;
-    const int smax = std::max(1, c.C / (8 * qp));
-    int S = (chunks + cmax - 1) / cmax;
-    while (S < chunks && S < smax && (long long)c.T * p.tiles * S < kCUs) ++S;
-    const int cps = (chunks + S - 1) / S;
-    p.kc = cps * kLdsChunk;
-    p.slices = (chunks + cps - 1) / cps;
   } else if (p.kind == kRelMfma) {
     const int cap = 16 * kMaxWaves;
     p.tiles = (N + cap - 1) / cap;

@@ -111,103 +111,3 @@ __device__ void rank_frame(int N, int H, int W, float lam, float lo, float hi, c
 
 }  // namespace
 }  // namespace wz
-
-namespace wz {
-namespace {
-
-// The same order computed by ONE wave (no workgroup barrier), for frames of
-// at most 64 * TPL tokens: each lane holds TPL keys; bins, counts and the
-// bin order sit in LDS and are ordered by wave-level fences.
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
-
-template <int TPL>
-__device__ void rank_frame_wave(int N, int H, int W, float lam, const RankLds& s) {
-  const int lane = threadIdx.x & 63;
-  uint64_t k[TPL];
-  float lo = INFINITY, hi = -INFINITY;
-#pragma unroll
-  for (int u = 0; u < TPL; ++u) {
-    const int n = lane + kWave * u;
-    k[u] = n < N ? s.key[n] : 0ull;
-    if (n < N) {
-      const float a = order_value(uint32_t(k[u] >> 12));
-      lo = fminf(lo, a);
-      hi = fmaxf(hi, a);
-    }
-  }
-  lo = wave_min_f32(lo);
-  hi = wave_max_f32(hi);
-  for (int q = lane; q < kBins; q += kWave) s.fill[q] = 0;
-  const float range = hi - lo;
-  const float bscale = range > 0.f && range < INFINITY ? float(kBins) / range : 0.f;
-  auto bin_of = [&](uint64_t key) {
-    const float a = order_value(uint32_t(key >> 12));
-    if (a != a) return (key >> 43) ? kBins - 1 : 0;
-    return min(kBins - 1, max(0, int((a - lo) * bscale)));
-  };
-  int b[TPL];
-#pragma unroll
-  for (int u = 0; u < TPL; ++u) b[u] = bin_of(k[u]);
-  wave_sync_lds();
-#pragma unroll
-  for (int u = 0; u < TPL; ++u)
-    if (lane + kWave * u < N) atomicAdd(&s.fill[b[u]], 1);
-  wave_sync_lds();
-  {
-    constexpr int PL = kBins / kWave;
-    int c[PL], sum = 0;
-#pragma unroll
-    for (int e = 0; e < PL; ++e) {
-      c[e] = s.fill[kBins - 1 - (lane * PL + e)];
-      sum += c[e];
-    }
-    int run = wave_incl_scan_i32(sum) - sum;
-#pragma unroll
-    for (int e = 0; e < PL; ++e) {
-      const int q = kBins - 1 - (lane * PL + e);
-      s.start[q] = run;
-      run += c[e];
-      s.fill[q] = 0;
-    }
-  }
-  wave_sync_lds();
-#pragma unroll
-  for (int u = 0; u < TPL; ++u) {
-    const int n = lane + kWave * u;
-    if (n < N) s.order[s.start[b[u]] + atomicAdd(&s.fill[b[u]], 1)] = n;
-  }
-  wave_sync_lds();
-#pragma unroll
-  for (int u = 0; u < TPL; ++u) {
-    const int n = lane + kWave * u;
-    if (n < N) {
-      const int j0 = s.start[b[u]], j1 = j0 + s.fill[b[u]];
-      int r = j0;
-      for (int j = j0; j < j1; ++j) r += s.key[s.order[j]] > k[u];
-      s.rank[n] = r;
-      s.byrank[r] = n;
-    }
-  }
-  auto sal = [&](int n) {
-    const float a = order_value(uint32_t(s.key[n] >> 12));
-    return range > 0.f ? (a - lo) / range : 0.f;
-  };
-#pragma unroll
-  for (int u = 0; u < TPL; ++u) {
-    const int n = lane + kWave * u;
-    if (n < N) {
-      const int h = n / W, w = n - h * W;
-      const int i0 = h & ~1, j0 = w & ~1;
-      const int i1 = min(i0 + 1, H - 1), j1 = min(j0 + 1, W - 1);
-      const float m00 = sal(i0 * W + j0), m01 = sal(i0 * W + j1), m10 = sal(i1 * W + j0), m11 = sal(i1 * W + j1);
-      s.gate[n] = lam * (0.25f * (((m00 + m01) + m10) + m11));
-    }
-  }
-  wave_sync_lds();
-}
-
-}  // namespace
-}  // namespace wz

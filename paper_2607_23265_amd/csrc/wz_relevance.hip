@@ -4,26 +4,28 @@
 //     x . q_j  (all j),  |x|^2,  |q_j|^2,
 // and per frame the channel sums p_t = sum_n x_{t,n} (the mean's cosine is the
 // sum's) and sigma_j = sum_n x_{t,n} . q_j = p_t . q_j.  It writes them per
-// work unit; the frame kernel adds the units' partials in a fixed order and
-// forms a_{t,n}, r_t and delta_t.
+// work unit; the per-frame kernel adds the units' partials in a fixed order
+// and forms r_t and delta_t (and a_{t,n} when a unit holds only some channels).
 //
-// Work decomposition (MFMA path: bf16 inputs, Q >= 16, frames of >= 49 tokens).
-// A workgroup owns one token tile of one frame (the whole frame when
-// H*W <= 256; each wave holds two 16-row MFMA tiles) and one slice of at most
-// 32 x 32 channels.  At the start it stages the slice of the query (MFMA B
-// layout) in LDS, where every wave reads it; X streams from HBM into A-operand
-// registers through an R-deep ring of 16-byte buffer loads with no barrier in
-// the loop.  Per 32-channel step each wave runs v_mfma_f32_16x16x32_bf16 for
-//     S += X Q^T      (the relevance contraction),
-//     G += X X^T      (diagonal: |x|^2),
-//     P += X I        (identity columns: channel sums of its tokens),
-// and one wave per step adds the query's Gram matrix (diagonal: |q_j|^2), so
-// norms and pooling cost no vector-ALU work.  The waves' channel sums meet in
-// LDS and are added in wave order.  With one slice the workgroup also finishes
-// its tokens' a_{t,n}; with several it writes the partial x . q_j and |x|^2.
-//
-// Vector-ALU path (fp32 inputs, Q < 16 or tiny frames): tiles of up to 32
-// tokens over all channels, one wave per token, wave-reduced dot products.
+// Three decompositions, chosen by shape:
+//  * token tiles (bf16, Q <= 32; below): a workgroup owns up to 64 tokens of a
+//    frame with every channel, so a_{t,n} is final in the pass;
+//  * MFMA layout (bf16, Q > 32, frames of >= 49 tokens): a workgroup owns one
+//    token tile of one frame (the whole frame when H*W <= 256; each wave holds
+//    two 16-row MFMA tiles) and one slice of at most 32 x 32 channels.  It
+//    stages the slice of the query (MFMA B layout) in LDS, where every wave
+//    reads it; X streams into A-operand registers through an R-deep ring of
+//    16-byte buffer loads with no barrier in the loop.  Per 32-channel step
+//    each wave runs v_mfma_f32_16x16x32_bf16 for
+//        S += X Q^T      (the relevance contraction),
+//        G += X X^T      (diagonal: |x|^2),
+//        P += X I        (identity columns: channel sums of its tokens),
+//    and one wave per step adds the query's Gram matrix (diagonal: |q_j|^2).
+//    With one slice the workgroup also finishes its tokens' a_{t,n}; with
+//    several it writes the partial x . q_j and |x|^2;
+//  * vector ALU (fp32 inputs, small frames with many queries): tiles of up to
+//    32 tokens over all channels, one wave per token, wave-reduced dot
+//    products.
 #include <type_traits>
 
 #include "wz_device.h"
@@ -295,22 +297,7 @@ __global__ __launch_bounds__(kMaxWaves / kTilesPerWave * 64) void k_relevance_mf
   }
 }
 
-// ---------------------------------------------------------------------------
-// LDS-transpose path (bf16, Q <= 32)
-// ---------------------------------------------------------------------------
-// A workgroup owns one token tile of one frame (one wave per 4*IPC tokens) and
-// one slice of whole 128-channel chunks.  A load instruction covers 4 token
-// rows x 256 contiguous bytes, so every access is a whole 128-byte line; the
-// MFMA operand layout (16 rows x 64 bytes per register) is built afterwards in
-// a wave-private LDS buffer, written with 16-byte units XOR-swizzled by row so
-// that neither side conflicts on banks.  The query slice is staged once per
-// workgroup in LDS in the MFMA B layout.  Per chunk a wave
-//   1. stores its X registers to its LDS buffer and, from the same registers,
-//      accumulates |x|^2 and the channel sums with bf16 dot2 instructions;
-//   2. re-issues the ring slot for chunk c + R;
-//   3. runs four 32-channel steps of S += X Q^T (v_mfma_f32_16x16x32_bf16)
-//      on two 16-row tiles, reading A from its buffer and B from the query.
-// No barrier sits in the chunk loop: each wave reads only what it wrote.
+// bf16 dot2 helpers of the token-tiled path
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
@@ -322,290 +309,6 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
 constexpr uint32_t kBf16OneLo = 0x00003F80u;  // bf16 pair (1, 0)
 constexpr uint32_t kBf16OneHi = 0x3F800000u;  // bf16 pair (0, 1)
 
-template <int NTG>
-struct LdsShape {
-  static constexpr int kSteps = (NTG == 1 ? kLdsSliceMax1 : kLdsSliceMax2) / 32;  // 32-channel steps per slice
-};
-
-template <int NTG, int IPC, int R>
-__global__ __launch_bounds__(kLdsWavesMax * 64) void k_relevance_lds(const uint16_t* __restrict__ X,
-                                                                    const uint16_t* __restrict__ query,
-                                                                    int tile_tokens, int kc, StreamArgs f) {
-  constexpr int KSL = LdsShape<NTG>::kSteps;
-  constexpr int NCHM = KSL * 32 / kLdsChunk;  // chunks per slice at most
-  constexpr int RW = 4 * IPC;  // token rows per wave
-  constexpr int QB = 8;        // query units staged per thread per batch
-  __shared__ u32x4 s_q[KSL][NTG][kWave];                // query slice, MFMA B layout
-  __shared__ u32x4 s_x[kLdsWavesMax][32][16];           // per-wave chunk, 16-byte units swizzled by row
-  __shared__ float s_p[kLdsWavesMax][KSL * 32];         // per-wave channel sums of the slice
-  __shared__ float s_colw[kLdsWavesMax][NTG * 16];      // per-wave column sums of S
-  __shared__ float s_qgw[kLdsWavesMax][NTG * 16];       // per-wave |q_j|^2 partials
-  __shared__ float s_xt[kLdsWavesMax * 32];             // |x| of the tile's tokens (one slice)
-  __shared__ float s_rq[NTG * 16];                      // 1/|q_j| (one slice)
-
-  int t, tile, sl;
-  unit_of_block(blockIdx.x, f.tiles, f.slices, t, tile, sl);
-  if (t >= f.T) return;
-  const int N = f.N, C = f.C, Q = f.Q, QP = f.QP, S = f.slices;
-  const int tok0 = tile * tile_tokens;
-  const int TM = min(tile_tokens, N - tok0);
-  const int tid = threadIdx.x, nthreads = blockDim.x;
-  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), nw = nthreads >> 6;
-  const int r16 = lane & 15, grp = lane >> 4;
-  const int c_lo = sl * kc, c_hi = min(C, c_lo + kc);
-  const int nch = (c_hi - c_lo + kLdsChunk - 1) / kLdsChunk;  // chunks of this slice
-  const int wrow0 = wave * RW;                                 // first tile row of this wave
-
-  // X of this wave's rows only: a row past the tile falls outside the resource
-  const int wrows = max(0, min(RW, TM - wrow0));
-  const __amdgpu_buffer_rsrc_t xres =
-      make_rsrc_uniform(X + (size_t(t) * N + tok0 + min(wrow0, TM)) * C, uint32_t(wrows) * C * 2);
-  const __amdgpu_buffer_rsrc_t qres = make_rsrc_uniform(query, uint32_t(Q) * C * 2);
-
-  // X ring: slot r holds chunks c = r (mod R); register k of a slot is row
-  // wrow0 + 4k + grp, channels c_lo + 128c + 8*r16 .. +7.  An invalid chunk
-  // or channel adds kOOB, which puts the offset past the resource.
-  const uint32_t rowstride = uint32_t(4 * C * 2);
-  const uint32_t rowbase = uint32_t(grp * C * 2);
-  bf16x8 a[R][IPC];
-  auto issue = [&](int c, bf16x8 (&dst)[IPC]) {
-    const int ch = c_lo + c * kLdsChunk + 8 * r16;
-    const uint32_t base = rowbase + ((c < nch && ch < c_hi) ? uint32_t(ch * 2) : uint32_t(kOOB));
-#pragma unroll
-    for (int k = 0; k < IPC; ++k) dst[k] = buf_load_bf16x8(xres, int(base + k * rowstride));
-  };
-  // query slice into LDS: unit u -> step u / (64 NTG), tile (u / 64) % NTG,
-  // lane u % 64.  nthreads is a multiple of 64, so a thread's units all
-  // belong to the lane tid % 64, i.e. to query j = 16 n + tid % 16; it adds
-  // their |q_j|^2 share on the way.  The first batch of query loads goes out
-  // before the X ring: loads complete in order, so waiting for the query then
-  // leaves the ring in flight.
-  const int qunits = nch * 4 * NTG * kWave;
-  float qq[NTG];
-#pragma unroll
-  for (int n = 0; n < NTG; ++n) qq[n] = 0.f;
-  u32x4 qv[QB];
-  auto load_query = [&](int u0) {
-#pragma unroll
-    for (int k = 0; k < QB; ++k) {
-      const int u = u0 + tid + k * nthreads;
-      const int l = u & 63, n = (u >> 6) % NTG, ks = u / (NTG * kWave);
-      const int j = n * 16 + (l & 15);
-      const int c = c_lo + ks * 32 + (l >> 4) * 8;
-      const bool ok = u < qunits && j < Q && c < c_hi;
-      qv[k] = buf_load_u32x4(qres, ok ? (j * C + c) * 2 : kOOB);
-    }
-  };
-  auto store_query = [&](int u0) {
-#pragma unroll
-    for (int k = 0; k < QB; ++k) {
-      const int u = u0 + tid + k * nthreads;
-      if (u < qunits) (&s_q[0][0][0])[u] = qv[k];
-      float d = 0.f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) d = dot2(qv[k][e], qv[k][e], d);
-#pragma unroll
-      for (int n = 0; n < NTG; ++n) qq[n] += ((u >> 6) % NTG == n) ? d : 0.f;
-    }
-  };
-  load_query(0);
-#pragma unroll
-  for (int r = 0; r < R && r < NCHM; ++r) issue(r, a[r]);
-  store_query(0);
-  for (int u0 = QB * nthreads; u0 < qunits; u0 += QB * nthreads) {
-    load_query(u0);
-    store_query(u0);
-  }
-  // steps past the slice run MFMAs on zero X; their query operands must be
-  // finite too (0 * NaN from stale LDS would be NaN), so they are zeroed
-  for (int u = qunits + tid; u < NCHM * 4 * NTG * kWave; u += nthreads) (&s_q[0][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
-  // |q_j|^2 shares: the four lane groups of the wave now, the waves in the epilogue
-#pragma unroll
-  for (int n = 0; n < NTG; ++n) {
-    const float q = row_sum4(qq[n]);
-    if (lane < 16) s_qgw[wave][n * 16 + lane] = q;
-  }
-  // rows this wave never loads (4*IPC..31) stay zero in its buffer
-  if (IPC < 8) s_x[wave][RW + (lane >> 4)][lane & 15] = u32x4{0u, 0u, 0u, 0u};
-  lds_barrier();
-
-  f32x4 Sacc[2][NTG];
-  float xx[IPC];
-#pragma unroll
-  for (int n = 0; n < NTG; ++n) Sacc[0][n] = Sacc[1][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int k = 0; k < IPC; ++k) xx[k] = 0.f;
-
-  uint32_t one_lo = kBf16OneLo, one_hi = kBf16OneHi;
-  asm volatile("" : "+v"(one_lo), "+v"(one_hi));  // opaque: keeps them out of inline constants
-
-  // Fully unrolled over the slice's chunk limit and free of branches, so the
-  // scheduler can overlap each step's LDS reads with the previous MFMAs (a
-  // runtime trip count makes the compiler rotate the ring through register
-  // copies at the back-edge, which waits for every load in flight).  Chunks
-  // past nch load zeros: their stores, sums and MFMAs add nothing.
-#pragma unroll
-  for (int c0 = 0; c0 < NCHM; c0 += R) {
-#pragma unroll
-    for (int r = 0; r < R && c0 + r < NCHM; ++r) {
-      const int c = c0 + r;
-      // chunk boundary: nothing moves across it, which bounds register pressure
-      __builtin_amdgcn_sched_barrier(0);
-      {
-        float cs[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) cs[e] = 0.f;
-#pragma unroll
-        for (int k = 0; k < IPC; ++k) {
-          const int lr = 4 * k + grp;
-          const u32x4 v = __builtin_bit_cast(u32x4, a[r][k]);
-          s_x[wave][lr][r16 ^ (lr & 15)] = v;
-#pragma unroll
-          for (int d = 0; d < 4; ++d) {
-            xx[k] = dot2(v[d], v[d], xx[k]);
-            cs[2 * d] = dot2(v[d], one_lo, cs[2 * d]);
-            cs[2 * d + 1] = dot2(v[d], one_hi, cs[2 * d + 1]);
-          }
-        }
-        // channel sums over the wave's rows: the four row groups, in order
-#pragma unroll
-        for (int e = 0; e < 8; ++e) cs[e] = row_sum4(cs[e]);
-        if (lane < 16) {
-          float* dst = &s_p[wave][c * kLdsChunk + 8 * lane];
-          *reinterpret_cast<f32x4*>(dst) = f32x4{cs[0], cs[1], cs[2], cs[3]};
-          *reinterpret_cast<f32x4*>(dst + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
-        }
-      }
-      if (c + R < NCHM) issue(c + R, a[r]);
-      {
-#pragma unroll
-        for (int st = 0; st < 4; ++st) {
-          const int ks = 4 * c + st;
-          bf16x8 A[2], B[NTG];
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-            A[i] = __builtin_bit_cast(bf16x8, s_x[wave][16 * i + r16][(4 * st + grp) ^ r16]);
-#pragma unroll
-          for (int n = 0; n < NTG; ++n) B[n] = __builtin_bit_cast(bf16x8, s_q[ks][n][lane]);
-#pragma unroll
-          for (int n = 0; n < NTG; ++n)
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-              Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[i], B[n], Sacc[i][n], 0, 0, 0);
-        }
-      }
-    }
-  }
-
-  // ---- epilogue ----
-  // With one workgroup per CU, all finishing together, the epilogue's latency
-  // is the kernel's tail: stores that need no other wave go out before the
-  // barrier, and the cross-wave sums issue all their LDS reads at once.
-  // |x|^2 of row wrow0 + 4k + grp over the slice: the 16 lanes of the group
-#pragma unroll
-  for (int k = 0; k < IPC; ++k) xx[k] = row_sum16(xx[k]);
-#pragma unroll
-  for (int n = 0; n < NTG; ++n) {
-    float v = 0.f;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) v += (Sacc[i][n][0] + Sacc[i][n][1]) + (Sacc[i][n][2] + Sacc[i][n][3]);
-    v = row_sum4(v);
-    if (lane < 16) s_colw[wave][n * 16 + lane] = v;
-  }
-  // (plain stores under lane predicates: a buffer descriptor built from
-  // values that meet divergent control flow would need a waterfall loop)
-  if (S > 1) {
-    float* gdst = f.g_part + (size_t(t) * S + sl) * N + tok0;
-#pragma unroll
-    for (int k = 0; k < IPC; ++k) {
-      const int r = wrow0 + 4 * k + grp;
-      if (r16 == 0 && r < TM) gdst[r] = xx[k];
-    }
-    float* sdst = f.s_part + ((size_t(t) * S + sl) * N + tok0) * QP;
-#pragma unroll
-    for (int n = 0; n < NTG; ++n) {
-      const int j = n * 16 + r16;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int lr = 16 * i + 4 * grp + e, r = wrow0 + lr;
-          if (lr < RW && r < TM && j < Q) sdst[r * QP + j] = Sacc[i][n][e];
-        }
-    }
-  } else if (r16 == 0) {
-#pragma unroll
-    for (int k = 0; k < IPC; ++k) s_xt[wrow0 + 4 * k + grp] = sqrtf(xx[k]);
-  }
-  lds_barrier();
-  // channel sums of the slice, |q_j|^2 and sigma_j: waves added in order
-  float* pdst = f.pool_part + (size_t(t) * f.tiles + tile) * C + c_lo;
-  for (int c = tid; c < c_hi - c_lo; c += nthreads) {
-    float v[kLdsWavesMax];
-#pragma unroll
-    for (int w = 0; w < kLdsWavesMax; ++w) v[w] = s_p[w][c];
-    float sum = 0.f;
-#pragma unroll
-    for (int w = 0; w < kLdsWavesMax; ++w) sum += w < nw ? v[w] : 0.f;
-    pdst[c] = sum;
-  }
-  if (tid < NTG * 16) {
-    const int j = tid;
-    float vq[kLdsWavesMax], vs[kLdsWavesMax];
-#pragma unroll
-    for (int w = 0; w < kLdsWavesMax; ++w) {
-      vq[w] = s_qgw[w][j];
-      vs[w] = s_colw[w][j];
-    }
-    float qgs = 0.f, sg = 0.f;
-#pragma unroll
-    for (int w = 0; w < kLdsWavesMax; ++w) {
-      qgs += w < nw ? vq[w] : 0.f;
-      sg += w < nw ? vs[w] : 0.f;
-    }
-    if (j < Q) {
-      if (S == 1) s_rq[j] = qgs > 0.f ? 1.0f / sqrtf(qgs) : 0.f;
-      if (tile == 0) f.qg_part[(size_t(t) * S + sl) * Q + j] = qgs;
-      f.sig_part[((size_t(t) * f.tiles + tile) * S + sl) * Q + j] = sg;
-    }
-  }
-  if (S > 1) return;
-  // one slice: a_{t,n} = max_j S_nj / (|q_j| |x_n|) directly
-  lds_barrier();
-  float best[2][4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) best[i][e] = -INFINITY;
-#pragma unroll
-  for (int n = 0; n < NTG; ++n) {
-    const int j = n * 16 + r16;
-    const float rq = j < Q ? s_rq[j] : 0.f;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) best[i][e] = fmaxf(best[i][e], j < Q ? Sacc[i][n][e] * rq : -INFINITY);
-  }
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int m = 1; m < 16; m <<= 1) best[i][e] = fmaxf(best[i][e], __shfl_xor(best[i][e], m, kWave));
-  if (r16 == 0) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int lr = 16 * i + 4 * grp + e, r = wrow0 + lr;
-        if (lr < RW && r < TM) {
-          const float xn = s_xt[r];
-          f.tok_score[size_t(t) * N + tok0 + r] = xn > 0.f ? best[i][e] / xn : 0.f;
-        }
-      }
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Token-tiled path (bf16, Q <= 32)
 // ---------------------------------------------------------------------------
@@ -614,41 +317,40 @@ __global__ __launch_bounds__(kLdsWavesMax * 64) void k_relevance_lds(const uint1
 // written; its tokens are one contiguous stretch of X.  The eight waves split
 // the channels into 64-channel chunks (wave w takes chunks w, w + 8, ...) and
 // never wait for each other until the epilogue.  Per chunk a wave
-//   1. loads the tile's rows (8 rows x 128 bytes per instruction, whole cache
-//      lines) and the query's 64 channels directly in the MFMA B layout (16
-//      query rows x 64 bytes per instruction; the query is L2-resident);
-//   2. stores the rows to its own LDS buffer (16-byte units XOR-swizzled by
-//      row) and, from the same registers, accumulates |x|^2 and the chunk's
-//      channel sums with bf16 dot2 instructions; the channel sums of the
-//      chunk are reduced across the wave by DPP and lane swaps and stored;
-//   3. re-issues the ring slot for the chunk after next;
-//   4. runs two 32-channel steps of S += X Q^T (v_mfma_f32_16x16x32_bf16) on
-//      four 16-row tiles, reading A from its buffer.
+//   1. loads the tile's rows and the query's rows for the chunk (8 rows x 128
+//      bytes per instruction, whole cache lines; the query is L2-resident);
+//   2. stores both to its own LDS buffers (16-byte units XOR-swizzled by row)
+//      and, from the same registers, accumulates |x|^2, |q_j|^2 and the
+//      chunk's channel sums with bf16 dot2 instructions; the channel sums are
+//      reduced across the wave by DPP and lane swaps and gathered in LDS;
+//   3. runs two 32-channel steps of S += X Q^T (v_mfma_f32_16x16x32_bf16) on
+//      four 16-row tiles, reading both operands from its buffers;
+//   4. re-issues the ring slot for the chunk after next.
 // The epilogue adds the waves' partial S, |x|^2 and |q_j|^2 in wave order
 // through LDS and forms a_{t,n} = max_j S_nj / (|q_j| |x_n|) and the tile's
-// sigma_j = sum_n S_nj.
+// sigma_j = sum_n S_nj; the tile's channel sums leave in one coalesced store.
 constexpr int kTokWaves = 8;
-constexpr int kTokChunk = 64;   // channels per chunk (128 bytes of a bf16 row)
-constexpr int kTokRows = 64;    // tokens per tile at most (four 16-row MFMA tiles)
-
-constexpr int kTokPoolMax = 8192;  // channels whose sums are gathered in LDS before one coalesced store
+constexpr int kTokChunk = 64;      // channels per chunk (128 bytes of a bf16 row)
+constexpr int kTokRows = 64;       // tokens per tile at most (four 16-row MFMA tiles)
+constexpr int kTokPoolMax = 8192;  // channels whose sums are gathered in LDS
 
 // POOL: the tile's channel sums are gathered in LDS (C <= kTokPoolMax) and
-// stored once at the end, instead of a few lanes per chunk storing them
-// between the stream's loads.
+// stored once at the end; otherwise a few lanes store them chunk by chunk.
 template <int NTG, int IPC, bool POOL>
 __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t* __restrict__ X,
                                                                  const uint16_t* __restrict__ query,
                                                                  int tile_tokens, StreamArgs f) {
-  constexpr int NQ = NTG * 16;       // query columns of the accumulators
-  // per-wave chunk buffer (16-byte units swizzled by row); after a wave's
-  // loop its buffer holds its partial S [64 rows][NQ] (fits: NQ <= 32)
+  constexpr int NQ = NTG * 16;  // query rows of the accumulators
+  constexpr int QI = NQ / 8;    // query load instructions per chunk
+  // per-wave chunk buffers (16-byte units swizzled by row); after a wave's
+  // loop its row buffer holds its partial S [64 rows][NQ] (fits: NQ <= 32)
   __shared__ __align__(16) u32x4 s_x[kTokWaves][kTokRows][8];
+  __shared__ __align__(16) u32x4 s_q[kTokWaves][NQ][8];
   __shared__ __align__(16) float s_pool[POOL ? kTokPoolMax : 4];
   __shared__ float s_xx[kTokWaves][kTokRows];
   __shared__ float s_qq[kTokWaves][NQ];
   __shared__ float s_rq[NQ];
-  __shared__ float s_sig[kTokWaves][NQ];             // per-wave column sums of S
+  __shared__ float s_sig[kTokWaves][NQ];  // per-wave column sums of S
 
   int t, tile, sl;
   unit_of_block(blockIdx.x, f.tiles, 1, t, tile, sl);
@@ -658,35 +360,30 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
   const int TM = min(tile_tokens, N - tok0);
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int r16 = lane & 15, grp = lane >> 4;  // MFMA layout
-  const int lr = lane >> 3, lu = lane & 7;     // coalesced layout: row lr of each 8-row group, 16-byte unit lu
+  const int r16 = lane & 15, grp = lane >> 4;  // MFMA layout: row / column, K group
+  const int lr = lane >> 3, lu = lane & 7;     // load layout: row lr of each 8-row group, 16-byte unit lu
   const int nch = (C + kTokChunk - 1) / kTokChunk;
 
   const __amdgpu_buffer_rsrc_t xres = make_rsrc_uniform(X + (size_t(t) * N + tok0) * C, uint32_t(TM) * C * 2);
   const __amdgpu_buffer_rsrc_t qres = make_rsrc_uniform(query, uint32_t(Q) * C * 2);
 
-  // ring slot: IPC row instructions (rows 8k + lr, unit lu) and the query
-  // operands of the chunk's two steps (tile n, step s: query row 16n + r16,
-  // channels 32s + 8 grp); chunks past the end and channels past C read zeros
+  // ring slot: the tile's rows 8k + lr and the query's rows 8k + lr, unit lu
+  // of the chunk; chunks past the end, rows past the tile or the query and
+  // channels past C read zeros
   struct Slot {
     bf16x8 x[IPC];
-    bf16x8 q[NTG][2];
+    bf16x8 q[QI];
   };
   auto issue = [&](int c, Slot& d) {
-    const int ch = c * kTokChunk;
-    const bool okc = c < nch;
+    const int cc = c * kTokChunk + 8 * lu;
+    const bool ok = c < nch && cc < C;
 #pragma unroll
-    for (int k = 0; k < IPC; ++k) {
-      const int cc = ch + 8 * lu;
-      d.x[k] = buf_load_bf16x8(xres, (okc && cc < C) ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
+    for (int k = 0; k < IPC; ++k) d.x[k] = buf_load_bf16x8(xres, ok ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
+#pragma unroll
+    for (int k = 0; k < QI; ++k) {
+      const int j = 8 * k + lr;
+      d.q[k] = buf_load_bf16x8(qres, (ok && j < Q) ? (j * C + cc) * 2 : kOOB);
     }
-#pragma unroll
-    for (int n = 0; n < NTG; ++n)
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const int j = 16 * n + r16, cc = ch + 32 * st + 8 * grp;
-        d.q[n][st] = buf_load_bf16x8(qres, (okc && j < Q && cc < C) ? (j * C + cc) * 2 : kOOB);
-      }
   };
 
   f32x4 Sacc[4][NTG];
@@ -694,17 +391,17 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int n = 0; n < NTG; ++n) Sacc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float xx[IPC], qq[NTG];
+  float xx[IPC], qq[QI];
 #pragma unroll
   for (int k = 0; k < IPC; ++k) xx[k] = 0.f;
 #pragma unroll
-  for (int n = 0; n < NTG; ++n) qq[n] = 0.f;
+  for (int k = 0; k < QI; ++k) qq[k] = 0.f;
   uint32_t one_lo = kBf16OneLo, one_hi = kBf16OneHi;
   asm volatile("" : "+v"(one_lo), "+v"(one_hi));  // opaque: keeps them out of inline constants
   float* pool = POOL ? s_pool : f.pool_part + (size_t(t) * f.tiles + tile) * C;
 
   auto consume = [&](int c, const Slot& d) {
-    // rows to LDS, |x|^2 and channel sums from the registers
+    // rows to LDS; |x|^2, |q_j|^2 and channel sums from the registers
     float cs[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) cs[e] = 0.f;
@@ -720,15 +417,14 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
         cs[2 * e + 1] = dot2(v[e], one_hi, cs[2 * e + 1]);
       }
     }
-    // |q_j|^2 shares of this lane's query operands
 #pragma unroll
-    for (int n = 0; n < NTG; ++n)
+    for (int k = 0; k < QI; ++k) {
+      const int row = 8 * k + lr;
+      const u32x4 v = __builtin_bit_cast(u32x4, d.q[k]);
+      s_q[wave][row][lu ^ (row & 7)] = v;
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const u32x4 v = __builtin_bit_cast(u32x4, d.q[n][st]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) qq[n] = dot2(v[e], v[e], qq[n]);
-      }
+      for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
+    }
     // channel sums over the wave's rows: lanes lu, lu + 8, ..., lu + 56 in a fixed order
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -745,20 +441,25 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
       *reinterpret_cast<f32x4*>(pool + c0 + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
     }
   };
-  auto contract = [&](const Slot& d) {
+  auto contract = [&]() {
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
-      bf16x8 A[4];
+      bf16x8 A[4], B[NTG];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * i + r16;
         A[i] = __builtin_bit_cast(bf16x8, s_x[wave][row][(4 * st + grp) ^ (row & 7)]);
       }
 #pragma unroll
+      for (int n = 0; n < NTG; ++n) {
+        const int row = 16 * n + r16;
+        B[n] = __builtin_bit_cast(bf16x8, s_q[wave][row][(4 * st + grp) ^ (row & 7)]);
+      }
+#pragma unroll
       for (int n = 0; n < NTG; ++n)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[i], d.q[n][st], Sacc[i][n], 0, 0, 0);
+          Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[i], B[n], Sacc[i][n], 0, 0, 0);
     }
   };
 
@@ -771,33 +472,36 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
   for (int c = wave; c < nch; c += 2 * kTokWaves) {
     __builtin_amdgcn_sched_barrier(0);
     consume(c, A);
-    contract(A);
+    contract();
     issue(c + 2 * kTokWaves, A);
     __builtin_amdgcn_sched_barrier(0);
     if (c + kTokWaves < nch) {
       consume(c + kTokWaves, B);
-      contract(B);
+      contract();
     }
     issue(c + 3 * kTokWaves, B);
   }
 
-  // ---- epilogue: waves added in order ----
-  // |x|^2 of row 8k + lr: the 8 lanes of the row
-#pragma unroll
-  for (int k = 0; k < IPC; ++k) {
-    float v = xx[k];
+  // ---- epilogue: waves added in order; LDS-only barriers, so nothing waits
+  // for outstanding global accesses ----
+  auto row8_sum = [](float v) {  // the 8 lanes of a load-layout row
     v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0xB1, 0xF, 0xF, false));   // lane ^ 1
     v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x4E, 0xF, 0xF, false));   // lane ^ 2
     v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x141, 0xF, 0xF, false));  // 7 - i in 8
+    return v;
+  };
+#pragma unroll
+  for (int k = 0; k < IPC; ++k) {
+    const float v = row8_sum(xx[k]);
     if (lu == 0) s_xx[wave][8 * k + lr] = v;
   }
   for (int r = 8 * IPC + lane; r < kTokRows; r += kWave) s_xx[wave][r] = 0.f;
 #pragma unroll
-  for (int n = 0; n < NTG; ++n) {
-    const float v = row_sum4(qq[n]);
-    if (lane < 16) s_qq[wave][16 * n + lane] = v;
+  for (int k = 0; k < QI; ++k) {
+    const float v = row8_sum(qq[k]);
+    if (lu == 0) s_qq[wave][8 * k + lr] = v;
   }
-  // wave w's partial S sits in its own chunk buffer: [row][NQ] floats from &s_x[w][0][0]
+  // wave w's partial S sits in its own row buffer: [row][NQ] floats from &s_x[w][0][0]
   auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_x[w][0][0])[r * NQ + j]; };
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -805,11 +509,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
     for (int n = 0; n < NTG; ++n)
 #pragma unroll
       for (int e = 0; e < 4; ++e) s_part(wave, 16 * i + 4 * grp + e, 16 * n + r16) = Sacc[i][n][e];
-  __syncthreads();
-  if (POOL) {
-    f32x4* gpool = reinterpret_cast<f32x4*>(f.pool_part + (size_t(t) * f.tiles + tile) * C);
-    for (int c4 = tid; c4 < C / 4; c4 += kTokWaves * kWave) gpool[c4] = reinterpret_cast<const f32x4*>(s_pool)[c4];
-  }
+  lds_barrier();
   if (tid < NQ) {
     float v = 0.f;
 #pragma unroll
@@ -831,7 +531,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
   float x2 = 0.f;
 #pragma unroll
   for (int w = 0; w < kTokWaves; ++w) x2 += s_xx[w][row];
-  __syncthreads();
+  lds_barrier();
   float best = -INFINITY;
 #pragma unroll
   for (int e = 0; e < CPT; ++e)
@@ -854,12 +554,16 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
     v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
     if (lane < 8) s_sig[wave][cg + e] = v;
   }
-  __syncthreads();
+  lds_barrier();
   if (tid < Q) {
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < kTokWaves; ++w) v += s_sig[w][tid];
     f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
+  }
+  if (POOL) {
+    f32x4* gpool = reinterpret_cast<f32x4*>(f.pool_part + (size_t(t) * f.tiles + tile) * C);
+    for (int c4 = tid; c4 < C / 4; c4 += kTokWaves * kWave) gpool[c4] = reinterpret_cast<const f32x4*>(s_pool)[c4];
   }
 }
 
@@ -989,9 +693,6 @@ __global__ __launch_bounds__(256) void k_relevance_valu(const In* __restrict__ X
 #ifndef WZ_REL_RING
 #define WZ_REL_RING 4  // X prefetch depth in 32-channel steps (MFMA-layout path)
 #endif
-#ifndef WZ_LDS_RING
-#define WZ_LDS_RING 2  // X prefetch depth in 128-channel chunks (LDS-transpose path)
-#endif
 
 template <int NTG>
 void launch_mfma(const RelPlan& pl, const void* X, const void* query, const StreamArgs& fa, hipStream_t s) {
@@ -1010,22 +711,11 @@ void launch_tok(const RelPlan& pl, const void* X, const void* query, const Strea
                        static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, fa);
 }
 
-template <int NTG, int IPC>
-void launch_lds(const RelPlan& pl, const void* X, const void* query, const StreamArgs& fa, hipStream_t s) {
-  hipLaunchKernelGGL((k_relevance_lds<NTG, IPC, WZ_LDS_RING>), dim3(pl.grid), dim3(pl.threads), 0, s,
-                     static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, pl.kc,
-                     fa);
-}
-
 }  // namespace
 
 RelKind relevance_kind(const wz_config& c) {
   if (c.in_dtype != WZ_BF16) return kRelValu;
-#ifdef WZ_REL_SLICES
-  if (c.Q <= 32) return kRelLds;
-#else
   if (c.Q <= 32) return kRelTok;
-#endif
   // two 16-row MFMA tiles per wave, at least 2 waves: frames of at least 49 tokens
   return c.H * c.W >= 49 ? kRelMfma : kRelValu;
 }
@@ -1049,14 +739,6 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
   }
     if (pl.ntg == 1) { WZ_TOK(1) } else { WZ_TOK(2) }
 #undef WZ_TOK
-  } else if (pl.kind == kRelLds) {
-    if (pl.ntg == 1) {
-      if (pl.ipc == 7) launch_lds<1, 7>(pl, X, query, fa, s);
-      else launch_lds<1, 8>(pl, X, query, fa, s);
-    } else {
-      if (pl.ipc == 7) launch_lds<2, 7>(pl, X, query, fa, s);
-      else launch_lds<2, 8>(pl, X, query, fa, s);
-    }
   } else if (pl.kind == kRelMfma) {
     // queries of more than 32 tokens take several passes of 32 over the slice:
     // wider query groups no longer fit the accumulators in registers
