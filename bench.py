@@ -64,9 +64,9 @@ def kernel_sources_sha256():
 
 
 def recorded_traffic(workload):
-    """HBM bytes per wz_relevance call measured with rocprofv3 byte counters (profiles/), or None when
-    there is no record for the workload or the kernels changed since it was taken."""
-    path = os.path.join(HERE, "profiles", f"stage1_traffic_{workload}.json")
+    """HBM bytes per launch of the relevance pass measured with rocprofv3 byte counters (profiles/), or
+    None when there is no record for the workload or the kernels changed since it was taken."""
+    path = os.path.join(HERE, "profiles", f"relevance_pass_traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as fh:
@@ -77,9 +77,10 @@ def recorded_traffic(workload):
 
 
 def relevance_bytes(wl):
-    """Bytes the relevance pass must move: frames and query read, scores written."""
+    """Bytes the relevance pass must move: frames and query read once, per-token scores written (the
+    per-unit partial sums it also writes are left out, so the rate is a lower bound)."""
     s_in = 2 if wl.dtype == "bf16" else 4
-    return wl.T * wl.N * wl.C * s_in + wl.Q * wl.C * s_in + 4 * wl.T * wl.N + 8 * wl.T
+    return wl.T * wl.N * wl.C * s_in + wl.Q * wl.C * s_in + 4 * wl.T * wl.N
 
 
 def cpu_baseline(inp, wl, seconds):
@@ -149,21 +150,19 @@ def main():
     wall = time.perf_counter() - t0
     ms_step = ev0.elapsed_time(ev1) / args.steps
 
-    # dominant stage: wz_relevance (the pass over X and the per-frame kernel), called alone
-    # back to back on the same stream
+    # dominant kernel: the relevance pass over X (k_relevance_tok), launched alone through
+    # wz_relevance_pass, back to back on the same stream
     a = torch.empty(wl.T * wl.N, dtype=torch.float32, device=dev)
-    r = torch.empty(wl.T, dtype=torch.float32, device=dev)
-    d = torch.empty(wl.T, dtype=torch.float32, device=dev)
     import ctypes
     L = wz.lib()
     cfg = p.config()
     sp = ctypes.c_void_p(stream.cuda_stream)
 
     def rel(i):
-        st = L.wz_relevance(ctypes.byref(cfg), wz._ptr(Xs[i % nsets]), wz._ptr(qs[i % nsets]), wz._ptr(a),
-                            wz._ptr(r), wz._ptr(d), wz._ptr(ws), ws.numel(), sp)
+        st = L.wz_relevance_pass(ctypes.byref(cfg), wz._ptr(Xs[i % nsets]), wz._ptr(qs[i % nsets]), wz._ptr(a),
+                                 wz._ptr(ws), ws.numel(), sp)
         if st != 0:
-            raise wz.WZError(st, "wz_relevance")
+            raise wz.WZError(st, "wz_relevance_pass")
 
     for i in range(args.warmup):
         rel(i)
@@ -201,7 +200,7 @@ def main():
         "hbm_frac": call_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": call_bytes,
         "wall_s": wall,
-        "roofline": {"kernel": "stage 1, wz_relevance: streaming pass k_relevance_mfma + per-frame k_frame_scores",
+        "roofline": {"kernel": "k_relevance_tok (wz_relevance_pass: the one pass over the frames)",
                      "bound": "hbm", "achieved": k1_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k1_gbps / HBM_PEAK_GBPS,
                      "traffic": recorded_traffic(wl.name), "bytes_per_launch": k1_bytes,

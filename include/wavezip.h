@@ -95,11 +95,26 @@ size_t wz_workspace_bytes(const wz_config* cfg);
  *                          delta_0 = 0                                  [T]
  * where v_t is the spatial mean of frame t's tokens.  Accumulation is fp32,
  * the frame-level cosines fp64.  ws: at least wz_workspace_bytes(cfg) bytes
- * of device memory.  Two kernel launches: one pass over X writing per-unit
- * partials, then five workgroups per frame adding them in a fixed order.    */
+ * of device memory.  Two kernel launches: one pass over X (wz_relevance_pass)
+ * writing per-unit partials, then a per-frame step adding them in a fixed
+ * order.                                                                     */
 wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
                        float* tok_score, float* frame_rel, float* frame_delta,
                        void* ws, size_t ws_bytes, void* stream);
+
+/* The pass over X that stage 1 starts with -- the one kernel of the whole
+ * pass that reads the frames -- on its own.  It writes the per-token scores
+ * a_{t,n} to tok_score [T*H*W] where one workgroup sees every channel of a
+ * token (always for bf16 inputs with at most 32 query tokens and for fp32
+ * inputs; for bf16 with more query tokens, when the grid has no channel
+ * slices), and leaves in ws the per-work-unit partial sums that
+ * wz_relevance's per-frame step completes r_t, delta_t (and, with channel
+ * slices, a_{t,n}) from.  It
+ * lets a caller run or time the pass alone; nothing else reads what it
+ * leaves in ws.  Same arguments and checks as wz_relevance.  One kernel
+ * launch.                                                                     */
+wz_status wz_relevance_pass(const wz_config* cfg, const void* X, const void* query,
+                            float* tok_score, void* ws, size_t ws_bytes, void* stream);
 
 /* Stage 2 -- Wavelet Temporal Allocator and budget (Sec. 3.2.2; Eq. (9)-(11);
  * Eq. (16) under Eq. (5)).  From r and delta (as produced by wz_relevance):

@@ -79,6 +79,18 @@ wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query, f
   return from_hip(launch_frame(*cfg, w, tok_score, frame_rel, frame_delta, false, s));
 }
 
+wz_status wz_relevance_pass(const wz_config* cfg, const void* X, const void* query, float* tok_score, void* ws,
+                            size_t ws_bytes, void* stream) {
+  WZ_TRY(check_config(cfg));
+  WZ_TRY(check_ptr(X, 16));
+  WZ_TRY(check_ptr(query, 16));
+  WZ_TRY(check_ptr(tok_score, 4));
+  if (!ws) return WZ_ERR_NULL;
+  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
+  if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
+  return from_hip(launch_relevance_stream(*cfg, X, query, tok_score, w, static_cast<hipStream_t>(stream)));
+}
+
 wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel, const float* frame_delta,
                              int32_t* budget, int32_t* offset, float* rel_rect, void* stream) {
   WZ_TRY(check_config(cfg));

@@ -44,6 +44,18 @@ __device__ __forceinline__ int buf_load_i32(__amdgpu_buffer_rsrc_t r, int off) {
 __device__ __forceinline__ void buf_store_f32(float v, __amdgpu_buffer_rsrc_t r, int off) {
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, off, 0, 0);
 }
+// Stores of results that this kernel does not read back, written through the
+// L2 to memory (system-coherent, sc1): they do not sit dirty in the L2 until
+// the end of the kernel, whose write-back otherwise delays the next kernel by
+// about 0.15 us per MB.
+constexpr int kWriteThrough = 16;  // buffer-store cache policy: sc1
+__device__ __forceinline__ void buf_store_wt_b128(u32x4 v, __amdgpu_buffer_rsrc_t r, int off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kWriteThrough);
+}
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void buf_store_wt_b64(uint64_t v, __amdgpu_buffer_rsrc_t r, int off) {
+  __builtin_amdgcn_raw_buffer_store_b64(u32x2v{uint32_t(v), uint32_t(v >> 32)}, r, off, 0, kWriteThrough);
+}
 
 // Sum over the four 16-lane rows of a wave, every lane getting the total of
 // its column (lane & 15): ((row0 + row1) + (row2 + row3)).  gfx950's lane

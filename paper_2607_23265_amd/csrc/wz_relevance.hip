@@ -562,8 +562,10 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t
     f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
   }
   if (POOL) {
-    f32x4* gpool = reinterpret_cast<f32x4*>(f.pool_part + (size_t(t) * f.tiles + tile) * C);
-    for (int c4 = tid; c4 < C / 4; c4 += kTokWaves * kWave) gpool[c4] = reinterpret_cast<const f32x4*>(s_pool)[c4];
+    const __amdgpu_buffer_rsrc_t pres =
+        make_rsrc_uniform(f.pool_part + (size_t(t) * f.tiles + tile) * C, uint32_t(C) * 4);
+    for (int c4 = tid; c4 < C / 4; c4 += kTokWaves * kWave)
+      buf_store_wt_b128(reinterpret_cast<const u32x4*>(s_pool)[c4], pres, c4 * 16);
   }
 }
 

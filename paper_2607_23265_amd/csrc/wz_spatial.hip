@@ -79,30 +79,34 @@ struct Vec16<float> {
   }
 };
 
+// One row vector of the output (16 bytes of input widened to V floats), at
+// byte offset off of the row's buffer, written through the L2.
 template <typename Out, int V>
-__device__ __forceinline__ void store_row(Out* p, const float* v);
+__device__ __forceinline__ void store_row(__amdgpu_buffer_rsrc_t r, int off, const float* v);
 template <>
-__device__ __forceinline__ void store_row<float, 4>(float* p, const float* v) {
-  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+__device__ __forceinline__ void store_row<float, 4>(__amdgpu_buffer_rsrc_t r, int off, const float* v) {
+  buf_store_wt_b128(u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])},
+                    r, off);
 }
 template <>
-__device__ __forceinline__ void store_row<float, 8>(float* p, const float* v) {
-  reinterpret_cast<f32x4*>(p)[0] = f32x4{v[0], v[1], v[2], v[3]};
-  reinterpret_cast<f32x4*>(p)[1] = f32x4{v[4], v[5], v[6], v[7]};
+__device__ __forceinline__ void store_row<float, 8>(__amdgpu_buffer_rsrc_t r, int off, const float* v) {
+  buf_store_wt_b128(u32x4{__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3])},
+                    r, off);
+  buf_store_wt_b128(u32x4{__float_as_uint(v[4]), __float_as_uint(v[5]), __float_as_uint(v[6]), __float_as_uint(v[7])},
+                    r, off + 16);
 }
 template <>
-__device__ __forceinline__ void store_row<uint16_t, 8>(uint16_t* p, const float* v) {
+__device__ __forceinline__ void store_row<uint16_t, 8>(__amdgpu_buffer_rsrc_t r, int off, const float* v) {
   u32x4 o;
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = f32_to_bf16_rne(v[2 * i]) | (f32_to_bf16_rne(v[2 * i + 1]) << 16);
-  *reinterpret_cast<u32x4*>(p) = o;
+  buf_store_wt_b128(o, r, off);
 }
 template <>
-__device__ __forceinline__ void store_row<uint16_t, 4>(uint16_t* p, const float* v) {
-  u32x2 o;
-  o[0] = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
-  o[1] = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
-  *reinterpret_cast<u32x2*>(p) = o;
+__device__ __forceinline__ void store_row<uint16_t, 4>(__amdgpu_buffer_rsrc_t r, int off, const float* v) {
+  const uint64_t lo = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
+  const uint64_t hi = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
+  buf_store_wt_b64(lo | (hi << 32), r, off);
 }
 
 template <typename In, typename Out, int U, int MODE>
@@ -273,7 +277,8 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
     const int h = n / f.W, w = n - h * f.W;
     const float sw = (w & 1) ? -1.f : 1.f;
     const float sh = (h & 1) ? -1.f : 1.f;
-    Out* dst = static_cast<Out*>(f.out_tokens) + size_t(k) * f.C;
+    const __amdgpu_buffer_rsrc_t ores =
+        make_rsrc_uniform(static_cast<Out*>(f.out_tokens) + size_t(k) * f.C, uint32_t(f.C) * sizeof(Out));
     const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -293,7 +298,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
         // gate the detail bands (Eq. (14)) and invert at the token's position (Eq. (15))
         y[e] = 0.5f * (LL + g * (sw * LH + sh * HL + (sw * sh) * HH));
       }
-      if (v < ve) store_row<Out, V>(dst + v * V, y);
+      if (v < ve) store_row<Out, V>(ores, v * V * int(sizeof(Out)), y);
     }
     if (j % parts == 0 && lane == 0) f.out_index[k] = t * N + n;
   };

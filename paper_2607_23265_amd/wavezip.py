@@ -18,8 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libwavezip.so")
 WZ_F32, WZ_BF16 = 0, 1
 _STATUS = {0: "WZ_OK", 1: "WZ_ERR_NULL", 2: "WZ_ERR_ALIGN", 3: "WZ_ERR_SHAPE", 4: "WZ_ERR_DTYPE",
            5: "WZ_ERR_PARAM", 6: "WZ_ERR_BUDGET", 7: "WZ_ERR_WORKSPACE", 8: "WZ_ERR_DEVICE"}
-EXPORTS = ("wz_workspace_bytes", "wz_relevance", "wz_temporal_budget", "wz_spatial_dwt_condense",
-           "wz_condense", "wz_status_str")
+EXPORTS = ("wz_workspace_bytes", "wz_relevance", "wz_relevance_pass", "wz_temporal_budget",
+           "wz_spatial_dwt_condense", "wz_condense", "wz_status_str")
 
 
 class WZError(RuntimeError):
@@ -52,10 +52,11 @@ def lib():
     L.wz_workspace_bytes.argtypes = [cfgp]
     L.wz_workspace_bytes.restype = S
     L.wz_relevance.argtypes = [cfgp, P, P, P, P, P, P, S, P]
+    L.wz_relevance_pass.argtypes = [cfgp, P, P, P, P, S, P]
     L.wz_temporal_budget.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_spatial_dwt_condense.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_condense.argtypes = [cfgp, P, P, P, P, P, P, P, S, P]
-    for f in ("wz_relevance", "wz_temporal_budget", "wz_spatial_dwt_condense", "wz_condense"):
+    for f in ("wz_relevance", "wz_relevance_pass", "wz_temporal_budget", "wz_spatial_dwt_condense", "wz_condense"):
         getattr(L, f).restype = ctypes.c_int
     L.wz_status_str.argtypes = [ctypes.c_int]
     L.wz_status_str.restype = ctypes.c_char_p
@@ -129,6 +130,14 @@ def relevance(p: Problem, X, query, ws=None):
     _check(lib().wz_relevance(ctypes.byref(cfg), _ptr(X), _ptr(query), _ptr(a), _ptr(r), _ptr(d), _ptr(ws),
                               ws.numel(), _stream(dev)), "wz_relevance")
     return a, r, d
+
+
+def relevance_pass(p: Problem, X, query, tok_score, ws):
+    """wz_relevance_pass: the pass over X alone, into caller-owned tok_score and ws."""
+    _require_device(X, query, tok_score, ws)
+    cfg = p.config()
+    _check(lib().wz_relevance_pass(ctypes.byref(cfg), _ptr(X), _ptr(query), _ptr(tok_score), _ptr(ws),
+                                   ws.numel(), _stream(X.device)), "wz_relevance_pass")
 
 
 def temporal_budget(p: Problem, frame_rel, frame_delta):

@@ -65,6 +65,7 @@ def test_invalid_config(L, kw, code):
     c = cfg(**kw)
     fake = ctypes.c_void_p(0x10000)
     assert L.wz_relevance(ctypes.byref(c), fake, fake, fake, fake, fake, fake, 1 << 30, None) == code
+    assert L.wz_relevance_pass(ctypes.byref(c), fake, fake, fake, fake, 1 << 30, None) == code
     assert L.wz_temporal_budget(ctypes.byref(c), fake, fake, fake, fake, None, None) == code
     assert L.wz_spatial_dwt_condense(ctypes.byref(c), fake, fake, fake, fake, fake, None) == code
     assert L.wz_condense(ctypes.byref(c), fake, fake, fake, fake, None, None, fake, 1 << 30, None) == code
@@ -85,6 +86,13 @@ def test_pointer_checks(L):
     assert L.wz_relevance(ctypes.byref(c), ok, ok, ok, ok, ok, nul, need, None) == NULL
     assert L.wz_relevance(ctypes.byref(c), ok, ok, ok, ok, ok, ok, need - 1, None) == WORKSPACE
     assert L.wz_relevance(ctypes.byref(c), ok, ok, ok, ok, ok, ctypes.c_void_p(0x10010), need, None) == WORKSPACE
+    assert L.wz_relevance_pass(None, ok, ok, ok, ok, need, None) == NULL
+    assert L.wz_relevance_pass(ctypes.byref(c), nul, ok, ok, ok, need, None) == NULL
+    assert L.wz_relevance_pass(ctypes.byref(c), ok, odd, ok, ok, need, None) == ALIGN
+    assert L.wz_relevance_pass(ctypes.byref(c), ok, ok, odd4, ok, need, None) == ALIGN
+    assert L.wz_relevance_pass(ctypes.byref(c), ok, ok, ok, nul, need, None) == NULL
+    assert L.wz_relevance_pass(ctypes.byref(c), ok, ok, ok, ok, need - 1, None) == WORKSPACE
+    assert L.wz_relevance_pass(ctypes.byref(c), ok, ok, ok, ctypes.c_void_p(0x10010), need, None) == WORKSPACE
     assert L.wz_temporal_budget(ctypes.byref(c), ok, ok, nul, ok, None, None) == NULL
     assert L.wz_temporal_budget(ctypes.byref(c), ok, ok, ok, odd4, None, None) == ALIGN
     assert L.wz_temporal_budget(ctypes.byref(c), ok, ok, ok, ok, odd4, None) == ALIGN

@@ -82,6 +82,21 @@ def test_benchmarked_launch_bf16_out_and_determinism():
     assert G.within(_np(tok), out["tokens"], G.TOL_BF16_OUT)
 
 
+@pytest.mark.parametrize("name", ["tiny", "t64_14x14_c3584"])
+def test_relevance_pass_alone(name):
+    """wz_relevance_pass writes the same per-token scores as wz_relevance (one slice: the pass completes them)."""
+    wl, inp, out = G.workload_case(name)
+    p = wz.problem_of(wl)
+    X, q = wz.to_device(inp, DEV)
+    ws = wz.new_workspace(p, DEV)
+    a = torch.full((wl.T * wl.N,), float("nan"), dtype=torch.float32, device=DEV)
+    wz.relevance_pass(p, X, q, a, ws)
+    a_full, _, _ = wz.relevance(p, X, q)
+    torch.cuda.synchronize()
+    assert torch.equal(a, a_full)
+    assert G.within(_np(a), out["a"].ravel(), G.tol_for(wl.dtype))
+
+
 @pytest.mark.parametrize("name", ["tiny", "t64_14x14_c3584", "t128_13x13_c3584"])
 def test_stage_temporal_budget(name):
     """wz_temporal_budget fed the oracle's r and delta (as fp32) vs the oracle's stage on the same values."""
