@@ -327,54 +327,6 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
 // reads instead of LDS round trips; compaction uses a ballot; the Haar levels
 // move data with lane shuffles.  Same arithmetic as budget_body.
 // ---------------------------------------------------------------------------
-constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
-constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
-constexpr int kDppHalfMirror = 0x141;  // lane i <-> 7 - i within each half row
-constexpr int kDppMirror = 0x140;      // lane i <-> 15 - i within each row
-
-template <int CTRL>
-__device__ __forceinline__ double dpp_f64(double v) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(u)), CTRL, 0xF, 0xF, false));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(u >> 32)), CTRL, 0xF, 0xF, false));
-  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
-}
-template <int CTRL>
-__device__ __forceinline__ int dpp_i32(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
-}
-__device__ __forceinline__ double readlane_f64(double v, int l) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u)), l));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(u >> 32)), l));
-  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
-}
-__device__ __forceinline__ double permute_f64(int dst_lane, double v) {  // value of lane l goes to lane dst(l)
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const uint32_t lo = uint32_t(__builtin_amdgcn_ds_permute(dst_lane * 4, int(uint32_t(u))));
-  const uint32_t hi = uint32_t(__builtin_amdgcn_ds_permute(dst_lane * 4, int(uint32_t(u >> 32))));
-  return __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
-}
-
-// op over all 64 lanes (every lane gets the result): within each row of 16
-// lanes by DPP, then the four row results in a fixed order.
-template <typename Op>
-__device__ __forceinline__ double wave_reduce_f64(double v, Op op) {
-  v = op(v, dpp_f64<kDppXor1>(v));
-  v = op(v, dpp_f64<kDppXor2>(v));
-  v = op(v, dpp_f64<kDppHalfMirror>(v));
-  v = op(v, dpp_f64<kDppMirror>(v));
-  return op(op(readlane_f64(v, 0), readlane_f64(v, 16)), op(readlane_f64(v, 32), readlane_f64(v, 48)));
-}
-__device__ __forceinline__ int wave_reduce_sum_i32(int v) {
-  v += dpp_i32<kDppXor1>(v);
-  v += dpp_i32<kDppXor2>(v);
-  v += dpp_i32<kDppHalfMirror>(v);
-  v += dpp_i32<kDppMirror>(v);
-  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
-         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
-}
-
 // Runs on one whole wave (wave 0 of its workgroup).  Lane t holds delta_t
 // and r_t (anything for lanes >= T); outputs may point to global memory or
 // LDS.

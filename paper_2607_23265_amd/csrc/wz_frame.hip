@@ -264,11 +264,11 @@ __device__ void lead_role(const FrameArgs& f, int t) {
         bb += double(y[i][e]) * y[i][e];
       }
   }
-  ab = wave_sum_f64(ab);
-  aa = wave_sum_f64(aa);
-  bb = wave_sum_f64(bb);
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) rbest = fmax(rbest, __shfl_xor(rbest, m, kWave));
+  auto add = [](double x, double y) { return x + y; };
+  ab = wave_reduce_f64(ab, add);
+  aa = wave_reduce_f64(aa, add);
+  bb = wave_reduce_f64(bb, add);
+  rbest = wave_reduce_f64(rbest, [](double x, double y) { return fmax(x, y); });
   if (lane == 0) {
     s_red[0][wave] = ab;
     s_red[1][wave] = aa;

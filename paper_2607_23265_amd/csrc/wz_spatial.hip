@@ -18,12 +18,15 @@
 //      order by ballots;
 //   C. kept tokens of rank p, p + P, ... are reconstructed, each split into
 //      channel parts of at most two 16-byte vectors per lane, one part per
-//      wave at a time: LL, LH, HL, HH of the token's 2x2 Haar block (the last
-//      row / column repeated when H or W is odd) by the orthonormal
-//      butterflies (Eq. (12)), the three detail bands multiplied by the
-//      block's gate (Eq. (13)-(14)) and the token's position inverted
-//      (Eq. (15)); the row goes to out_tokens[offset_t + position], its flat
-//      index t*H*W + n to out_index.
+//      wave at a time, the next part's reads in flight meanwhile (a wave's
+//      first part after the read-ahead ones is requested before B).  The
+//      orthonormal butterflies of the token's 2x2 Haar block (Eq. (12); the
+//      last row / column repeated when H or W is odd), the three detail bands
+//      multiplied by the block's gate (Eq. (13)-(14)) and the inverse at the
+//      token's position (Eq. (15)) amount to mu + g (x - mu), mu the block
+//      mean, which is what is evaluated.  The row goes to
+//      out_tokens[offset_t + position], its flat index t*H*W + n to
+//      out_index.
 // Only the blocks of kept tokens are read: at most 4 * B token rows, partly
 // from the Infinity Cache right after the pass over the frames.
 #include "wz_budget.h"
@@ -151,21 +154,23 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   // budget is known.
   const int kp = min(f.kpre, N);
   const int npre = given && kp > p ? min(GW, (kp - p + f.P - 1) / f.P * parts) : 0;
+  // the four rows of token n's 2x2 block, the token's own row first: the
+  // block's other row h2 and column w2 (the last row / column repeated when
+  // H or W is odd)
   auto load_item = [&](int j, int n, u32x4 (&x)[U][4]) {
     const int h = n / f.W, w = n - h * f.W;
-    const int i0 = h & ~1, j0 = w & ~1;
-    const int i1 = min(i0 + 1, f.H - 1), j1 = min(j0 + 1, f.W - 1);
-    const int r00 = (i0 * f.W + j0) * rb, r01 = (i0 * f.W + j1) * rb;
-    const int r10 = (i1 * f.W + j0) * rb, r11 = (i1 * f.W + j1) * rb;
+    const int h2 = (h & 1) ? h - 1 : min(h + 1, f.H - 1), w2 = (w & 1) ? w - 1 : min(w + 1, f.W - 1);
+    const int r0 = (h * f.W + w) * rb, r1 = (h * f.W + w2) * rb;
+    const int r2 = (h2 * f.W + w) * rb, r3 = (h2 * f.W + w2) * rb;
     const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = vb + u * kWave + lane;
       const int cb = v < ve ? v * 16 : kOOB;
-      x[u][0] = __builtin_amdgcn_raw_buffer_load_b128(xres, r00 + cb, 0, 0);
-      x[u][1] = __builtin_amdgcn_raw_buffer_load_b128(xres, r01 + cb, 0, 0);
-      x[u][2] = __builtin_amdgcn_raw_buffer_load_b128(xres, r10 + cb, 0, 0);
-      x[u][3] = __builtin_amdgcn_raw_buffer_load_b128(xres, r11 + cb, 0, 0);
+      x[u][0] = __builtin_amdgcn_raw_buffer_load_b128(xres, r0 + cb, 0, 0);
+      x[u][1] = __builtin_amdgcn_raw_buffer_load_b128(xres, r1 + cb, 0, 0);
+      x[u][2] = __builtin_amdgcn_raw_buffer_load_b128(xres, r2 + cb, 0, 0);
+      x[u][3] = __builtin_amdgcn_raw_buffer_load_b128(xres, r3 + cb, 0, 0);
     }
   };
 
@@ -245,6 +250,13 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
     }
   }
 
+  // this wave's first item after the ones read ahead: its block reads go out
+  // now, to land while the positions are formed
+  const int mine = nt > p ? (nt - p + f.P - 1) / f.P : 0;  // kept tokens of this workgroup
+  const int nitems = mine * parts;
+  u32x4 xa[U][4];
+  if (npre + wave < nitems) load_item(npre + wave, rl.byrank[p + f.P * ((npre + wave) / parts)], xa);
+
   // ---- B. raster positions of the kept tokens (ballots, one token per thread and round) ----
   int run = 0;  // kept tokens of earlier rounds
   for (int n0 = 0; n0 < N; n0 += kThreads) {
@@ -267,47 +279,49 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   }
 
   // ---- C. reconstruction of the kept tokens of rank p, p + P, ... ----
-  const int mine = nt > p ? (nt - p + f.P - 1) / f.P : 0;  // kept tokens of this workgroup
   auto finish_item = [&](int j, const u32x4 (&x)[U][4]) {
     const int r = p + f.P * (j / parts);
     const long long k = base + s_posr[r];
     if (k < 0 || k >= total) return;
     const int n = rl.byrank[r];
     const float g = rl.gate[n];
-    const int h = n / f.W, w = n - h * f.W;
-    const float sw = (w & 1) ? -1.f : 1.f;
-    const float sh = (h & 1) ? -1.f : 1.f;
+    const float c = 0.25f * (1.f - g);
     const __amdgpu_buffer_rsrc_t ores =
         make_rsrc_uniform(static_cast<Out*>(f.out_tokens) + size_t(k) * f.C, uint32_t(f.C) * sizeof(Out));
     const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = vb + u * kWave + lane;
-      float x00[V], x01[V], x10[V], x11[V], y[V];
-      Vec16<In>::widen(x[u][0], x00);
-      Vec16<In>::widen(x[u][1], x01);
-      Vec16<In>::widen(x[u][2], x10);
-      Vec16<In>::widen(x[u][3], x11);
+      float x0[V], x1[V], x2[V], x3[V], y[V];
+      Vec16<In>::widen(x[u][0], x0);
+      Vec16<In>::widen(x[u][1], x1);
+      Vec16<In>::widen(x[u][2], x2);
+      Vec16<In>::widen(x[u][3], x3);
 #pragma unroll
       for (int e = 0; e < V; ++e) {
-        // orthonormal 2-D Haar butterflies of the block (Eq. (12))
-        const float LL = 0.5f * ((x00[e] + x01[e]) + (x10[e] + x11[e]));
-        const float LH = 0.5f * ((x00[e] - x01[e]) + (x10[e] - x11[e]));
-        const float HL = 0.5f * ((x00[e] + x01[e]) - (x10[e] + x11[e]));
-        const float HH = 0.5f * ((x00[e] - x01[e]) - (x10[e] - x11[e]));
-        // gate the detail bands (Eq. (14)) and invert at the token's position (Eq. (15))
-        y[e] = 0.5f * (LL + g * (sw * LH + sh * HL + (sw * sh) * HH));
+        // The orthonormal 2-D Haar butterflies of the block (Eq. (12)), the
+        // three detail bands times the gate (Eq. (13)-(14)) and the inverse
+        // at the token's own position (Eq. (15)) come to mu + g (x - mu),
+        // mu the block mean: the approximation band alone synthesises mu at
+        // every position and the detail bands alone x - mu.
+        y[e] = fmaf(c, (x0[e] + x1[e]) + (x2[e] + x3[e]), g * x0[e]);
       }
       if (v < ve) store_row<Out, V>(ores, v * V * int(sizeof(Out)), y);
     }
     if (j % parts == 0 && lane == 0) f.out_index[k] = t * N + n;
   };
   // blocks read ahead whose token is kept, then the rest
-  if (wave >= G0 && wave - G0 < npre && wave - G0 < mine * parts) finish_item(wave - G0, xp);
-  for (int j = npre + wave; j < mine * parts; j += kNW) {
-    u32x4 x[U][4];
-    load_item(j, rl.byrank[p + f.P * (j / parts)], x);
-    finish_item(j, x);
+  if (wave >= G0 && wave - G0 < npre && wave - G0 < nitems) finish_item(wave - G0, xp);
+  // the rest, the next item's reads in flight while one is finished
+  for (int j = npre + wave; j < nitems; j += kNW) {
+    u32x4 xb[U][4];
+    const int jn = j + kNW;
+    if (jn < nitems) load_item(jn, rl.byrank[p + f.P * (jn / parts)], xb);
+    finish_item(j, xa);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) xa[u][q] = xb[u][q];
   }
 }
 
