@@ -10,23 +10,21 @@
 //   A. wave 0 computes the budgets (T <= 64; all waves up to T = 256) while
 //      the other waves take the frame's selection ranks and block gates
 //      (from the per-frame kernel, or formed here from the scores when the
-//      stage runs on its own, wz_rank.h) and read the 2x2 blocks of the first
-//      tokens this workgroup will reconstruct: most frames keep at least
-//      three quarters of the mean budget, so those reads are rarely wasted
-//      and overlap the budget;
-//   B. the frame keeps its n_t tokens of rank < n_t, numbered in raster
-//      order by ballots;
-//   C. kept tokens of rank p, p + P, ... are reconstructed, each split into
-//      channel parts of at most two 16-byte vectors per lane, one part per
-//      wave at a time, the next part's reads in flight meanwhile (a wave's
-//      first part after the read-ahead ones is requested before B).  The
-//      orthonormal butterflies of the token's 2x2 Haar block (Eq. (12); the
-//      last row / column repeated when H or W is odd), the three detail bands
-//      multiplied by the block's gate (Eq. (13)-(14)) and the inverse at the
-//      token's position (Eq. (15)) amount to mu + g (x - mu), mu the block
-//      mean, which is what is evaluated.  The row goes to
-//      out_tokens[offset_t + position], its flat index t*H*W + n to
-//      out_index.
+//      stage runs on its own, wz_rank.h) and form the rows of the first
+//      tokens this workgroup will emit: most frames keep at least three
+//      quarters of the mean budget, so that work is rarely wasted and it
+//      overlaps the budget;
+//   B. the frame keeps its n_t tokens of rank < n_t; kept tokens of rank
+//      p, p + P, ... are emitted, each split into channel parts of at most two
+//      16-byte vectors per lane, one part per wave at a time, the next part's
+//      block reads in flight meanwhile.  A token's row is its 2x2 Haar block
+//      (the last row / column repeated when H or W is odd) through the
+//      orthonormal butterflies (Eq. (12)), the three detail bands multiplied
+//      by the block's gate (Eq. (13)-(14)) and the inverse at the token's
+//      position (Eq. (15)), evaluated in the equivalent form mu + g (x - mu),
+//      mu the block mean.  It goes to out_tokens[offset_t + position],
+//      position = kept tokens before it in raster order (a wave's own
+//      ballots over the ranks), its flat index t*H*W + n to out_index.
 // Only the blocks of kept tokens are read: at most 4 * B token rows, partly
 // from the Infinity Cache right after the pass over the frames.
 #include "wz_budget.h"
@@ -121,7 +119,6 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   extern __shared__ __align__(16) char s_dyn[];
   __shared__ int32_t s_nb[kFusedTMax];       // budgets (budget modes)
   __shared__ int32_t s_off[kFusedTMax + 1];  // offsets (budget modes)
-  __shared__ int s_cnt[kNW];
   __shared__ float s_mm[2 * kNW];
   __shared__ int s_start[kBins], s_fill[kBins];
 
@@ -138,7 +135,6 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   rl.start = s_start;
   rl.fill = s_fill;
   rl.mm = s_mm;
-  int32_t* s_posr = rl.order;  // raster position among the kept, by rank (after the ranking)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bool given = f.rank != nullptr;
 
@@ -189,16 +185,69 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   } else {
     budget_body<kThreads, kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
   }
-  u32x4 xp[U][4];
+  // The gated 2x2 Haar round trip of a token, for the channel part in x:
+  // the orthonormal butterflies of its block (Eq. (12)), the three detail
+  // bands times the gate g (Eq. (13)-(14)) and the inverse at the token's own
+  // position (Eq. (15)) come to mu + g (x - mu), mu the block mean: the
+  // approximation band alone synthesises mu at every position and the detail
+  // bands alone x - mu.  x[.][0] is the token's own row.
+  auto modulate = [&](const u32x4 (&x)[U][4], float g, float (&y)[U][V]) {
+    const float c = 0.25f * (1.f - g);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float x0[V], x1[V], x2[V], x3[V];
+      Vec16<In>::widen(x[u][0], x0);
+      Vec16<In>::widen(x[u][1], x1);
+      Vec16<In>::widen(x[u][2], x2);
+      Vec16<In>::widen(x[u][3], x3);
+#pragma unroll
+      for (int e = 0; e < V; ++e) y[u][e] = fmaf(c, (x0[e] + x1[e]) + (x2[e] + x3[e]), g * x0[e]);
+    }
+  };
+  // kept tokens (rank < nt) before token n in raster order: ballots over the
+  // frame's ranks in LDS, by the calling wave alone
+  auto position = [&](int n, int nt) {
+    int before = 0;
+    for (int m0 = 0; m0 < n; m0 += kWave) {
+      const int m = m0 + lane;
+      before += __popcll(__ballot(m < n && rl.rank[m] < nt));
+    }
+    return before;
+  };
+  // row k of the output: the channel part of item j
+  auto store_item = [&](int j, int n, long long k, const float (&y)[U][V]) {
+    const __amdgpu_buffer_rsrc_t ores =
+        make_rsrc_uniform(static_cast<Out*>(f.out_tokens) + size_t(k) * f.C, uint32_t(f.C) * sizeof(Out));
+    const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int v = vb + u * kWave + lane;
+      if (v < ve) store_row<Out, V>(ores, v * V * int(sizeof(Out)), y[u]);
+    }
+    if (j % parts == 0 && lane == 0) f.out_index[k] = t * N + n;
+  };
+
+  // read-ahead item of this wave (waves G0.., item wave - G0): its block and
+  // gate are read and the row formed while the budgets are computed
+  const int jp = wave - G0;
+  const bool ahead = given && wave >= G0 && jp < npre;
+  int np = 0;
+  float yp[U][V];
   if (given) {
     if (wave >= G0) {
-      const int jp = wave - G0;
-      if (jp < npre) load_item(jp, f.byrank[size_t(t) * N + p + f.P * (jp / parts)], xp);
+      u32x4 xp[U][4];
+      float gp = 0.f;
+      if (ahead) {
+        np = f.byrank[size_t(t) * N + p + f.P * (jp / parts)];
+        load_item(jp, np, xp);
+        gp = f.gate[size_t(t) * N + np];
+      }
       for (int n = tid - G0 * kWave; n < N; n += GW * kWave) {
         rl.rank[n] = f.rank[size_t(t) * N + n];
         rl.byrank[n] = f.byrank[size_t(t) * N + n];
         rl.gate[n] = f.gate[size_t(t) * N + n];
       }
+      if (ahead) modulate(xp, gp, yp);
     } else {
       budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
     }
@@ -249,75 +298,30 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
       if (tid == 0 && f.offset_out) f.offset_out[T] = s_off[T];
     }
   }
-
-  // this wave's first item after the ones read ahead: its block reads go out
-  // now, to land while the positions are formed
   const int mine = nt > p ? (nt - p + f.P - 1) / f.P : 0;  // kept tokens of this workgroup
   const int nitems = mine * parts;
+
+  // ---- B. the rows: the read-ahead one (if its token is kept), then the
+  // rest, the next item's block reads in flight while one is finished ----
+  auto item_token = [&](int j) { return rl.byrank[p + f.P * (j / parts)]; };
   u32x4 xa[U][4];
-  if (npre + wave < nitems) load_item(npre + wave, rl.byrank[p + f.P * ((npre + wave) / parts)], xa);
-
-  // ---- B. raster positions of the kept tokens (ballots, one token per thread and round) ----
-  int run = 0;  // kept tokens of earlier rounds
-  for (int n0 = 0; n0 < N; n0 += kThreads) {
-    const int n = n0 + tid;
-    const int r = n < N ? rl.rank[n] : 0;
-    const bool kept = n < N && r < nt;
-    const uint64_t m = __ballot(kept);
-    if (lane == 0) s_cnt[wave] = __popcll(m);
-    lds_barrier();
-    int before = run, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kNW; ++w) {
-      const int cw = s_cnt[w];
-      before += w < wave ? cw : 0;
-      tot += cw;
-    }
-    if (kept) s_posr[r] = before + __popcll(m & ((1ull << lane) - 1ull));
-    run += tot;
-    lds_barrier();
+  int j = npre + wave;
+  if (j < nitems) load_item(j, item_token(j), xa);
+  if (ahead && jp < nitems) {
+    const long long k = base + position(np, nt);
+    if (k >= 0 && k < total) store_item(jp, np, k, yp);
   }
-
-  // ---- C. reconstruction of the kept tokens of rank p, p + P, ... ----
-  auto finish_item = [&](int j, const u32x4 (&x)[U][4]) {
-    const int r = p + f.P * (j / parts);
-    const long long k = base + s_posr[r];
-    if (k < 0 || k >= total) return;
-    const int n = rl.byrank[r];
-    const float g = rl.gate[n];
-    const float c = 0.25f * (1.f - g);
-    const __amdgpu_buffer_rsrc_t ores =
-        make_rsrc_uniform(static_cast<Out*>(f.out_tokens) + size_t(k) * f.C, uint32_t(f.C) * sizeof(Out));
-    const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int v = vb + u * kWave + lane;
-      float x0[V], x1[V], x2[V], x3[V], y[V];
-      Vec16<In>::widen(x[u][0], x0);
-      Vec16<In>::widen(x[u][1], x1);
-      Vec16<In>::widen(x[u][2], x2);
-      Vec16<In>::widen(x[u][3], x3);
-#pragma unroll
-      for (int e = 0; e < V; ++e) {
-        // The orthonormal 2-D Haar butterflies of the block (Eq. (12)), the
-        // three detail bands times the gate (Eq. (13)-(14)) and the inverse
-        // at the token's own position (Eq. (15)) come to mu + g (x - mu),
-        // mu the block mean: the approximation band alone synthesises mu at
-        // every position and the detail bands alone x - mu.
-        y[e] = fmaf(c, (x0[e] + x1[e]) + (x2[e] + x3[e]), g * x0[e]);
-      }
-      if (v < ve) store_row<Out, V>(ores, v * V * int(sizeof(Out)), y);
-    }
-    if (j % parts == 0 && lane == 0) f.out_index[k] = t * N + n;
-  };
-  // blocks read ahead whose token is kept, then the rest
-  if (wave >= G0 && wave - G0 < npre && wave - G0 < nitems) finish_item(wave - G0, xp);
-  // the rest, the next item's reads in flight while one is finished
-  for (int j = npre + wave; j < nitems; j += kNW) {
+  for (; j < nitems; j += kNW) {
     u32x4 xb[U][4];
     const int jn = j + kNW;
-    if (jn < nitems) load_item(jn, rl.byrank[p + f.P * (jn / parts)], xb);
-    finish_item(j, xa);
+    if (jn < nitems) load_item(jn, item_token(jn), xb);
+    const int n = item_token(j);
+    const long long k = base + position(n, nt);
+    if (k >= 0 && k < total) {
+      float y[U][V];
+      modulate(xa, rl.gate[n], y);
+      store_item(j, n, k, y);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
