@@ -334,15 +334,14 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
                                     int32_t* __restrict__ budget, int32_t* __restrict__ offset,
                                     float* __restrict__ rel_rect) {
   const double inv_sqrt2 = 0.70710678118654752440;
-  auto dmin = [](double a, double b) { return fmin(a, b); };
-  auto dmax = [](double a, double b) { return fmax(a, b); };
   auto dadd = [](double a, double b) { return a + b; };
   const int lane = threadIdx.x & 63;
   const bool valid = lane < T;
 
   // ---- gamma = min-max(delta); retained set M in temporal order ----
-  const double lo = wave_reduce_f64(valid ? d : INFINITY, dmin);
-  const double hi = wave_reduce_f64(valid ? d : -INFINITY, dmax);
+  // delta arrives in fp32, so its extremes are exact in fp32
+  const double lo = double(wave_min_f32(valid ? float(d) : INFINITY));
+  const double hi = double(wave_max_f32(valid ? float(d) : -INFINITY));
   const double gam = hi > lo ? (d - lo) / (hi - lo) : 0.0;
   const bool keep = valid && (lane == 0 || d >= double(tau));
   const uint64_t kmask = __ballot(keep);
@@ -413,8 +412,13 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
       // they fit, else the search continues among them; positions still tied
       // after the last bit go by index.
       const uint64_t fb = __builtin_bit_cast(uint64_t, frac);
+      // bits on which every active position agrees decide nothing: start
+      // below them
+      const uint64_t any = wave_reduce_u64(act ? fb : 0ull, [](uint64_t x, uint64_t y) { return x | y; });
+      const uint64_t all = wave_reduce_u64(act ? fb : ~0ull, [](uint64_t x, uint64_t y) { return x & y; });
+      const int top = (any ^ all) ? 63 - __clzll(any ^ all) : -1;
       uint64_t cand = active, chosen = 0;
-      for (int bit = 61; bit >= 0 && need > 0; --bit) {
+      for (int bit = top; bit >= 0 && need > 0; --bit) {
         if (__popcll(cand) <= need) break;
         const uint64_t ones = cand & __ballot((fb >> bit) & 1ull);
         const int c1 = __popcll(ones);
@@ -439,12 +443,7 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
   const int nb = __shfl(n, pos, kWave);
   const double rt = __shfl(x, pos, kWave);
   const int bt = keep ? nb : 0;
-  int incl = bt;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int v = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += v;
-  }
+  const int incl = wave_incl_scan_i32(bt);
   if (valid) {
     budget[lane] = bt;
     offset[lane] = incl - bt;

@@ -169,6 +169,24 @@ __device__ __forceinline__ double wave_reduce_f64(double v, Op op) {
   v = op(v, dpp_f64<kDppMirror>(v));
   return op(op(readlane_f64(v, 0), readlane_f64(v, 16)), op(readlane_f64(v, 32), readlane_f64(v, 48)));
 }
+template <typename Op>
+__device__ __forceinline__ uint64_t wave_reduce_u64(uint64_t v, Op op) {
+  auto dpp = [](uint64_t x, auto ctrl) {
+    constexpr int c = decltype(ctrl)::value;
+    const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(x)), c, 0xF, 0xF, false));
+    const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(x >> 32)), c, 0xF, 0xF, false));
+    return (uint64_t(hi) << 32) | lo;
+  };
+  auto rl = [](uint64_t x, int l) {
+    return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(x >> 32)), l))) << 32) |
+           uint32_t(__builtin_amdgcn_readlane(int(uint32_t(x)), l));
+  };
+  v = op(v, dpp(v, std::integral_constant<int, kDppXor1>{}));
+  v = op(v, dpp(v, std::integral_constant<int, kDppXor2>{}));
+  v = op(v, dpp(v, std::integral_constant<int, kDppHalfMirror>{}));
+  v = op(v, dpp(v, std::integral_constant<int, kDppMirror>{}));
+  return op(op(rl(v, 0), rl(v, 16)), op(rl(v, 32), rl(v, 48)));
+}
 __device__ __forceinline__ int wave_reduce_sum_i32(int v) {
   v += dpp_i32<kDppXor1>(v);
   v += dpp_i32<kDppXor2>(v);
