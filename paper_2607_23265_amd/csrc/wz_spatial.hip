@@ -14,10 +14,15 @@
 //      tokens this workgroup will emit: most frames keep at least three
 //      quarters of the mean budget, so that work is rarely wasted and it
 //      overlaps the budget;
-//   B. the frame keeps its n_t tokens of rank < n_t; kept tokens of rank
-//      p, p + P, ... are emitted, each split into channel parts of at most two
-//      16-byte vectors per lane, one part per wave at a time, the next part's
-//      block reads in flight meanwhile.  A token's row is its 2x2 Haar block
+//   B. the frame keeps its n_t tokens of rank < n_t.  Each token is emitted
+//      in channel parts of at most two 16-byte vectors per lane, one part per
+//      wave at a time.  The read-ahead rows go out first; the kept tokens of
+//      higher rank of ALL frames are then shared out evenly over all
+//      workgroups (every workgroup knows every budget), so frames with large
+//      budgets do not leave a few CUs working alone.  With the offsets given
+//      (T > 256, or the stage on its own) each workgroup emits its frame's
+//      kept tokens of rank p, p + P, ... instead, the next part's block reads
+//      in flight while one is finished.  A token's row is its 2x2 Haar block
 //      (the last row / column repeated when H or W is odd) through the
 //      orthonormal butterflies (Eq. (12)), the three detail bands multiplied
 //      by the block's gate (Eq. (13)-(14)) and the inverse at the token's
@@ -119,6 +124,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   extern __shared__ __align__(16) char s_dyn[];
   __shared__ int32_t s_nb[kFusedTMax];       // budgets (budget modes)
   __shared__ int32_t s_off[kFusedTMax + 1];  // offsets (budget modes)
+  __shared__ int32_t s_ext[kFusedTMax + 1];  // kept tokens of rank >= kp in the frames before t (budget modes)
   __shared__ float s_mm[2 * kNW];
   __shared__ int s_start[kBins], s_fill[kBins];
 
@@ -148,27 +154,30 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   // is part j % parts of the token of rank p + P * (j / parts).  The first
   // items, one per reading wave and for ranks below kpre, are read before the
   // budget is known.
-  const int kp = min(f.kpre, N);
-  const int npre = given && kp > p ? min(GW, (kp - p + f.P - 1) / f.P * parts) : 0;
+  // ranks below kp are read ahead (before the budget), each by its frame's
+  // workgroup p = rank mod P, one item per reading wave
+  const int kp = given ? min(min(f.kpre, N), f.P * (GW / parts)) : 0;
+  const int npre = kp > p ? (kp - p + f.P - 1) / f.P * parts : 0;
   // the four rows of token n's 2x2 block, the token's own row first: the
   // block's other row h2 and column w2 (the last row / column repeated when
   // H or W is odd)
-  auto load_item = [&](int j, int n, u32x4 (&x)[U][4]) {
+  auto load_rows = [&](__amdgpu_buffer_rsrc_t xr, int part, int n, u32x4 (&x)[U][4]) {
     const int h = n / f.W, w = n - h * f.W;
     const int h2 = (h & 1) ? h - 1 : min(h + 1, f.H - 1), w2 = (w & 1) ? w - 1 : min(w + 1, f.W - 1);
     const int r0 = (h * f.W + w) * rb, r1 = (h * f.W + w2) * rb;
     const int r2 = (h2 * f.W + w) * rb, r3 = (h2 * f.W + w2) * rb;
-    const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
+    const int vb = part * vpp, ve = min(nvec, vb + vpp);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = vb + u * kWave + lane;
       const int cb = v < ve ? v * 16 : kOOB;
-      x[u][0] = __builtin_amdgcn_raw_buffer_load_b128(xres, r0 + cb, 0, 0);
-      x[u][1] = __builtin_amdgcn_raw_buffer_load_b128(xres, r1 + cb, 0, 0);
-      x[u][2] = __builtin_amdgcn_raw_buffer_load_b128(xres, r2 + cb, 0, 0);
-      x[u][3] = __builtin_amdgcn_raw_buffer_load_b128(xres, r3 + cb, 0, 0);
+      x[u][0] = __builtin_amdgcn_raw_buffer_load_b128(xr, r0 + cb, 0, 0);
+      x[u][1] = __builtin_amdgcn_raw_buffer_load_b128(xr, r1 + cb, 0, 0);
+      x[u][2] = __builtin_amdgcn_raw_buffer_load_b128(xr, r2 + cb, 0, 0);
+      x[u][3] = __builtin_amdgcn_raw_buffer_load_b128(xr, r3 + cb, 0, 0);
     }
   };
+  auto load_item = [&](int j, int n, u32x4 (&x)[U][4]) { load_rows(xres, j % parts, n, x); };
 
   // ---- A. budgets; ranks and gates; the first blocks ----
   double bd = 0.0, br = 0.0;
@@ -214,18 +223,39 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
     }
     return before;
   };
-  // row k of the output: the channel part of item j
-  auto store_item = [&](int j, int n, long long k, const float (&y)[U][V]) {
+  // row k of the output: channel part `part` of token n of frame tf
+  auto store_rows = [&](int part, int tf, int n, long long k, const float (&y)[U][V]) {
     const __amdgpu_buffer_rsrc_t ores =
         make_rsrc_uniform(static_cast<Out*>(f.out_tokens) + size_t(k) * f.C, uint32_t(f.C) * sizeof(Out));
-    const int vb = (j % parts) * vpp, ve = min(nvec, vb + vpp);
+    const int vb = part * vpp, ve = min(nvec, vb + vpp);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int v = vb + u * kWave + lane;
       if (v < ve) store_row<Out, V>(ores, v * V * int(sizeof(Out)), y[u]);
     }
-    if (j % parts == 0 && lane == 0) f.out_index[k] = t * N + n;
+    if (part == 0 && lane == 0) f.out_index[k] = tf * N + n;
   };
+  auto store_item = [&](int j, int n, long long k, const float (&y)[U][V]) { store_rows(j % parts, t, n, k, y); };
+
+  // s_ext[t] = kept tokens of rank >= kp in frames before t (one wave; the
+  // budgets are in s_nb)
+  auto extra_prefix = [&]() {
+    int carry = 0;
+    for (int t0 = 0; t0 < T; t0 += kWave) {
+      const int tt = t0 + lane;
+      const int e = tt < T ? max(0, s_nb[tt] - kp) : 0;
+      const int incl = wave_incl_scan_i32(e);
+      if (tt < T) s_ext[tt + 1] = carry + incl;
+      carry += __builtin_amdgcn_readlane(incl, kWave - 1);
+    }
+    if (lane == 0) s_ext[0] = 0;
+  };
+  if constexpr (MODE == kBlockBudget) {
+    if (given) {
+      lds_barrier();  // budgets of budget_body visible to wave 0
+      if (wave == 0) extra_prefix();
+    }
+  }
 
   // read-ahead item of this wave (waves G0.., item wave - G0): its block and
   // gate are read and the row formed while the budgets are computed
@@ -250,6 +280,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
       if (ahead) modulate(xp, gp, yp);
     } else {
       budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+      extra_prefix();
     }
   } else {
     // the frame's order from its scores, all waves (after the budgets)
@@ -304,28 +335,83 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
   // ---- B. the rows: the read-ahead one (if its token is kept), then the
   // rest, the next item's block reads in flight while one is finished ----
   auto item_token = [&](int j) { return rl.byrank[p + f.P * (j / parts)]; };
-  u32x4 xa[U][4];
-  int j = npre + wave;
-  if (j < nitems) load_item(j, item_token(j), xa);
   if (ahead && jp < nitems) {
     const long long k = base + position(np, nt);
     if (k >= 0 && k < total) store_item(jp, np, k, yp);
   }
-  for (; j < nitems; j += kNW) {
-    u32x4 xb[U][4];
-    const int jn = j + kNW;
-    if (jn < nitems) load_item(jn, item_token(jn), xb);
-    const int n = item_token(j);
-    const long long k = base + position(n, nt);
-    if (k >= 0 && k < total) {
-      float y[U][V];
-      modulate(xa, rl.gate[n], y);
-      store_item(j, n, k, y);
+  if (MODE == kOffsets || !given) {
+    // offsets given: this workgroup's other kept tokens of its frame
+    u32x4 xa[U][4];
+    int j = npre + wave;
+    if (j < nitems) load_item(j, item_token(j), xa);
+    for (; j < nitems; j += kNW) {
+      u32x4 xb[U][4];
+      const int jn = j + kNW;
+      if (jn < nitems) load_item(jn, item_token(jn), xb);
+      const int n = item_token(j);
+      const long long k = base + position(n, nt);
+      if (k >= 0 && k < total) {
+        float y[U][V];
+        modulate(xa, rl.gate[n], y);
+        store_item(j, n, k, y);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) xa[u][q] = xb[u][q];
     }
+    return;
+  }
+  // Kept tokens of rank >= kp of every frame, in (frame, rank) order and
+  // split into channel parts, are shared out evenly over all T * P
+  // workgroups, whatever the frames' budgets: item i of this workgroup's
+  // share is token e = i / parts of that list (frame te, rank kp + e -
+  // s_ext[te]), part i % parts.  Its token, gate and the frame's ranks come
+  // from the per-frame kernel's arrays.
+  const long long items = (long long)s_ext[T] * parts, groups = (long long)T * f.P, g = (long long)t * f.P + p;
+  const long long i1 = (g + 1) * items / groups;
+  for (long long i = g * items / groups + wave; i < i1; i += kNW) {
+    const long long e = i / parts;
+    const int part = int(i - e * parts);
+    int lo = 0, hi = T;  // s_ext[lo] <= e < s_ext[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_ext[mid] <= e) lo = mid;
+      else hi = mid;
+    }
+    const int te = lo, nte = s_nb[te], rank = kp + int(e - s_ext[te]);
+    u32x4 x[U][4];
+    int n, before = 0;
+    float gn;
+    if (te == t) {  // this workgroup's own frame: its order is in LDS
+      n = rl.byrank[rank];
+      load_item(part, n, x);
+      gn = rl.gate[n];
+      before = position(n, nte);
+    } else {
+      const size_t fo = size_t(te) * N;
+      n = f.byrank[fo + rank];
+      load_rows(make_rsrc(static_cast<const In*>(f.X) + fo * f.C, uint32_t(N) * rb), part, n, x);
+      gn = f.gate[fo + n];
+      // kept tokens of frame te before n in raster order
+      const __amdgpu_buffer_rsrc_t rres = make_rsrc(f.rank + fo, uint32_t(N) * 4);
+      for (int m0 = 0; m0 < n; m0 += 4 * kWave) {
+        int rv[4];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+        for (int u = 0; u < 4; ++u) {
+          const int m = m0 + u * kWave + lane;
+          rv[u] = buf_load_i32(rres, m < n ? m * 4 : kOOB);
+        }
 #pragma unroll
-      for (int q = 0; q < 4; ++q) xa[u][q] = xb[u][q];
+        for (int u = 0; u < 4; ++u) before += __popcll(__ballot(m0 + u * kWave + lane < n && rv[u] < nte));
+      }
+    }
+    const long long k = (long long)s_off[te] + before;
+    if (k < total) {
+      float y[U][V];
+      modulate(x, gn, y);
+      store_rows(part, te, n, k, y);
+    }
   }
 }
 
