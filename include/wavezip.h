@@ -15,7 +15,8 @@
  *   wz_spatial_dwt_condense saliency map, per-frame selection and the
  *                           saliency-gated 2-D Haar modulation, compacted in
  *                           temporal order (Eq. (7), Eq. (12)-(15), Eq. (19));
- *   wz_condense             the three stages in sequence.
+ *   wz_condense             the three stages in sequence;
+ *   wz_condense_batch       the same for several videos at once.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -161,6 +162,23 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query,
                       int32_t* offset, void* ws, size_t ws_bytes, void* stream);
 
 /* Static, human-readable name of a status code.                               */
+/* Several videos of one shape condensed in one call: the whole pass of
+ * wz_condense for each of `videos` videos (1 <= videos <= 8, else
+ * WZ_ERR_SHAPE), every kernel launched once for all of them, so launch and
+ * kernel-boundary costs are shared and the videos' work overlaps (a
+ * throughput mode for short videos; each video keeps its own query and its
+ * own budget B).  Layouts add a leading video index: X [V][T][H][W][C],
+ * query [V][Q][C], out_tokens [V][B][C], out_index [V][B] (flat index within
+ * the video), budget [V][T] and offset [V][T+1] (optional, NULL: kept in the
+ * workspace).  ws: at least videos * wz_workspace_bytes(cfg) bytes, video v
+ * using the v-th slice of that size.  Video v's outputs are bitwise those of
+ * wz_condense on video v alone.                                             */
+wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X,
+                            const void* query, void* out_tokens,
+                            int32_t* out_index, int32_t* budget,
+                            int32_t* offset, void* ws, size_t ws_bytes,
+                            void* stream);
+
 const char* wz_status_str(wz_status s);
 
 #ifdef __cplusplus

@@ -41,6 +41,53 @@ wz_status from_hip(hipError_t e) { return e == hipSuccess ? WZ_OK : WZ_ERR_DEVIC
 
 }  // namespace
 
+namespace {
+
+// The whole pass for V videos of one shape (wz_condense, wz_condense_batch).
+wz_status condense_videos(const wz_config* cfg, int V, const void* X, const void* query, void* out_tokens,
+                          int32_t* out_index, int32_t* budget, int32_t* offset, void* ws, size_t ws_bytes,
+                          void* stream) {
+  WZ_TRY(check_config(cfg));
+  WZ_TRY(check_ptr(X, 16));
+  WZ_TRY(check_ptr(query, 16));
+  if (cfg->B > 0) {
+    WZ_TRY(check_ptr(out_tokens, 16));
+    WZ_TRY(check_ptr(out_index, 4));
+  }
+  if (budget && !aligned(budget, 4)) return WZ_ERR_ALIGN;
+  if (offset && !aligned(offset, 4)) return WZ_ERR_ALIGN;
+  if (!ws) return WZ_ERR_NULL;
+  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
+  if (!aligned(ws, 256) || ws_bytes / size_t(V) < w.bytes) return WZ_ERR_WORKSPACE;
+  const int s_in = cfg->in_dtype == WZ_BF16 ? 2 : 4, s_out = cfg->out_dtype == WZ_BF16 ? 2 : 4;
+  const long long TN = (long long)cfg->T * cfg->H * cfg->W;
+  Videos vs;
+  vs.V = V;
+  vs.x = TN * cfg->C * s_in;
+  vs.q = (long long)cfg->Q * cfg->C * s_in;
+  vs.ws = (long long)w.bytes;
+  vs.out = cfg->B * cfg->C * s_out;
+  vs.idx = cfg->B * 4;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s, vs)));
+  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s, vs)));
+  vs.bud = budget ? (long long)cfg->T * 4 : vs.ws;
+  vs.off = offset ? ((long long)cfg->T + 1) * 4 : vs.ws;
+  if (cfg->T <= kFusedTMax) {  // budgets computed inside the selection kernel
+    vs.bud = (long long)cfg->T * 4;
+    vs.off = ((long long)cfg->T + 1) * 4;
+    return from_hip(launch_assign_gather(*cfg, X, w.tok_score, w.frame_rel, w.frame_delta, nullptr, &w, budget,
+                                         offset, out_tokens, out_index, s, vs));
+  }
+  int32_t* bud = budget ? budget : w.budget;
+  int32_t* off = offset ? offset : w.offset;
+  WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s, vs)));
+  return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, &w, nullptr, nullptr, out_tokens,
+                                       out_index, s, vs));
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t wz_workspace_bytes(const wz_config* cfg) {
@@ -120,29 +167,14 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
 wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
                       int32_t* out_index, int32_t* budget, int32_t* offset, void* ws, size_t ws_bytes,
                       void* stream) {
-  WZ_TRY(check_config(cfg));
-  WZ_TRY(check_ptr(X, 16));
-  WZ_TRY(check_ptr(query, 16));
-  if (cfg->B > 0) {
-    WZ_TRY(check_ptr(out_tokens, 16));
-    WZ_TRY(check_ptr(out_index, 4));
-  }
-  if (budget && !aligned(budget, 4)) return WZ_ERR_ALIGN;
-  if (offset && !aligned(offset, 4)) return WZ_ERR_ALIGN;
-  if (!ws) return WZ_ERR_NULL;
-  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
-  if (!aligned(ws, 256) || ws_bytes < w.bytes) return WZ_ERR_WORKSPACE;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s)));
-  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s)));
-  if (cfg->T <= kFusedTMax)  // budgets computed inside the selection kernel
-    return from_hip(launch_assign_gather(*cfg, X, w.tok_score, w.frame_rel, w.frame_delta, nullptr, &w, budget,
-                                         offset, out_tokens, out_index, s));
-  int32_t* bud = budget ? budget : w.budget;
-  int32_t* off = offset ? offset : w.offset;
-  WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s)));
-  return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, &w, nullptr, nullptr, out_tokens,
-                                       out_index, s));
+  return condense_videos(cfg, 1, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes, stream);
+}
+
+wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X, const void* query,
+                            void* out_tokens, int32_t* out_index, int32_t* budget, int32_t* offset, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if (videos < 1 || videos > kMaxVideos) return WZ_ERR_SHAPE;
+  return condense_videos(cfg, videos, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -43,6 +43,7 @@ struct FrameArgs {
   int roles;               // workgroups per frame: 1 + (scores or order role)
   float lam;
 };
+static_assert(sizeof(VideoArgs<FrameArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
 // scores (and order) of frame t
 template <int NTH>
@@ -295,7 +296,8 @@ __device__ void lead_role(const FrameArgs& f, int t) {
 // frame runs on the XCD that streamed it), role (b / 8) % roles; the last role
 // is the lead.
 template <int NTH>
-__global__ __launch_bounds__(NTH) void k_frame(const FrameArgs f) {
+__global__ __launch_bounds__(NTH) void k_frame(const VideoArgs<FrameArgs> va) {
+  const FrameArgs& f = va.v[blockIdx.y];
   const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
   const int t = (slot / f.roles) * kXcds + xcd, role = slot % f.roles;
   if (t >= f.T) return;
@@ -306,18 +308,26 @@ __global__ __launch_bounds__(NTH) void k_frame(const FrameArgs f) {
 }  // namespace
 
 hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
-                        float* frame_delta, bool order, hipStream_t s) {
+                        float* frame_delta, bool order, hipStream_t s, const Videos& vs) {
   const RelPlan pl = relevance_plan(c);
   const int N = c.H * c.W;
   const int roles = (pl.slices > 1 || order) ? 2 : 1;
-  FrameArgs fa{ws.s_part, ws.g_part,  ws.qg_part,   ws.sig_part, ws.pool_part, tok_score, frame_rel,
-               frame_delta, ws.rank,  ws.byrank,    ws.gate,     c.T,          N,         c.H,
-               c.W,       c.C,        c.Q,          qpad(c.Q),   pl.tiles,     pl.slices, order ? 1 : 0,
-               roles,     c.lambda_};
+  VideoArgs<FrameArgs> va{};
+  for (int v = 0; v < vs.V; ++v) {
+    const Workspace w = advance(ws, v * vs.ws);
+    va.v[v] = FrameArgs{w.s_part,   w.g_part,  w.qg_part,
+                        w.sig_part, w.pool_part, advance(tok_score, v * vs.ws),
+                        advance(frame_rel, v * vs.ws), advance(frame_delta, v * vs.ws), w.rank,
+                        w.byrank,   w.gate,    c.T,
+                        N,          c.H,       c.W,
+                        c.C,        c.Q,       qpad(c.Q),
+                        pl.tiles,   pl.slices, order ? 1 : 0,
+                        roles,      c.lambda_};
+  }
   const size_t lds = roles == 2 ? size_t(N) * 24 : 0;  // key 8 B; rank, byrank, gate, bin order 4 B
-  const dim3 grid((c.T + kXcds - 1) / kXcds * kXcds * roles);
-  if (pl.slices > 1) hipLaunchKernelGGL((k_frame<kPartThreads>), grid, dim3(kPartThreads), lds, s, fa);
-  else hipLaunchKernelGGL((k_frame<kThreads>), grid, dim3(kThreads), lds, s, fa);
+  const dim3 grid((c.T + kXcds - 1) / kXcds * kXcds * roles, vs.V);
+  if (pl.slices > 1) hipLaunchKernelGGL((k_frame<kPartThreads>), grid, dim3(kPartThreads), lds, s, va);
+  else hipLaunchKernelGGL((k_frame<kThreads>), grid, dim3(kThreads), lds, s, va);
   return hipGetLastError();
 }
 

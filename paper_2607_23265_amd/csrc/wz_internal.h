@@ -178,20 +178,57 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   return w;
 }
 
-// Kernel launchers (each returns hipGetLastError() of its launches).
+// Several videos in one launch: video v = blockIdx.y of every kernel works
+// on X + v*x, query + v*q, the workspace and every intermediate kept in it
+// + v*ws, out_tokens + v*out, out_index + v*idx, budget + v*bud and
+// offset + v*off (byte strides).  Each kernel receives one argument set per
+// video, so its body sees a single video.
+constexpr int kMaxVideos = 8;
+struct Videos {
+  int V = 1;
+  long long x = 0, q = 0, ws = 0, out = 0, idx = 0, bud = 0, off = 0;
+};
+template <typename A>
+struct VideoArgs {
+  A v[kMaxVideos];
+};
+template <typename P>
+inline P* advance(P* p, long long bytes) {
+  return p ? reinterpret_cast<P*>(reinterpret_cast<uintptr_t>(p) + bytes) : p;
+}
+inline Workspace advance(const Workspace& w, long long bytes) {
+  Workspace o = w;
+  o.s_part = advance(w.s_part, bytes);
+  o.g_part = advance(w.g_part, bytes);
+  o.qg_part = advance(w.qg_part, bytes);
+  o.sig_part = advance(w.sig_part, bytes);
+  o.pool_part = advance(w.pool_part, bytes);
+  o.tok_score = advance(w.tok_score, bytes);
+  o.rank = advance(w.rank, bytes);
+  o.byrank = advance(w.byrank, bytes);
+  o.gate = advance(w.gate, bytes);
+  o.frame_rel = advance(w.frame_rel, bytes);
+  o.frame_delta = advance(w.frame_delta, bytes);
+  o.budget = advance(w.budget, bytes);
+  o.offset = advance(w.offset, bytes);
+  return o;
+}
+
+// Kernel launchers (each returns hipGetLastError() of its launches; `vs`
+// batches videos, one by default).
 // Streaming pass of stage 1: per-unit partials into ws (and a_{t,n} into
 // tok_score when there is one channel slice).
 hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void* query, float* tok_score,
-                                   const Workspace& ws, hipStream_t s);
+                                   const Workspace& ws, hipStream_t s, const Videos& vs = Videos{});
 // Per-frame finish of stage 1: a_{t,n} (several slices), r_t and delta_t;
 // with `order` also every frame's selection ranks and block gates (into
 // ws.rank, ws.byrank, ws.gate) for launch_assign_gather.
 hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_score, float* frame_rel,
-                        float* frame_delta, bool order, hipStream_t s);
+                        float* frame_delta, bool order, hipStream_t s, const Videos& vs = Videos{});
 // Budgets alone, in one workgroup (wz_temporal_budget, and wz_condense when
 // T > kFusedTMax).
 hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float* frame_delta, int32_t* budget,
-                         int32_t* offset, float* rel_rect, hipStream_t s);
+                         int32_t* offset, float* rel_rect, hipStream_t s, const Videos& vs = Videos{});
 // Selection, spatial modulation and compaction.  With offset_in the frames'
 // row offsets are given; without it (T <= kFusedTMax) every workgroup computes
 // the budgets from frame_rel and frame_delta itself and workgroup 0 writes
@@ -201,8 +238,8 @@ hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float
 hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* tok_score, const float* frame_rel,
                                 const float* frame_delta, const int32_t* offset_in, const Workspace* ws,
                                 int32_t* budget_out, int32_t* offset_out, void* out_tokens, int32_t* out_index,
-                                hipStream_t s);
-// Workgroups per frame of launch_assign_gather.
-int assign_groups_per_frame(const wz_config& c);
+                                hipStream_t s, const Videos& vs = Videos{});
+// Workgroups per frame of launch_assign_gather for V videos at once.
+int assign_groups_per_frame(const wz_config& c, int V = 1);
 
 }  // namespace wz

@@ -38,6 +38,8 @@ constexpr int kQMax = 1024;   // validated bound on query tokens
 
 // Per-unit outputs of the streaming pass (layouts in the workspace carve-up).
 struct StreamArgs {
+  const void* X;      // [T][H][W][C]
+  const void* query;  // [Q][C]
   float* s_part;
   float* g_part;
   float* qg_part;
@@ -46,6 +48,7 @@ struct StreamArgs {
   float* tok_score;  // written here when there is one slice
   int T, N, C, Q, QP, tiles, slices;
 };
+static_assert(sizeof(VideoArgs<StreamArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
 // ---------------------------------------------------------------------------
 // MFMA path
@@ -53,10 +56,11 @@ struct StreamArgs {
 // NTG: 16-column query tiles per pass over the slice (queries of more tokens
 // take several passes); R: depth of the X prefetch ring in 32-channel steps.
 template <int NTG, int R>
-__global__ __launch_bounds__(kMaxWaves / kTilesPerWave * 64) void k_relevance_mfma(const uint16_t* __restrict__ X,
-                                                                                   const uint16_t* __restrict__ query,
-                                                                                   int tile_tokens, int kc,
-                                                                                   StreamArgs f) {
+__global__ __launch_bounds__(kMaxWaves / kTilesPerWave * 64) void k_relevance_mfma(
+    int tile_tokens, int kc, const VideoArgs<StreamArgs> va) {
+  const StreamArgs f = va.v[blockIdx.y];
+  const uint16_t* __restrict__ X = static_cast<const uint16_t*>(f.X);
+  const uint16_t* __restrict__ query = static_cast<const uint16_t*>(f.query);
   constexpr int MTW = kTilesPerWave;
   constexpr int MAXW = kMaxWaves / MTW;
   constexpr int QB = 8;                          // query units staged per thread per batch
@@ -337,9 +341,10 @@ constexpr int kTokPoolMax = 8192;  // channels whose sums are gathered in LDS
 // POOL: the tile's channel sums are gathered in LDS (C <= kTokPoolMax) and
 // stored once at the end; otherwise a few lanes store them chunk by chunk.
 template <int NTG, int IPC, bool POOL>
-__global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(const uint16_t* __restrict__ X,
-                                                                 const uint16_t* __restrict__ query,
-                                                                 int tile_tokens, StreamArgs f) {
+__global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_tokens, const VideoArgs<StreamArgs> va) {
+  const StreamArgs f = va.v[blockIdx.y];
+  const uint16_t* __restrict__ X = static_cast<const uint16_t*>(f.X);
+  const uint16_t* __restrict__ query = static_cast<const uint16_t*>(f.query);
   constexpr int NQ = NTG * 16;  // query rows of the accumulators
   constexpr int QI = NQ / 8;    // query load instructions per chunk
   // per-wave chunk buffers (16-byte units swizzled by row); after a wave's
@@ -593,8 +598,10 @@ struct Vec<uint16_t> {
 };
 
 template <typename In>
-__global__ __launch_bounds__(256) void k_relevance_valu(const In* __restrict__ X, const In* __restrict__ query,
-                                                        int tile_tokens, StreamArgs f) {
+__global__ __launch_bounds__(256) void k_relevance_valu(int tile_tokens, const VideoArgs<StreamArgs> va) {
+  const StreamArgs f = va.v[blockIdx.y];
+  const In* __restrict__ X = static_cast<const In*>(f.X);
+  const In* __restrict__ query = static_cast<const In*>(f.query);
   constexpr int NW = 4;
   constexpr int V = Vec<In>::kN;
   constexpr int QB = 16;
@@ -697,20 +704,19 @@ __global__ __launch_bounds__(256) void k_relevance_valu(const In* __restrict__ X
 #endif
 
 template <int NTG>
-void launch_mfma(const RelPlan& pl, const void* X, const void* query, const StreamArgs& fa, hipStream_t s) {
-  hipLaunchKernelGGL((k_relevance_mfma<NTG, WZ_REL_RING>), dim3(pl.grid), dim3(pl.threads), 0, s,
-                     static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, pl.kc,
-                     fa);
+void launch_mfma(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
+  hipLaunchKernelGGL((k_relevance_mfma<NTG, WZ_REL_RING>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens,
+                     pl.kc, va);
 }
 
 template <int NTG, int IPC>
-void launch_tok(const RelPlan& pl, const void* X, const void* query, const StreamArgs& fa, hipStream_t s) {
-  if (fa.C <= kTokPoolMax)
-    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true>), dim3(pl.grid), dim3(pl.threads), 0, s,
-                       static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, fa);
+void launch_tok(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
+  if (va.v[0].C <= kTokPoolMax)
+    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens,
+                       va);
   else
-    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false>), dim3(pl.grid), dim3(pl.threads), 0, s,
-                       static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, fa);
+    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+                       pl.tile_tokens, va);
 }
 
 }  // namespace
@@ -723,34 +729,38 @@ RelKind relevance_kind(const wz_config& c) {
 }
 
 hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void* query, float* tok_score,
-                                   const Workspace& ws, hipStream_t s) {
+                                   const Workspace& ws, hipStream_t s, const Videos& vs) {
   const RelPlan pl = relevance_plan(c);
-  const StreamArgs fa{ws.s_part, ws.g_part, ws.qg_part, ws.sig_part, ws.pool_part, tok_score, c.T, c.H * c.W,
-                      c.C,       c.Q,       qpad(c.Q),  pl.tiles,    pl.slices};
+  VideoArgs<StreamArgs> va{};
+  for (int v = 0; v < vs.V; ++v) {
+    const Workspace w = advance(ws, v * vs.ws);
+    va.v[v] = StreamArgs{advance(X, v * vs.x), advance(query, v * vs.q), w.s_part, w.g_part, w.qg_part,
+                         w.sig_part, w.pool_part, advance(tok_score, v * vs.ws), c.T, c.H * c.W, c.C, c.Q,
+                         qpad(c.Q), pl.tiles, pl.slices};
+  }
+  const int V = vs.V;
   if (pl.kind == kRelTok) {
-#define WZ_TOK(NTG)                                    \
-  switch (pl.ipc) {                                    \
-    case 1: launch_tok<NTG, 1>(pl, X, query, fa, s); break; \
-    case 2: launch_tok<NTG, 2>(pl, X, query, fa, s); break; \
-    case 3: launch_tok<NTG, 3>(pl, X, query, fa, s); break; \
-    case 4: launch_tok<NTG, 4>(pl, X, query, fa, s); break; \
-    case 5: launch_tok<NTG, 5>(pl, X, query, fa, s); break; \
-    case 6: launch_tok<NTG, 6>(pl, X, query, fa, s); break; \
-    case 7: launch_tok<NTG, 7>(pl, X, query, fa, s); break; \
-    default: launch_tok<NTG, 8>(pl, X, query, fa, s); break; \
+#define WZ_TOK(NTG)                                 \
+  switch (pl.ipc) {                                 \
+    case 1: launch_tok<NTG, 1>(pl, va, V, s); break; \
+    case 2: launch_tok<NTG, 2>(pl, va, V, s); break; \
+    case 3: launch_tok<NTG, 3>(pl, va, V, s); break; \
+    case 4: launch_tok<NTG, 4>(pl, va, V, s); break; \
+    case 5: launch_tok<NTG, 5>(pl, va, V, s); break; \
+    case 6: launch_tok<NTG, 6>(pl, va, V, s); break; \
+    case 7: launch_tok<NTG, 7>(pl, va, V, s); break; \
+    default: launch_tok<NTG, 8>(pl, va, V, s); break; \
   }
     if (pl.ntg == 1) { WZ_TOK(1) } else { WZ_TOK(2) }
 #undef WZ_TOK
   } else if (pl.kind == kRelMfma) {
     // queries of more than 32 tokens take several passes of 32 over the slice:
     // wider query groups no longer fit the accumulators in registers
-    launch_mfma<2>(pl, X, query, fa, s);
+    launch_mfma<2>(pl, va, V, s);
   } else if (c.in_dtype == WZ_BF16) {
-    hipLaunchKernelGGL((k_relevance_valu<uint16_t>), dim3(pl.grid), dim3(pl.threads), 0, s,
-                       static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(query), pl.tile_tokens, fa);
+    hipLaunchKernelGGL((k_relevance_valu<uint16_t>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens, va);
   } else {
-    hipLaunchKernelGGL((k_relevance_valu<float>), dim3(pl.grid), dim3(pl.threads), 0, s,
-                       static_cast<const float*>(X), static_cast<const float*>(query), pl.tile_tokens, fa);
+    hipLaunchKernelGGL((k_relevance_valu<float>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens, va);
   }
   return hipGetLastError();
 }

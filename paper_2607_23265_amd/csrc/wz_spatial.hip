@@ -62,6 +62,7 @@ struct AssignArgs {
   int kpre;  // ranks read before the budget is known (a performance setting)
   float lam, tau;
 };
+static_assert(sizeof(VideoArgs<AssignArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -116,7 +117,8 @@ __device__ __forceinline__ void store_row<uint16_t, 4>(__amdgpu_buffer_rsrc_t r,
 }
 
 template <typename In, typename Out, int U, int MODE>
-__global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) {
+__global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<AssignArgs> va) {
+  const AssignArgs& f = va.v[blockIdx.y];
   constexpr int V = Vec16<In>::kV;
   // waves that read ranks and blocks while wave 0 computes the budgets
   constexpr int G0 = MODE == kWaveBudget ? 1 : 0;
@@ -416,9 +418,9 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const AssignArgs f) 
 }
 
 template <typename In, typename Out, int MODE>
-void launch_typed(const wz_config& c, const AssignArgs& a, hipStream_t s) {
+void launch_typed(const wz_config& c, const VideoArgs<AssignArgs>& a, int V, hipStream_t s) {
   const int nvec = c.C / Vec16<In>::kV;
-  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * a.P)), block(kThreads);
+  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * a.v[0].P), V), block(kThreads);
   const size_t lds = size_t(c.H) * c.W * 24;  // key 8 B; rank, byrank, gate, order / position 4 B
   // one batch of loads per part: two vectors per lane, or one for short rows
   if (nvec <= kWave) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE>), grid, block, lds, s, a);
@@ -426,59 +428,64 @@ void launch_typed(const wz_config& c, const AssignArgs& a, hipStream_t s) {
 }
 
 template <int MODE>
-void launch_mode(const wz_config& c, const AssignArgs& a, hipStream_t s) {
+void launch_mode(const wz_config& c, const VideoArgs<AssignArgs>& a, int V, hipStream_t s) {
   if (c.in_dtype == WZ_BF16) {
-    if (c.out_dtype == WZ_BF16) launch_typed<uint16_t, uint16_t, MODE>(c, a, s);
-    else launch_typed<uint16_t, float, MODE>(c, a, s);
+    if (c.out_dtype == WZ_BF16) launch_typed<uint16_t, uint16_t, MODE>(c, a, V, s);
+    else launch_typed<uint16_t, float, MODE>(c, a, V, s);
   } else {
-    if (c.out_dtype == WZ_BF16) launch_typed<float, uint16_t, MODE>(c, a, s);
-    else launch_typed<float, float, MODE>(c, a, s);
+    if (c.out_dtype == WZ_BF16) launch_typed<float, uint16_t, MODE>(c, a, V, s);
+    else launch_typed<float, float, MODE>(c, a, V, s);
   }
 }
 
 }  // namespace
 
-int assign_groups_per_frame(const wz_config& c) {
-  // about one workgroup per CU over the whole grid, at most 16 per frame;
+int assign_groups_per_frame(const wz_config& c, int V) {
+  // about one workgroup per CU over the whole grid (all V videos), at most 16
+  // per frame;
   // each repeats its frame's ranking (N^2 key comparisons), so large frames
   // get fewer
   const int tr = (c.T + kXcds - 1) / kXcds * kXcds;
   const int cap = std::max(1, std::min(16, 8192 / (c.H * c.W)));
-  return std::max(1, std::min(cap, (kCUs + tr - 1) / tr));
+  return std::max(1, std::min(cap, (kCUs + tr * V - 1) / (tr * V)));
 }
 
 hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* tok_score, const float* frame_rel,
                                 const float* frame_delta, const int32_t* offset_in, const Workspace* ws,
                                 int32_t* budget_out, int32_t* offset_out, void* out_tokens, int32_t* out_index,
-                                hipStream_t s) {
+                                hipStream_t s, const Videos& vs) {
   // three quarters of the mean budget: most frames keep at least that many
   const int kpre = int(std::min<long long>(c.H * c.W, 3 * c.B / (4LL * c.T)));
-  AssignArgs a{};
-  a.X = X;
-  a.tok_score = tok_score;
-  a.rel = frame_rel;
-  a.delta = frame_delta;
-  a.offset_in = offset_in;
-  a.rank = ws ? ws->rank : nullptr;
-  a.byrank = ws ? ws->byrank : nullptr;
-  a.gate = ws ? ws->gate : nullptr;
-  a.budget_out = budget_out;
-  a.offset_out = offset_out;
-  a.out_tokens = out_tokens;
-  a.out_index = out_index;
-  a.B = c.B;
-  a.T = c.T;
-  a.H = c.H;
-  a.W = c.W;
-  a.C = c.C;
-  a.P = assign_groups_per_frame(c);
-  a.levels = c.levels;
-  a.kpre = kpre;
-  a.lam = c.lambda_;
-  a.tau = c.tau;
-  if (offset_in) launch_mode<kOffsets>(c, a, s);
-  else if (c.T <= kWave) launch_mode<kWaveBudget>(c, a, s);
-  else if (c.T <= kFusedTMax) launch_mode<kBlockBudget>(c, a, s);
+  VideoArgs<AssignArgs> va{};
+  for (int v = 0; v < vs.V; ++v) {
+    AssignArgs& a = va.v[v];
+    const long long w = v * vs.ws;
+    a.X = advance(X, v * vs.x);
+    a.tok_score = advance(tok_score, w);
+    a.rel = advance(frame_rel, w);
+    a.delta = advance(frame_delta, w);
+    a.offset_in = advance(offset_in, v * vs.off);
+    a.rank = ws ? advance(ws->rank, w) : nullptr;
+    a.byrank = ws ? advance(ws->byrank, w) : nullptr;
+    a.gate = ws ? advance(ws->gate, w) : nullptr;
+    a.budget_out = advance(budget_out, v * vs.bud);
+    a.offset_out = advance(offset_out, v * vs.off);
+    a.out_tokens = advance(out_tokens, v * vs.out);
+    a.out_index = advance(out_index, v * vs.idx);
+    a.B = c.B;
+    a.T = c.T;
+    a.H = c.H;
+    a.W = c.W;
+    a.C = c.C;
+    a.P = assign_groups_per_frame(c, vs.V);
+    a.levels = c.levels;
+    a.kpre = kpre;
+    a.lam = c.lambda_;
+    a.tau = c.tau;
+  }
+  if (offset_in) launch_mode<kOffsets>(c, va, vs.V, s);
+  else if (c.T <= kWave) launch_mode<kWaveBudget>(c, va, vs.V, s);
+  else if (c.T <= kFusedTMax) launch_mode<kBlockBudget>(c, va, vs.V, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

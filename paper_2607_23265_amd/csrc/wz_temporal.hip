@@ -8,29 +8,40 @@
 namespace wz {
 namespace {
 
+struct BudgetArgs {
+  const float* rel;
+  const float* delta;
+  int32_t* budget;
+  int32_t* offset;
+  float* rel_rect;
+};
+static_assert(sizeof(VideoArgs<BudgetArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
+
 template <int NT, int TV>
-__global__ __launch_bounds__(NT) void k_budget(const float* __restrict__ rel, const float* __restrict__ delta,
-                                               int T, int N, long long B, int levels, float tau,
-                                               int32_t* __restrict__ budget, int32_t* __restrict__ offset,
-                                               float* __restrict__ rel_rect) {
-  if constexpr (NT == kWave) budget_wave_body(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
-  else budget_body<NT, TV>(rel, delta, T, N, B, levels, tau, budget, offset, rel_rect);
+__global__ __launch_bounds__(NT) void k_budget(const VideoArgs<BudgetArgs> va, int T, int N, long long B, int levels,
+                                               float tau) {
+  const BudgetArgs& a = va.v[blockIdx.y];
+  if constexpr (NT == kWave) budget_wave_body(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
+  else budget_body<NT, TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
 }
 
 template <int NT, int TV>
-void launch_k(const wz_config& c, const float* rel, const float* delta, int32_t* budget, int32_t* offset,
-              float* rel_rect, hipStream_t s) {
-  hipLaunchKernelGGL((k_budget<NT, TV>), dim3(1), dim3(NT), 0, s, rel, delta, c.T, c.H * c.W, (long long)c.B,
-                     c.levels, c.tau, budget, offset, rel_rect);
+void launch_k(const wz_config& c, const VideoArgs<BudgetArgs>& va, int V, hipStream_t s) {
+  hipLaunchKernelGGL((k_budget<NT, TV>), dim3(1, V), dim3(NT), 0, s, va, c.T, c.H * c.W, (long long)c.B, c.levels,
+                     c.tau);
 }
 
 }  // namespace
 
 hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float* frame_delta, int32_t* budget,
-                         int32_t* offset, float* rel_rect, hipStream_t s) {
-  if (c.T <= 64) launch_k<kWave, 64>(c, frame_rel, frame_delta, budget, offset, rel_rect, s);
-  else if (c.T <= 256) launch_k<256, 256>(c, frame_rel, frame_delta, budget, offset, rel_rect, s);
-  else launch_k<1024, kTMax>(c, frame_rel, frame_delta, budget, offset, rel_rect, s);
+                         int32_t* offset, float* rel_rect, hipStream_t s, const Videos& vs) {
+  VideoArgs<BudgetArgs> va{};
+  for (int v = 0; v < vs.V; ++v)
+    va.v[v] = BudgetArgs{advance(frame_rel, v * vs.ws), advance(frame_delta, v * vs.ws), advance(budget, v * vs.bud),
+                         advance(offset, v * vs.off), advance(rel_rect, v * vs.ws)};
+  if (c.T <= 64) launch_k<kWave, 64>(c, va, vs.V, s);
+  else if (c.T <= 256) launch_k<256, 256>(c, va, vs.V, s);
+  else launch_k<1024, kTMax>(c, va, vs.V, s);
   return hipGetLastError();
 }
 
