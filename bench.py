@@ -10,8 +10,10 @@ that the 256 MB Infinity Cache cannot serve a repeated frame tensor.
 
 Prints one JSON line: frames condensed per second (value), tokens/s, the
 algorithmic HBM rate of the whole call, the roofline of the dominant kernel
-(the relevance pass, timed with HIP events on its stream) and the CPU oracle's
-rate on the host as a reported baseline.
+(the relevance pass, timed with HIP events on its stream), the CPU oracle's
+rate on the host as a reported baseline, and (`batched`) the rate of
+wz_condense_batch on several videos of the same workload per call -- a
+separate throughput mode, not the headline value.
 """
 import argparse
 import hashlib
@@ -38,6 +40,8 @@ def parse():
     ap.add_argument("--out-dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle (0 disables)")
+    ap.add_argument("--videos", type=int, default=4,
+                    help="also time wz_condense_batch on this many videos of the workload per call (0 disables)")
     ap.add_argument("--copy-calib", type=int, default=0,
                     help="only run this many plain device copies of a frame tensor (the known-size kernel that "
                          "scales HBM byte counters) and exit")
@@ -176,6 +180,32 @@ def main():
     k1_bytes = relevance_bytes(wl)
     k1_gbps = k1_bytes / (k1_ms * 1e-3) / 1e9
 
+    batched = None
+    if args.videos > 1:
+        # several videos per call (wz_condense_batch): distinct copies of the input so that no video's
+        # frames are served from the Infinity Cache of another call
+        V = args.videos
+        vsets = max(2, math.ceil(2 * MALL_BYTES / (V * X0.numel() * X0.element_size())))
+        XB = [torch.stack([Xs[(i * V + v) % nsets] for v in range(V)]) for i in range(vsets)]
+        QB = [torch.stack([qs[(i * V + v) % nsets] for v in range(V)]) for i in range(vsets)]
+        wsb = torch.empty(V * ws.numel(), dtype=torch.uint8, device=dev)
+        dt = torch.float32 if out_dtype == wz.WZ_F32 else torch.bfloat16
+        outb = (torch.empty((V, p.B, p.C), dtype=dt, device=dev), torch.empty((V, p.B), dtype=torch.int32, device=dev))
+        for i in range(args.warmup):
+            wz.condense_batch(p, XB[i % vsets], QB[i % vsets], ws=wsb, out=outb)
+        torch.cuda.synchronize()
+        bsteps = max(1, args.steps // V)
+        ev0.record(stream)
+        for i in range(bsteps):
+            wz.condense_batch(p, XB[i % vsets], QB[i % vsets], ws=wsb, out=outb)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        b_ms = ev0.elapsed_time(ev1) / bsteps
+        batched = {"videos": V, "calls": bsteps, "ms_per_call": b_ms,
+                   "frames_per_s": V * wl.T / (b_ms * 1e-3),
+                   "hbm_gbps": V * algorithmic_bytes(wl, 2 if out_dtype == wz.WZ_BF16 else 4) / (b_ms * 1e-3) / 1e9}
+        del XB, QB, wsb, outb
+
     out_bytes = 2 if out_dtype == wz.WZ_BF16 else 4
     call_bytes = algorithmic_bytes(wl, out_bytes)
     frames_s = wl.T / (ms_step * 1e-3)
@@ -206,6 +236,8 @@ def main():
                      "traffic": recorded_traffic(wl.name), "bytes_per_launch": k1_bytes,
                      "us_per_launch": k1_ms * 1e3},
     }
+    if batched:
+        line["batched"] = batched
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
