@@ -330,9 +330,11 @@ constexpr uint32_t kBf16OneHi = 0x3F800000u;  // bf16 pair (0, 1)
 //   3. runs two 32-channel steps of S += X Q^T (v_mfma_f32_16x16x32_bf16) on
 //      four 16-row tiles, reading both operands from its buffers;
 //   4. re-issues the ring slot for the chunk after next.
-// The epilogue adds the waves' partial S, |x|^2 and |q_j|^2 in wave order
-// through LDS and forms a_{t,n} = max_j S_nj / (|q_j| |x_n|) and the tile's
-// sigma_j = sum_n S_nj; the tile's channel sums leave in one coalesced store.
+// In the epilogue each wave first reduces its own accumulator rows to
+// sigma_j (lane swaps); then the waves' partial S, |x|^2, |q_j|^2 and sigma_j
+// are added in wave order through LDS (two barriers), a_{t,n} = max_j S_nj /
+// (|q_j| |x_n|) is formed, and the tile's channel sums leave in one coalesced
+// store.
 constexpr int kTokWaves = 8;
 constexpr int kTokChunk = 64;      // channels per chunk (128 bytes of a bf16 row)
 constexpr int kTokRows = 64;       // tokens per tile at most (four 16-row MFMA tiles)
@@ -506,6 +508,22 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     const float v = row8_sum(qq[k]);
     if (lu == 0) s_qq[wave][8 * k + lr] = v;
   }
+  // sigma_j of the wave: its accumulator column j = 16 n + r16 summed over the
+  // wave's 64 rows (rows past the tile hold zeros), the four lane groups by
+  // lane swaps
+#pragma unroll
+  for (int n = 0; n < NTG; ++n) {
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v += Sacc[i][n][e];
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+    if (lane < 16) s_sig[wave][16 * n + r16] = v;
+  }
   // wave w's partial S sits in its own row buffer: [row][NQ] floats from &s_x[w][0][0]
   auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_x[w][0][0])[r * NQ + j]; };
 #pragma unroll
@@ -514,18 +532,26 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     for (int n = 0; n < NTG; ++n)
 #pragma unroll
       for (int e = 0; e < 4; ++e) s_part(wave, 16 * i + 4 * grp + e, 16 * n + r16) = Sacc[i][n][e];
-  lds_barrier();
-  if (tid < NQ) {
-    float v = 0.f;
+  lds_barrier();  // every sum below reads the waves' partials in wave order
+  if (tid < Q) {
+    float v = 0.f, qv = 0.f;
 #pragma unroll
-    for (int w = 0; w < kTokWaves; ++w) v += s_qq[w][tid];
-    s_rq[tid] = v > 0.f ? 1.0f / sqrtf(v) : 0.f;
-    if (tile == 0 && tid < Q) f.qg_part[size_t(t) * Q + tid] = v;
+    for (int w = 0; w < kTokWaves; ++w) {
+      v += s_sig[w][tid];
+      qv += s_qq[w][tid];
+    }
+    f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
+    if (tile == 0) f.qg_part[size_t(t) * Q + tid] = qv;
+  }
+  if (tid < NQ) {
+    float qv = 0.f;
+    for (int w = 0; w < kTokWaves; ++w) qv += s_qq[w][tid];
+    s_rq[tid] = qv > 0.f ? 1.0f / sqrtf(qv) : 0.f;
   }
   // thread -> row tid / 8, columns 4 * (tid % 8) .. + 3 (NTG = 2) or 2 * (tid % 8) .. + 1 (NTG = 1)
   constexpr int CPT = NQ / 8;
   const int row = tid >> 3, cg = (tid & 7) * CPT;
-  float sv[CPT];
+  float sv[CPT], rq[CPT];
 #pragma unroll
   for (int e = 0; e < CPT; ++e) {
     float v = 0.f;
@@ -536,35 +562,19 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   float x2 = 0.f;
 #pragma unroll
   for (int w = 0; w < kTokWaves; ++w) x2 += s_xx[w][row];
-  lds_barrier();
+  lds_barrier();  // 1 / |q_j| in s_rq
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) rq[e] = s_rq[cg + e];
   float best = -INFINITY;
 #pragma unroll
   for (int e = 0; e < CPT; ++e)
-    if (cg + e < Q) best = fmaxf(best, sv[e] * s_rq[cg + e]);
+    if (cg + e < Q) best = fmaxf(best, sv[e] * rq[e]);
   best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
   best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
   best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
   if ((tid & 7) == 0 && row < TM) {
     const float xn = sqrtf(x2);
     f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
-  }
-  // sigma_j of the tile: the wave's eight rows by lane swaps, then the waves in order
-#pragma unroll
-  for (int e = 0; e < CPT; ++e) {
-    float v = row < TM ? sv[e] : 0.f;
-    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
-    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
-    if (lane < 8) s_sig[wave][cg + e] = v;
-  }
-  lds_barrier();
-  if (tid < Q) {
-    float v = 0.f;
-#pragma unroll
-    for (int w = 0; w < kTokWaves; ++w) v += s_sig[w][tid];
-    f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
   }
   if (POOL) {
     const __amdgpu_buffer_rsrc_t pres =
