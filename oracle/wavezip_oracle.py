@@ -29,7 +29,16 @@ Points where the paper is silent or ambiguous follow these readings:
     weights are uniform;
   * the budget-guided interpolation of Eq. (17) is replaced by keeping the n_m
     tokens of largest saliency a (ties -> smaller index), emitted in raster
-    order; frames are concatenated in temporal order as in Eq. (19).
+    order; frames are concatenated in temporal order as in Eq. (19);
+  * the interpolation itself (assign="interp"), Psi of Eq. (17), whose grid
+    the paper does not give: n tokens are the first n cells, in raster order,
+    of an h' x w' grid keeping the frame's aspect ratio (h0 = the integer
+    nearest sqrt(n H / W), halves up, within [1, H]; w' = min(W, ceil(n / h0));
+    h' = ceil(n / w'), so that no grid row is empty); cell (i, j) is the
+    bilinear interpolation of the modulated map at the half-pixel centre
+    ((2i + 1) H / (2 h') - 1/2, (2j + 1) W / (2 w') - 1/2), negative
+    coordinates clamped to 0, the last row / column repeated past the edge;
+    its index is the token nearest that point (halves up).
 
 Arrays: X is [T, H, W, C] and query is [Q, C], both float64 holding the exact
 values of the (already cast) inputs.  Indices are 0-based.  parity pinned:
@@ -298,15 +307,63 @@ def wavelet_spatial_modulator(F, Mhw, lam):
 # Token Assigner: selection and concatenation (Eq. (17) replaced, Eq. (19))
 # ---------------------------------------------------------------------------
 
+def interpolation_grid(n, H, W):
+    """(h', w') of the grid that Psi of Eq. (17) samples for n tokens (reading above).
+
+    h0 is the integer nearest sqrt(n H / W) with halves rounded up, i.e. the largest
+    h >= 1 with (2h - 1)^2 W <= 4 n H, capped at H; w' = min(W, ceil(n / h0)) and
+    h' = ceil(n / w').
+    """
+    h0 = 1
+    while h0 < H and (2 * (h0 + 1) - 1) ** 2 * W <= 4 * n * H:
+        h0 += 1
+    w = min(W, -(-n // h0))
+    return -(-n // w), w
+
+
+def _sample(i, L, l):
+    """Cell i of l cells over L input samples: the half-pixel centre
+    s = (2i + 1) L / (2l) - 1/2 as exact integers (num / den), clamped at 0.
+    Returns (i0, i1, weight of i1, nearest sample)."""
+    num, den = (2 * i + 1) * L - l, 2 * l
+    if num < 0:
+        i0, frac = 0, 0.0
+    else:
+        i0, frac = num // den, (num % den) / den
+    return i0, min(i0 + 1, L - 1), frac, min(L - 1, ((2 * i + 1) * L) // (2 * l))
+
+
+def budget_guided_interpolation(Xt, n):
+    """Psi(X-tilde_m, n_m) of Eq. (17) for one modulated frame Xt [H, W, C] (reading above).
+
+    Returns (tokens [n, C], index [n]) with index = h * W + w of the nearest token.
+    """
+    H, W, C = Xt.shape
+    h, w = interpolation_grid(n, H, W)
+    out = np.zeros((n, C))
+    near = np.zeros(n, dtype=np.int64)
+    for k in range(n):
+        i, j = divmod(k, w)
+        y0, y1, fy, ny = _sample(i, H, h)
+        x0, x1, fx, nx = _sample(j, W, w)
+        top = (1.0 - fx) * Xt[y0, x0] + fx * Xt[y0, x1]
+        bottom = (1.0 - fx) * Xt[y1, x0] + fx * Xt[y1, x1]
+        out[k] = (1.0 - fy) * top + fy * bottom
+        near[k] = ny * W + nx
+    return out, near
+
+
 def select_tokens(a_t, n_t):
     """Indices of the n_t largest saliency scores (ties -> smaller index), ascending."""
     order = np.lexsort((np.arange(len(a_t)), -np.asarray(a_t)))
     return np.sort(order[:n_t])
 
 
-def condense(X, query, B, levels=1, lam=1.5, tau=0.0):
+def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select"):
     """The whole pass C(X, Q) of Eq. (4)/(6); returns every intermediate.
 
+    assign: "select" keeps each frame's n_t most salient modulated tokens,
+    "interp" interpolates the modulated frame to n_t tokens (Psi of Eq. (17)).
     Keys: a [T,N], vbar [T,C], r [T], delta [T], gamma [T], retained (list),
     r_tilde [L], budget [T] (0 for dropped frames), offset [T+1], M [T,N],
     tokens [offset[T], C], index [offset[T]] (flat t*N + h*W + w).
@@ -332,10 +389,15 @@ def condense(X, query, B, levels=1, lam=1.5, tau=0.0):
     for t in range(T):
         if budget[t] == 0:
             continue
-        sel = select_tokens(a[t], int(budget[t]))
         Xt = wavelet_spatial_modulator(X[t], M[t].reshape(H, W), lam)
-        tokens[offset[t]:offset[t + 1]] = Xt.reshape(N, C)[sel]
-        index[offset[t]:offset[t + 1]] = t * N + sel
+        if assign == "interp":
+            tok_t, near = budget_guided_interpolation(Xt, int(budget[t]))
+            tokens[offset[t]:offset[t + 1]] = tok_t
+            index[offset[t]:offset[t + 1]] = t * N + near
+        else:
+            sel = select_tokens(a[t], int(budget[t]))
+            tokens[offset[t]:offset[t + 1]] = Xt.reshape(N, C)[sel]
+            index[offset[t]:offset[t + 1]] = t * N + sel
     return dict(a=a, vbar=vbar, r=r, delta=delta, gamma=gamma, retained=kept_frames,
                 r_tilde=r_tilde, budget=budget, offset=offset, M=M,
                 tokens=tokens, index=index)

@@ -340,4 +340,34 @@ def pin_end_to_end_brute(cases=40, seed=61):
         assert np.allclose(o["r_tilde"], b["r_tilde"], atol=1e-12)
 
 
+def pin_interp_identity_and_grid():
+    """Psi at n = H*W is the identity; the grid keeps every row occupied and the aspect ratio."""
+    for H, W in ((14, 14), (3, 5), (7, 1), (13, 13)):
+        rng = np.random.default_rng(H * 31 + W)
+        X = rng.standard_normal((H, W, 2))
+        out, near = oracle.budget_guided_interpolation(X, H * W)
+        assert np.array_equal(out, X.reshape(H * W, 2)) and np.array_equal(near, np.arange(H * W))
+        for n in range(1, H * W + 1):
+            h, w = oracle.interpolation_grid(n, H, W)
+            h0 = min(H, max(1, int(np.floor(np.sqrt(n * H / W) + 0.5))))
+            assert w == min(W, -(-n // h0)) and h * w >= n > (h - 1) * w
+
+
+def pin_interp_affine_exact():
+    """Bilinear interpolation at half-pixel centres reproduces an affine map exactly
+    (coordinates clamped at 0); the index is the nearest token, halves up."""
+    H, W = 13, 11
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    X = (0.75 * yy - 1.25 * xx + 0.5)[:, :, None]
+    for n in (1, 2, 5, 17, 40, 100, 142):
+        out, near = oracle.budget_guided_interpolation(X, n)
+        h, w = oracle.interpolation_grid(n, H, W)
+        for k in range(n):
+            i, j = divmod(k, w)
+            sy, sx = max(0.0, (i + 0.5) * H / h - 0.5), max(0.0, (j + 0.5) * W / w - 0.5)
+            assert abs(out[k, 0] - (0.75 * sy - 1.25 * sx + 0.5)) < 1e-12
+            ny, nx = min(H - 1, math.floor((i + 0.5) * H / h)), min(W - 1, math.floor((j + 0.5) * W / w))
+            assert near[k] == ny * W + nx
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

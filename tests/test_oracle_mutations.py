@@ -119,6 +119,19 @@ def _filter_drops_first(delta, tau):
     return [t for t in range(len(delta)) if delta[t] >= tau and (t > 0 or tau <= 0)] or [0]
 
 
+def _sample_corners(i, L, l):
+    # align-corners sampling instead of half-pixel centres
+    s = i * (L - 1) / (l - 1) if l > 1 else 0.0
+    i0 = int(np.floor(s))
+    return i0, min(i0 + 1, L - 1), s - i0, min(L - 1, int(np.floor(s + 0.5)))
+
+
+def _grid_swap(n, H, Wd):
+    # rows and columns of the grid exchanged
+    w, h = W._orig["interpolation_grid"](n, Wd, H)
+    return min(h, H), min(w, Wd)
+
+
 MUTATIONS = {
     "haar_detail_sign": ("haar_analysis", _analysis_detail_sign),
     "haar_synthesis_swapped": ("haar_synthesis", _synthesis_swapped),
@@ -137,13 +150,16 @@ MUTATIONS = {
     "select_smallest": ("select_tokens", _select_ascending),
     "minmax_degenerate_ones": ("min_max", _minmax_degenerate_ones),
     "filter_drops_frame0": ("retained_frames", _filter_drops_first),
+    "interp_align_corners": ("_sample", _sample_corners),
+    "interp_grid_transposed": ("interpolation_grid", _grid_swap),
 }
 
 
 @pytest.fixture(autouse=True)
 def _originals():
     W._orig = {name: getattr(W, name) for name, _ in
-               [(n, None) for n in ("haar_analysis", "haar_synthesis", "allocate_budget_trace", "haar_analysis_2d")]}
+               [(n, None) for n in ("haar_analysis", "haar_synthesis", "allocate_budget_trace", "haar_analysis_2d",
+                                    "interpolation_grid")]}
     yield
     del W._orig
 
