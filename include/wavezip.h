@@ -68,10 +68,25 @@ typedef enum {
 
 typedef enum { WZ_F32 = 0, WZ_BF16 = 1 } wz_dtype;
 
+/* How a frame's n_t output tokens are formed from its modulated map
+ * (Token Assigner, Eq. (17)).                                                 */
+typedef enum {
+  WZ_SELECT = 0,  /* the n_t tokens of largest score, in raster order (default) */
+  WZ_INTERP = 1   /* budget-guided bilinear interpolation Psi: the first n_t
+                     cells, in raster order, of an h' x w' grid keeping the
+                     frame's aspect ratio (h0 = the integer nearest
+                     sqrt(n_t H / W), halves up, within [1, H]; w' = min(W,
+                     ceil(n_t / h0)); h' = ceil(n_t / w')), cell (i, j) the
+                     bilinear interpolation at the half-pixel centre
+                     ((2i+1) H / (2h') - 1/2, (2j+1) W / (2w') - 1/2) with
+                     negative coordinates clamped to 0; out_index holds the
+                     token nearest that point (halves up)                    */
+} wz_assign;
+
 /* Problem description.  Supported ranges (anything else is WZ_ERR_SHAPE /
  * WZ_ERR_PARAM): 1 <= T <= 2048; 1 <= H, W and H*W <= 4096; 1 <= Q <= 1024;
  * 8 <= C <= 65536 with C % 8 == 0; 1 <= levels <= 16; lambda_ finite and
- * >= 0; tau in [0, 2].                                                        */
+ * >= 0; tau in [0, 2]; assign a wz_assign value.                             */
 typedef struct {
   int32_t T, H, W, C, Q;
   int32_t in_dtype;   /* wz_dtype of X and query                               */
@@ -80,6 +95,8 @@ typedef struct {
   int64_t B;          /* global token budget, 0 <= B <= T*H*W                  */
   float lambda_;      /* WSM modulation strength (the paper's default: 1.5)    */
   float tau;          /* frame-filter threshold on delta; 0 keeps every frame  */
+  int32_t assign;     /* wz_assign (0, the zero-initialised default: selection) */
+  int32_t reserved;   /* must be 0                                             */
 } wz_config;
 
 /* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`

@@ -19,7 +19,8 @@ wz_status check_config(const wz_config* c) {
       c->Q > 1024 || c->C < 8 || c->C > 65536 || c->C % 8 != 0)
     return WZ_ERR_SHAPE;
   if (c->levels < 1 || c->levels > 16 || !std::isfinite(c->lambda_) || c->lambda_ < 0.f ||
-      !std::isfinite(c->tau) || c->tau < 0.f || c->tau > 2.f)
+      !std::isfinite(c->tau) || c->tau < 0.f || c->tau > 2.f || (c->assign != WZ_SELECT && c->assign != WZ_INTERP) ||
+      c->reserved != 0)
     return WZ_ERR_PARAM;
   if (c->B < 0 || c->B > int64_t(c->T) * c->H * c->W) return WZ_ERR_BUDGET;
   return WZ_OK;

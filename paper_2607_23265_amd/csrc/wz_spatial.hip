@@ -116,7 +116,7 @@ __device__ __forceinline__ void store_row<uint16_t, 4>(__amdgpu_buffer_rsrc_t r,
   buf_store_wt_b64(lo | (hi << 32), r, off);
 }
 
-template <typename In, typename Out, int U, int MODE>
+template <typename In, typename Out, int U, int MODE, bool INTERP>
 __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<AssignArgs> va) {
   const AssignArgs& f = va.v[blockIdx.y];
   constexpr int V = Vec16<In>::kV;
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
   // budget is known.
   // ranks below kp are read ahead (before the budget), each by its frame's
   // workgroup p = rank mod P, one item per reading wave
-  const int kp = given ? min(min(f.kpre, N), f.P * (GW / parts)) : 0;
+  const int kp = given && !INTERP ? min(min(f.kpre, N), f.P * (GW / parts)) : 0;
   const int npre = kp > p ? (kp - p + f.P - 1) / f.P * parts : 0;
   // the four rows of token n's 2x2 block, the token's own row first: the
   // block's other row h2 and column w2 (the last row / column repeated when
@@ -334,9 +334,79 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
   const int mine = nt > p ? (nt - p + f.P - 1) / f.P : 0;  // kept tokens of this workgroup
   const int nitems = mine * parts;
 
+  // Output cell k of frame te under the budget-guided interpolation (Psi of
+  // Eq. (17)): the grid, sample point and taps in exact integer arithmetic,
+  // each tap the modulated token mu + g (x - mu) of its own 2x2 block, the
+  // four blended as (1 - fy) ((1 - fx) A + fx B) + fy ((1 - fx) C + fx D).
+  auto interp_item = [&](int te, int nte, int k, int part, long long row, bool own) {
+    long long h0 = 1;  // the integer nearest sqrt(n H / W), halves up, within [1, H]
+    while (h0 < f.H && (2 * h0 + 1) * (2 * h0 + 1) * f.W <= 4LL * nte * f.H) ++h0;
+    const int gw = min(f.W, int((nte + h0 - 1) / h0)), gh = (nte + gw - 1) / gw;
+    const int ci = k / gw, cj = k - ci * gw;
+    auto axis = [](int i, int L, int l, int& i0, int& i1, float& fr, int& nearest) {
+      const int num = (2 * i + 1) * L - l, den = 2 * l;
+      i0 = num < 0 ? 0 : num / den;
+      fr = num < 0 ? 0.f : float(num - i0 * den) / float(den);
+      i1 = min(i0 + 1, L - 1);
+      nearest = min(L - 1, ((2 * i + 1) * L) / den);
+    };
+    int y0, y1, ny, x0, x1, nx;
+    float fy, fx;
+    axis(ci, f.H, gh, y0, y1, fy, ny);
+    axis(cj, f.W, gw, x0, x1, fx, nx);
+    const int tap[4] = {y0 * f.W + x0, y0 * f.W + x1, y1 * f.W + x0, y1 * f.W + x1};
+    const size_t fo = size_t(te) * N;
+    const __amdgpu_buffer_rsrc_t xr = own ? xres : make_rsrc(static_cast<const In*>(f.X) + fo * f.C, uint32_t(N) * rb);
+    u32x4 xt[4][U][4];
+    float g[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      load_rows(xr, part, tap[q], xt[q]);
+      g[q] = own ? rl.gate[tap[q]] : f.gate[fo + tap[q]];
+    }
+    float a[U][V], b[U][V], c[U][V], d[U][V], y[U][V];
+    modulate(xt[0], g[0], a);
+    modulate(xt[1], g[1], b);
+    modulate(xt[2], g[2], c);
+    modulate(xt[3], g[3], d);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const float top = (1.f - fx) * a[u][e] + fx * b[u][e];
+        const float bottom = (1.f - fx) * c[u][e] + fx * d[u][e];
+        y[u][e] = (1.f - fy) * top + fy * bottom;
+      }
+    store_rows(part, te, ny * f.W + nx, row, y);
+  };
+
   // ---- B. the rows: the read-ahead one (if its token is kept), then the
   // rest, the next item's block reads in flight while one is finished ----
   auto item_token = [&](int j) { return rl.byrank[p + f.P * (j / parts)]; };
+  if constexpr (INTERP) {
+    if (MODE == kOffsets || !given) {
+      // this workgroup's cells k = p, p + P, ... of its own frame
+      for (int j = wave; j < nitems; j += kNW) {
+        const int k = p + f.P * (j / parts);
+        if (base + k >= 0 && base + k < total) interp_item(t, nt, k, j % parts, base + k, true);
+      }
+    } else {
+      // every frame's cells shared out evenly over all T * P workgroups
+      const long long items = (long long)s_off[T] * parts, groups = (long long)T * f.P, g = (long long)t * f.P + p;
+      const long long i1 = (g + 1) * items / groups;
+      for (long long i = g * items / groups + wave; i < i1; i += kNW) {
+        const long long e = i / parts;
+        int lo = 0, hi = T;  // s_off[lo] <= e < s_off[hi]
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (s_off[mid] <= e) lo = mid;
+          else hi = mid;
+        }
+        interp_item(lo, s_off[lo + 1] - s_off[lo], int(e - s_off[lo]), int(i - e * parts), e, lo == t);
+      }
+    }
+    return;
+  }
   if (ahead && jp < nitems) {
     const long long k = base + position(np, nt);
     if (k >= 0 && k < total) store_item(jp, np, k, yp);
@@ -422,9 +492,11 @@ void launch_typed(const wz_config& c, const VideoArgs<AssignArgs>& a, int V, hip
   const int nvec = c.C / Vec16<In>::kV;
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * a.v[0].P), V), block(kThreads);
   const size_t lds = size_t(c.H) * c.W * 24;  // key 8 B; rank, byrank, gate, order / position 4 B
-  // one batch of loads per part: two vectors per lane, or one for short rows
-  if (nvec <= kWave) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE>), grid, block, lds, s, a);
-  else hipLaunchKernelGGL((k_assign_gather<In, Out, kVecPerLane, MODE>), grid, block, lds, s, a);
+  // one batch of loads per part: two vectors per lane, or one for short rows;
+  // the interpolation reads four blocks at once, one vector per lane each
+  if (c.assign == WZ_INTERP) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, true>), grid, block, lds, s, a);
+  else if (nvec <= kWave) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, false>), grid, block, lds, s, a);
+  else hipLaunchKernelGGL((k_assign_gather<In, Out, kVecPerLane, MODE, false>), grid, block, lds, s, a);
 }
 
 template <int MODE>

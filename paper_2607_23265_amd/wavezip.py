@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libwavezip.so")
 
 WZ_F32, WZ_BF16 = 0, 1
+WZ_SELECT, WZ_INTERP = 0, 1
 _STATUS = {0: "WZ_OK", 1: "WZ_ERR_NULL", 2: "WZ_ERR_ALIGN", 3: "WZ_ERR_SHAPE", 4: "WZ_ERR_DTYPE",
            5: "WZ_ERR_PARAM", 6: "WZ_ERR_BUDGET", 7: "WZ_ERR_WORKSPACE", 8: "WZ_ERR_DEVICE"}
 EXPORTS = ("wz_workspace_bytes", "wz_relevance", "wz_relevance_pass", "wz_temporal_budget",
@@ -33,7 +34,8 @@ class Config(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32),
                 ("C", ctypes.c_int32), ("Q", ctypes.c_int32), ("in_dtype", ctypes.c_int32),
                 ("out_dtype", ctypes.c_int32), ("levels", ctypes.c_int32), ("B", ctypes.c_int64),
-                ("lambda_", ctypes.c_float), ("tau", ctypes.c_float)]
+                ("lambda_", ctypes.c_float), ("tau", ctypes.c_float), ("assign", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 _lib = None
@@ -79,10 +81,11 @@ class Problem:
     levels: int = 1
     lam: float = 1.5
     tau: float = 0.0
+    assign: int = 0  # WZ_SELECT; WZ_INTERP for the budget-guided interpolation
 
     def config(self):
         return Config(self.T, self.H, self.W, self.C, self.Q, self.in_dtype, self.out_dtype, self.levels,
-                      self.B, self.lam, self.tau)
+                      self.B, self.lam, self.tau, self.assign, 0)
 
     @property
     def N(self):
@@ -218,8 +221,8 @@ def to_device(inp, device="cuda:0"):
     return X.contiguous(), q.contiguous()
 
 
-def problem_of(wl, out_dtype=WZ_F32):
+def problem_of(wl, out_dtype=WZ_F32, assign=0):
     """Problem description of a workload (paper_2607_23265_amd.synth.Workload)."""
     return Problem(T=wl.T, H=wl.H, W=wl.W, C=wl.C, Q=wl.Q, B=wl.B,
                    in_dtype=WZ_BF16 if wl.dtype == "bf16" else WZ_F32, out_dtype=out_dtype,
-                   levels=wl.levels, lam=wl.lam, tau=wl.tau)
+                   levels=wl.levels, lam=wl.lam, tau=wl.tau, assign=assign)
