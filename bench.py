@@ -11,9 +11,10 @@ that the 256 MB Infinity Cache cannot serve a repeated frame tensor.
 Prints one JSON line: frames condensed per second (value), tokens/s, the
 algorithmic HBM rate of the whole call, the roofline of the dominant kernel
 (the relevance pass, timed with HIP events on its stream), the CPU oracle's
-rate on the host as a reported baseline, and (`batched`) the rate of
-wz_condense_batch on several videos of the same workload per call -- a
-separate throughput mode, not the headline value.
+rate on the host as a reported baseline, (`interp`) the rate with the
+budget-guided interpolation forming the tokens instead of selection, and
+(`batched`) the rate of wz_condense_batch on several videos of the same
+workload per call -- separate modes, not the headline value.
 """
 import argparse
 import hashlib
@@ -206,6 +207,19 @@ def main():
                    "hbm_gbps": V * algorithmic_bytes(wl, 2 if out_dtype == wz.WZ_BF16 else 4) / (b_ms * 1e-3) / 1e9}
         del XB, QB, wsb, outb
 
+    # the same pass with the budget-guided interpolation forming the tokens (cfg.assign = WZ_INTERP)
+    pi = wz.problem_of(wl, out_dtype, assign=wz.WZ_INTERP)
+    for i in range(args.warmup):
+        wz.condense(pi, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        wz.condense(pi, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    i_ms = ev0.elapsed_time(ev1) / args.steps
+    interp = {"ms_per_step": i_ms, "frames_per_s": wl.T / (i_ms * 1e-3)}
+
     out_bytes = 2 if out_dtype == wz.WZ_BF16 else 4
     call_bytes = algorithmic_bytes(wl, out_bytes)
     frames_s = wl.T / (ms_step * 1e-3)
@@ -236,6 +250,7 @@ def main():
                      "traffic": recorded_traffic(wl.name), "bytes_per_launch": k1_bytes,
                      "us_per_launch": k1_ms * 1e3},
     }
+    line["interp"] = interp
     if batched:
         line["batched"] = batched
     if args.cpu_seconds > 0:
