@@ -86,7 +86,8 @@ typedef enum {
 /* Problem description.  Supported ranges (anything else is WZ_ERR_SHAPE /
  * WZ_ERR_PARAM): 1 <= T <= 2048; 1 <= H, W and H*W <= 4096; 1 <= Q <= 1024;
  * 8 <= C <= 65536 with C % 8 == 0; 1 <= levels <= 16; lambda_ finite and
- * >= 0; tau in [0, 2]; assign a wz_assign value.                             */
+ * >= 0; tau in [0, 2]; assign a wz_assign value; spatial_levels 0, 1 or 2
+ * (2 only with WZ_SELECT).                                                    */
 typedef struct {
   int32_t T, H, W, C, Q;
   int32_t in_dtype;   /* wz_dtype of X and query                               */
@@ -96,7 +97,11 @@ typedef struct {
   float lambda_;      /* WSM modulation strength (the paper's default: 1.5)    */
   float tau;          /* frame-filter threshold on delta; 0 keeps every frame  */
   int32_t assign;     /* wz_assign (0, the zero-initialised default: selection) */
-  int32_t reserved;   /* must be 0                                             */
+  int32_t spatial_levels; /* levels of the spatial Haar modulator: 0 or 1 for
+                         the single level of Eq. (12)-(15) (default), 2 for two
+                         levels -- the approximation decomposed once more, level
+                         2's details gated by lambda times M pooled twice (the
+                         multi-level variant of the ablations); selection only */
 } wz_config;
 
 /* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`

@@ -22,7 +22,9 @@ Points where the paper is silent or ambiguous follow these readings:
   * odd-length signals are extended by repeating the last sample before every
     Haar step (half-point symmetric extension), and cropped after synthesis;
   * the orthonormal Haar filters are used in 1-D and, separably, in 2-D; the
-    2-D transform is the single-level Haar version of Eq. (12)-(15);
+    2-D transform is the single-level Haar version of Eq. (12)-(15); the
+    multi-level variant (spatial_levels > 1) gates level j's details by the
+    saliency map pooled j times;
   * Eq. (16)'s Round is realised as a capped largest-remainder (Hamilton)
     apportionment so that Eq. (5) (budgets sum to B) holds with 0 <= n <= N;
     remainder ties go to the smaller frame index; if every weight is zero the
@@ -289,18 +291,30 @@ def block_average(Mhw):
     return 0.25 * (Me[0::2, 0::2] + Me[0::2, 1::2] + Me[1::2, 0::2] + Me[1::2, 1::2])
 
 
-def wavelet_spatial_modulator(F, Mhw, lam):
+def wavelet_spatial_modulator(F, Mhw, lam, levels=1):
     """X-tilde_m for one frame F [H, W, C] with saliency map Mhw [H, W].
 
     G_m = lam * P(M_m) (Eq. (13)); the three detail subbands are multiplied by G_m
     (Eq. (14)) and the frame is rebuilt by the inverse transform (Eq. (15)); the
-    approximation LL is left unchanged.
+    approximation LL is left unchanged.  With levels = J > 1 (the multi-level
+    variant of the ablation space) the approximation is decomposed again J - 1
+    times; level j's details are gated by lam times M pooled j times (odd sizes
+    repeat the last row / column at every level) and the levels are rebuilt from
+    the coarsest.
     """
     H, W = Mhw.shape
-    LL, LH, HL, HH = haar_analysis_2d(F)
-    G = lam * block_average(Mhw)
-    G = G[:, :, None]
-    return haar_synthesis_2d(LL, G * LH, G * HL, G * HH, H, W)
+    LL = np.asarray(F, dtype=np.float64)
+    M = np.asarray(Mhw, dtype=np.float64)
+    shapes, gated = [], []
+    for _ in range(levels):
+        shapes.append(LL.shape[:2])
+        LL, LH, HL, HH = haar_analysis_2d(LL)
+        M = block_average(M)
+        G = (lam * M)[:, :, None]
+        gated.append((G * LH, G * HL, G * HH))
+    for (h, w), (LH, HL, HH) in zip(reversed(shapes), reversed(gated)):
+        LL = haar_synthesis_2d(LL, LH, HL, HH, h, w)
+    return LL
 
 
 # ---------------------------------------------------------------------------
@@ -359,11 +373,12 @@ def select_tokens(a_t, n_t):
     return np.sort(order[:n_t])
 
 
-def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select"):
+def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select", spatial_levels=1):
     """The whole pass C(X, Q) of Eq. (4)/(6); returns every intermediate.
 
     assign: "select" keeps each frame's n_t most salient modulated tokens,
     "interp" interpolates the modulated frame to n_t tokens (Psi of Eq. (17)).
+    spatial_levels: levels of the spatial Haar modulator (1 as in Eq. (12)-(15)).
     Keys: a [T,N], vbar [T,C], r [T], delta [T], gamma [T], retained (list),
     r_tilde [L], budget [T] (0 for dropped frames), offset [T+1], M [T,N],
     tokens [offset[T], C], index [offset[T]] (flat t*N + h*W + w).
@@ -389,7 +404,7 @@ def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select"):
     for t in range(T):
         if budget[t] == 0:
             continue
-        Xt = wavelet_spatial_modulator(X[t], M[t].reshape(H, W), lam)
+        Xt = wavelet_spatial_modulator(X[t], M[t].reshape(H, W), lam, spatial_levels)
         if assign == "interp":
             tok_t, near = budget_guided_interpolation(Xt, int(budget[t]))
             tokens[offset[t]:offset[t + 1]] = tok_t

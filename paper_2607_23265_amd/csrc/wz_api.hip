@@ -20,7 +20,7 @@ wz_status check_config(const wz_config* c) {
     return WZ_ERR_SHAPE;
   if (c->levels < 1 || c->levels > 16 || !std::isfinite(c->lambda_) || c->lambda_ < 0.f ||
       !std::isfinite(c->tau) || c->tau < 0.f || c->tau > 2.f || (c->assign != WZ_SELECT && c->assign != WZ_INTERP) ||
-      c->reserved != 0)
+      c->spatial_levels < 0 || c->spatial_levels > 2 || (c->spatial_levels == 2 && c->assign != WZ_SELECT))
     return WZ_ERR_PARAM;
   if (c->B < 0 || c->B > int64_t(c->T) * c->H * c->W) return WZ_ERR_BUDGET;
   return WZ_OK;

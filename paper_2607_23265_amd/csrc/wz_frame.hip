@@ -38,6 +38,7 @@ struct FrameArgs {
   int32_t* rank;           // [T][N]  out (order role)
   int32_t* byrank;         // [T][N]
   float* gate;             // [T][N]
+  float* gate2;            // [T][N] level-2 gates, or null (one spatial level)
   int T, N, H, W, C, Q, QP, tiles, slices;
   int order;               // the order role runs
   int roles;               // workgroups per frame: 1 + (scores or order role)
@@ -63,6 +64,7 @@ __device__ void scores_role(const FrameArgs& f, int t) {
   rl.byrank = rl.rank + N;
   rl.gate = reinterpret_cast<float*>(rl.byrank + N);
   rl.order = reinterpret_cast<int32_t*>(rl.gate + N);
+  rl.gate2 = f.gate2 ? reinterpret_cast<float*>(rl.order + N) : nullptr;
   rl.start = s_start;
   rl.fill = s_fill;
   rl.mm = s_mm;
@@ -186,6 +188,7 @@ __device__ void scores_role(const FrameArgs& f, int t) {
     f.rank[size_t(t) * N + n] = rl.rank[n];
     f.byrank[size_t(t) * N + n] = rl.byrank[n];
     f.gate[size_t(t) * N + n] = rl.gate[n];
+    if (f.gate2) f.gate2[size_t(t) * N + n] = rl.gate2[n];
   }
 }
 
@@ -318,13 +321,14 @@ hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_scor
     va.v[v] = FrameArgs{w.s_part,   w.g_part,  w.qg_part,
                         w.sig_part, w.pool_part, advance(tok_score, v * vs.ws),
                         advance(frame_rel, v * vs.ws), advance(frame_delta, v * vs.ws), w.rank,
-                        w.byrank,   w.gate,    c.T,
+                        w.byrank,   w.gate,    c.spatial_levels == 2 && order ? w.gate2 : nullptr, c.T,
                         N,          c.H,       c.W,
                         c.C,        c.Q,       qpad(c.Q),
                         pl.tiles,   pl.slices, order ? 1 : 0,
                         roles,      c.lambda_};
   }
-  const size_t lds = roles == 2 ? size_t(N) * 24 : 0;  // key 8 B; rank, byrank, gate, bin order 4 B
+  // key 8 B; rank, byrank, gate, bin order (and level-2 gate) 4 B
+  const size_t lds = roles == 2 ? size_t(N) * (c.spatial_levels == 2 ? 28 : 24) : 0;
   const dim3 grid((c.T + kXcds - 1) / kXcds * kXcds * roles, vs.V);
   if (pl.slices > 1) hipLaunchKernelGGL((k_frame<kPartThreads>), grid, dim3(kPartThreads), lds, s, va);
   else hipLaunchKernelGGL((k_frame<kThreads>), grid, dim3(kThreads), lds, s, va);

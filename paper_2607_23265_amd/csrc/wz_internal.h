@@ -145,6 +145,7 @@ struct Workspace {
   int32_t* rank;       // [T*N]                   selection rank of each token in its frame
   int32_t* byrank;     // [T*N]                   token of each rank
   float* gate;         // [T*N]                   saliency gate of each token's 2x2 block
+  float* gate2;        // [T*N]                   level-2 gate of each token (two spatial levels)
   float* frame_rel;    // [T]
   float* frame_delta;  // [T]
   int32_t* budget;     // [T]
@@ -170,6 +171,7 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   w.rank = reinterpret_cast<int32_t*>(take(T * N * 4));
   w.byrank = reinterpret_cast<int32_t*>(take(T * N * 4));
   w.gate = reinterpret_cast<float*>(take(T * N * 4));
+  w.gate2 = reinterpret_cast<float*>(take(c.spatial_levels == 2 ? T * N * 4 : 0));
   w.frame_rel = reinterpret_cast<float*>(take(T * 4));
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
   w.budget = reinterpret_cast<int32_t*>(take(T * 4));
@@ -207,6 +209,7 @@ inline Workspace advance(const Workspace& w, long long bytes) {
   o.rank = advance(w.rank, bytes);
   o.byrank = advance(w.byrank, bytes);
   o.gate = advance(w.gate, bytes);
+  o.gate2 = advance(w.gate2, bytes);
   o.frame_rel = advance(w.frame_rel, bytes);
   o.frame_delta = advance(w.frame_delta, bytes);
   o.budget = advance(w.budget, bytes);

@@ -6,7 +6,10 @@
 //   rank_n = number of keys larger than key_n (byrank inverts it);
 //   gate_n = lambda * mean of M over the 2x2 block of token n (Eq. (13)),
 //            M = min-max of the frame's scores (Eq. (7)), 0 when all equal;
-//            the last row / column is repeated when H or W is odd.
+//            the last row / column is repeated when H or W is odd;
+//   gate2_n (two spatial levels) = lambda * mean of those block means over
+//            the 2x2 blocks of blocks around token n, repeated at the edge
+//            likewise.
 // Ranks come from a counting sort into score bins (linear in the score
 // between the frame's extremes, so a larger key never lands in a lower bin)
 // and a comparison of the keys that share a bin.
@@ -24,6 +27,7 @@ struct RankLds {  // LDS arrays of the frame
   int32_t* rank;    // [N]
   int32_t* byrank;  // [N]
   float* gate;      // [N]
+  float* gate2;     // [N] level-2 gates (two spatial levels), or null
   int32_t* order;   // [N] scratch: tokens in bin order
   int* start;       // [kBins] first position of each bin, bins from the top
   int* fill;        // [kBins]
@@ -106,6 +110,21 @@ __device__ void rank_frame(int N, int H, int W, float lam, float lo, float hi, c
     const int i1 = min(i0 + 1, H - 1), j1 = min(j0 + 1, W - 1);
     const float m00 = sal(i0 * W + j0), m01 = sal(i0 * W + j1), m10 = sal(i1 * W + j0), m11 = sal(i1 * W + j1);
     s.gate[n] = lam * (0.25f * (((m00 + m01) + m10) + m11));
+  }
+  if (s.gate2) {
+    // two spatial levels: lambda * the mean of M over the level-1 cells (2x2
+    // token blocks) of the token's level-2 block, the last cell / token row
+    // and column repeated at each level
+    const int Hb = (H + 1) / 2, Wb = (W + 1) / 2;
+    auto cell = [&](int bi, int bj) {
+      const int i0 = 2 * bi, j0 = 2 * bj, i1 = min(i0 + 1, H - 1), j1 = min(j0 + 1, W - 1);
+      return 0.25f * (((sal(i0 * W + j0) + sal(i0 * W + j1)) + sal(i1 * W + j0)) + sal(i1 * W + j1));
+    };
+    for (int n = tid; n < N; n += NTH) {
+      const int h = n / W, w = n - h * W;
+      const int c0 = 2 * (h / 4), d0 = 2 * (w / 4), c1 = min(c0 + 1, Hb - 1), d1 = min(d0 + 1, Wb - 1);
+      s.gate2[n] = lam * (0.25f * (((cell(c0, d0) + cell(c0, d1)) + cell(c1, d0)) + cell(c1, d1)));
+    }
   }
 }
 

@@ -53,6 +53,7 @@ struct AssignArgs {
   const int32_t* rank;      // [T][H*W] or null: selection ranks from the per-frame kernel
   const int32_t* byrank;    // [T][H*W]
   const float* gate;        // [T][H*W]
+  const float* gate2;       // [T][H*W] level-2 gates (two spatial levels, with the per-frame kernel)
   int32_t* budget_out;      // [T] or null    (budget modes; written by workgroup (0, 0))
   int32_t* offset_out;      // [T+1] or null  (budget modes)
   void* out_tokens;         // [B][C]
@@ -116,8 +117,13 @@ __device__ __forceinline__ void store_row<uint16_t, 4>(__amdgpu_buffer_rsrc_t r,
   buf_store_wt_b64(lo | (hi << 32), r, off);
 }
 
-template <typename In, typename Out, int U, int MODE, bool INTERP>
+// AM: how the rows are formed -- kSelect1 (selection, one spatial level),
+// kInterp (budget-guided interpolation), kSelect2 (selection, two levels).
+enum AssignMode : int { kSelect1 = 0, kInterp = 1, kSelect2 = 2 };
+
+template <typename In, typename Out, int U, int MODE, int AM>
 __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<AssignArgs> va) {
+  constexpr bool INTERP = AM == kInterp, L2 = AM == kSelect2;
   const AssignArgs& f = va.v[blockIdx.y];
   constexpr int V = Vec16<In>::kV;
   // waves that read ranks and blocks while wave 0 computes the budgets
@@ -140,6 +146,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
   rl.byrank = rl.rank + N;
   rl.gate = reinterpret_cast<float*>(rl.byrank + N);
   rl.order = reinterpret_cast<int32_t*>(rl.gate + N);
+  rl.gate2 = L2 ? reinterpret_cast<float*>(rl.order + N) : nullptr;
   rl.start = s_start;
   rl.fill = s_fill;
   rl.mm = s_mm;
@@ -158,7 +165,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
   // budget is known.
   // ranks below kp are read ahead (before the budget), each by its frame's
   // workgroup p = rank mod P, one item per reading wave
-  const int kp = given && !INTERP ? min(min(f.kpre, N), f.P * (GW / parts)) : 0;
+  const int kp = given && AM == kSelect1 ? min(min(f.kpre, N), f.P * (GW / parts)) : 0;
   const int npre = kp > p ? (kp - p + f.P - 1) / f.P * parts : 0;
   // the four rows of token n's 2x2 block, the token's own row first: the
   // block's other row h2 and column w2 (the last row / column repeated when
@@ -225,6 +232,43 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
     }
     return before;
   };
+  // Two spatial levels: the 16 rows of the four level-1 cells (2x2 token
+  // blocks) of token n's level-2 block, the token's own cell first with its
+  // own row first (the last row / column repeated at each level), then
+  //   x~ = mu2 + g2 (mu1 - mu2) + g1 (x - mu1),
+  // mu1 the mean of the token's cell, mu2 the mean of the four cell means:
+  // what the two-level butterflies with gated details come to.
+  auto load_rows2 = [&](__amdgpu_buffer_rsrc_t xr, int part, int n, u32x4 (&x)[4][U][4]) {
+    const int Hb = (f.H + 1) / 2, Wb = (f.W + 1) / 2;
+    const int h = n / f.W, w = n - h * f.W, bi = h / 2, bj = w / 2;
+    const int bi2 = (bi & 1) ? bi - 1 : min(bi + 1, Hb - 1), bj2 = (bj & 1) ? bj - 1 : min(bj + 1, Wb - 1);
+    load_rows(xr, part, n, x[0]);
+    const int cells[3][2] = {{bi, bj2}, {bi2, bj}, {bi2, bj2}};
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      const int ci = cells[q][0], cj = cells[q][1];
+      load_rows(xr, part, (2 * ci) * f.W + 2 * cj, x[q + 1]);  // the cell's four tokens
+    }
+  };
+  auto modulate2 = [&](const u32x4 (&x)[4][U][4], float g1, float g2, float (&y)[U][V]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float r[4][4][V];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) Vec16<In>::widen(x[q][u][k], r[q][k]);
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        float m[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) m[q] = 0.25f * (((r[q][0][e] + r[q][1][e]) + r[q][2][e]) + r[q][3][e]);
+        const float mu2 = 0.25f * (((m[0] + m[1]) + m[2]) + m[3]);
+        y[u][e] = mu2 + g2 * (m[0] - mu2) + g1 * (r[0][0][e] - m[0]);
+      }
+    }
+  };
+
   // row k of the output: channel part `part` of token n of frame tf
   auto store_rows = [&](int part, int tf, int n, long long k, const float (&y)[U][V]) {
     const __amdgpu_buffer_rsrc_t ores =
@@ -278,6 +322,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
         rl.rank[n] = f.rank[size_t(t) * N + n];
         rl.byrank[n] = f.byrank[size_t(t) * N + n];
         rl.gate[n] = f.gate[size_t(t) * N + n];
+        if (L2) rl.gate2[n] = f.gate2[size_t(t) * N + n];
       }
       if (ahead) modulate(xp, gp, yp);
     } else {
@@ -411,6 +456,23 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
     const long long k = base + position(np, nt);
     if (k >= 0 && k < total) store_item(jp, np, k, yp);
   }
+  if constexpr (L2) {
+    if (MODE == kOffsets || !given) {
+      // offsets given: this workgroup's kept tokens of its frame
+      for (int j = wave; j < nitems; j += kNW) {
+        const int n = item_token(j);
+        const long long k = base + position(n, nt);
+        if (k >= 0 && k < total) {
+          u32x4 x4[4][U][4];
+          float y[U][V];
+          load_rows2(xres, j % parts, n, x4);
+          modulate2(x4, rl.gate[n], rl.gate2[n], y);
+          store_item(j, n, k, y);
+        }
+      }
+      return;
+    }
+  }
   if (MODE == kOffsets || !given) {
     // offsets given: this workgroup's other kept tokens of its frame
     u32x4 xa[U][4];
@@ -452,18 +514,29 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
       else hi = mid;
     }
     const int te = lo, nte = s_nb[te], rank = kp + int(e - s_ext[te]);
-    u32x4 x[U][4];
+    u32x4 x[L2 ? 1 : U][4], x4[L2 ? 4 : 1][L2 ? U : 1][4];
     int n, before = 0;
-    float gn;
+    float gn, gn2 = 0.f;
     if (te == t) {  // this workgroup's own frame: its order is in LDS
       n = rl.byrank[rank];
-      load_item(part, n, x);
+      if constexpr (L2) {
+        load_rows2(xres, part, n, x4);
+        gn2 = rl.gate2[n];
+      } else {
+        load_item(part, n, x);
+      }
       gn = rl.gate[n];
       before = position(n, nte);
     } else {
       const size_t fo = size_t(te) * N;
       n = f.byrank[fo + rank];
-      load_rows(make_rsrc(static_cast<const In*>(f.X) + fo * f.C, uint32_t(N) * rb), part, n, x);
+      const __amdgpu_buffer_rsrc_t xr = make_rsrc(static_cast<const In*>(f.X) + fo * f.C, uint32_t(N) * rb);
+      if constexpr (L2) {
+        load_rows2(xr, part, n, x4);
+        gn2 = f.gate2[fo + n];
+      } else {
+        load_rows(xr, part, n, x);
+      }
       gn = f.gate[fo + n];
       // kept tokens of frame te before n in raster order
       const __amdgpu_buffer_rsrc_t rres = make_rsrc(f.rank + fo, uint32_t(N) * 4);
@@ -481,7 +554,8 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
     const long long k = (long long)s_off[te] + before;
     if (k < total) {
       float y[U][V];
-      modulate(x, gn, y);
+      if constexpr (L2) modulate2(x4, gn, gn2, y);
+      else modulate(x, gn, y);
       store_rows(part, te, n, k, y);
     }
   }
@@ -491,12 +565,17 @@ template <typename In, typename Out, int MODE>
 void launch_typed(const wz_config& c, const VideoArgs<AssignArgs>& a, int V, hipStream_t s) {
   const int nvec = c.C / Vec16<In>::kV;
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * a.v[0].P), V), block(kThreads);
-  const size_t lds = size_t(c.H) * c.W * 24;  // key 8 B; rank, byrank, gate, order / position 4 B
+  // key 8 B; rank, byrank, gate, order / position (and level-2 gate) 4 B
+  const size_t lds = size_t(c.H) * c.W * (c.spatial_levels == 2 ? 28 : 24);
   // one batch of loads per part: two vectors per lane, or one for short rows;
-  // the interpolation reads four blocks at once, one vector per lane each
-  if (c.assign == WZ_INTERP) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, true>), grid, block, lds, s, a);
-  else if (nvec <= kWave) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, false>), grid, block, lds, s, a);
-  else hipLaunchKernelGGL((k_assign_gather<In, Out, kVecPerLane, MODE, false>), grid, block, lds, s, a);
+  // the interpolation and the two-level modulator read four blocks at once,
+  // one vector per lane each
+  if (c.assign == WZ_INTERP)
+    hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, kInterp>), grid, block, lds, s, a);
+  else if (c.spatial_levels == 2)
+    hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, kSelect2>), grid, block, lds, s, a);
+  else if (nvec <= kWave) hipLaunchKernelGGL((k_assign_gather<In, Out, 1, MODE, kSelect1>), grid, block, lds, s, a);
+  else hipLaunchKernelGGL((k_assign_gather<In, Out, kVecPerLane, MODE, kSelect1>), grid, block, lds, s, a);
 }
 
 template <int MODE>
@@ -540,6 +619,7 @@ hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* 
     a.rank = ws ? advance(ws->rank, w) : nullptr;
     a.byrank = ws ? advance(ws->byrank, w) : nullptr;
     a.gate = ws ? advance(ws->gate, w) : nullptr;
+    a.gate2 = ws ? advance(ws->gate2, w) : nullptr;
     a.budget_out = advance(budget_out, v * vs.bud);
     a.offset_out = advance(offset_out, v * vs.off);
     a.out_tokens = advance(out_tokens, v * vs.out);

@@ -35,7 +35,7 @@ class Config(ctypes.Structure):
                 ("C", ctypes.c_int32), ("Q", ctypes.c_int32), ("in_dtype", ctypes.c_int32),
                 ("out_dtype", ctypes.c_int32), ("levels", ctypes.c_int32), ("B", ctypes.c_int64),
                 ("lambda_", ctypes.c_float), ("tau", ctypes.c_float), ("assign", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("spatial_levels", ctypes.c_int32)]
 
 
 _lib = None
@@ -82,10 +82,11 @@ class Problem:
     lam: float = 1.5
     tau: float = 0.0
     assign: int = 0  # WZ_SELECT; WZ_INTERP for the budget-guided interpolation
+    spatial_levels: int = 1  # 2: the two-level spatial modulator (selection only)
 
     def config(self):
         return Config(self.T, self.H, self.W, self.C, self.Q, self.in_dtype, self.out_dtype, self.levels,
-                      self.B, self.lam, self.tau, self.assign, 0)
+                      self.B, self.lam, self.tau, self.assign, self.spatial_levels)
 
     @property
     def N(self):
@@ -221,8 +222,8 @@ def to_device(inp, device="cuda:0"):
     return X.contiguous(), q.contiguous()
 
 
-def problem_of(wl, out_dtype=WZ_F32, assign=0):
+def problem_of(wl, out_dtype=WZ_F32, assign=0, spatial_levels=1):
     """Problem description of a workload (paper_2607_23265_amd.synth.Workload)."""
     return Problem(T=wl.T, H=wl.H, W=wl.W, C=wl.C, Q=wl.Q, B=wl.B,
                    in_dtype=WZ_BF16 if wl.dtype == "bf16" else WZ_F32, out_dtype=out_dtype,
-                   levels=wl.levels, lam=wl.lam, tau=wl.tau, assign=assign)
+                   levels=wl.levels, lam=wl.lam, tau=wl.tau, assign=assign, spatial_levels=spatial_levels)

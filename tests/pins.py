@@ -370,4 +370,41 @@ def pin_interp_affine_exact():
             assert near[k] == ny * W + nx
 
 
+def _two_level_closed_form(F, M, lam):
+    """x~ = mu2 + g2 (mu1 - mu2) + g1 (x - mu1), written out with explicit index clamping:
+    mu1 / g1 over the token's 2x2 block, mu2 / g2 over the 2x2 level-1 cells of its
+    level-2 block (the last row / column repeated at each level)."""
+    H, W = M.shape
+    Hb, Wb = (H + 1) // 2, (W + 1) // 2
+
+    def cell(A, bi, bj):  # mean over level-1 cell (bi, bj) of a token map
+        return 0.25 * sum(A[min(2 * bi + a, H - 1), min(2 * bj + b, W - 1)] for a in (0, 1) for b in (0, 1))
+
+    def block2(A, ci, cj):  # mean over the level-1 cells of level-2 block (ci, cj)
+        return 0.25 * sum(cell(A, min(2 * ci + a, Hb - 1), min(2 * cj + b, Wb - 1)) for a in (0, 1) for b in (0, 1))
+
+    out = np.zeros_like(F)
+    for h in range(H):
+        for w in range(W):
+            bi, bj = h // 2, w // 2
+            mu1, mu2 = cell(F, bi, bj), block2(F, bi // 2, bj // 2)
+            g1, g2 = lam * cell(M, bi, bj), lam * block2(M, bi // 2, bj // 2)
+            out[h, w] = mu2 + g2 * (mu1 - mu2) + g1 * (F[h, w] - mu1)
+    return out
+
+
+def pin_wsm_two_levels():
+    """The two-level spatial modulator: its closed form on random maps, the identity under a unit gate and the
+    level-2 approximation under a zero gate (odd and even grids)."""
+    rng = np.random.default_rng(5)
+    for H, W in ((14, 14), (13, 13), (5, 7), (2, 3), (1, 1)):
+        F = rng.standard_normal((H, W, 3))
+        M = rng.random((H, W))
+        got = oracle.wavelet_spatial_modulator(F, M, 1.5, 2)
+        assert np.abs(got - _two_level_closed_form(F, M, 1.5)).max() < 1e-12
+        assert np.abs(oracle.wavelet_spatial_modulator(F, np.full((H, W), 2.0), 0.5, 2) - F).max() < 1e-12
+        flat = oracle.wavelet_spatial_modulator(F, np.zeros((H, W)), 1.5, 2)
+        assert np.abs(flat - _two_level_closed_form(F, np.zeros((H, W)), 1.5)).max() < 1e-12
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -19,13 +19,10 @@ def L():
 
 
 def cfg(**kw):
-    reserved = kw.pop("reserved", 0)
     p = dict(T=64, H=14, W=14, C=3584, Q=32, B=1254, in_dtype=wz.WZ_BF16, out_dtype=wz.WZ_F32, levels=2,
              lam=1.5, tau=0.0)
     p.update(kw)
-    c = wz.Problem(**p).config()
-    c.reserved = reserved
-    return c
+    return wz.Problem(**p).config()
 
 
 def test_every_declared_symbol_is_exported(L):
@@ -47,7 +44,7 @@ def test_status_strings(L):
 def test_config_struct_layout():
     assert ctypes.sizeof(wz.Config) == 56
     assert wz.Config.B.offset == 32 and wz.Config.lambda_.offset == 40 and wz.Config.tau.offset == 44
-    assert wz.Config.assign.offset == 48 and wz.Config.reserved.offset == 52
+    assert wz.Config.assign.offset == 48 and wz.Config.spatial_levels.offset == 52
 
 
 def test_workspace_bytes(L):
@@ -64,7 +61,8 @@ def test_workspace_bytes(L):
     (dict(in_dtype=7), DTYPE), (dict(out_dtype=-1), DTYPE), (dict(levels=0), PARAM), (dict(levels=17), PARAM),
     (dict(lam=-1.0), PARAM), (dict(lam=float("inf")), PARAM), (dict(tau=2.5), PARAM), (dict(tau=float("nan")), PARAM),
     (dict(B=-1), BUDGET), (dict(B=64 * 196 + 1), BUDGET), (dict(assign=2), PARAM), (dict(assign=-1), PARAM),
-    (dict(reserved=1), PARAM),
+    (dict(spatial_levels=3), PARAM), (dict(spatial_levels=-1), PARAM),
+    (dict(spatial_levels=2, assign=1), PARAM),
 ])
 def test_invalid_config(L, kw, code):
     c = cfg(**kw)

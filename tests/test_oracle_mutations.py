@@ -132,6 +132,22 @@ def _grid_swap(n, H, Wd):
     return min(h, H), min(w, Wd)
 
 
+def _wsm_level2_unpooled_gate(F, Mhw, lam, levels=1):
+    # level 2 gated by the level-1 gate (the saliency map pooled only once)
+    H, W = Mhw.shape
+    LL = np.asarray(F, dtype=np.float64)
+    M1 = W.block_average(Mhw)
+    shapes, gated = [], []
+    for j in range(levels):
+        shapes.append(LL.shape[:2])
+        LL, LH, HL, HH = W.haar_analysis_2d(LL)
+        G = (lam * (M1 if j == 0 else W.block_average(M1) * 0 + M1[:LL.shape[0], :LL.shape[1]]))[:, :, None]
+        gated.append((G * LH, G * HL, G * HH))
+    for (h, w), (LH, HL, HH) in zip(reversed(shapes), reversed(gated)):
+        LL = W.haar_synthesis_2d(LL, LH, HL, HH, h, w)
+    return LL
+
+
 MUTATIONS = {
     "haar_detail_sign": ("haar_analysis", _analysis_detail_sign),
     "haar_synthesis_swapped": ("haar_synthesis", _synthesis_swapped),
@@ -152,6 +168,7 @@ MUTATIONS = {
     "filter_drops_frame0": ("retained_frames", _filter_drops_first),
     "interp_align_corners": ("_sample", _sample_corners),
     "interp_grid_transposed": ("interpolation_grid", _grid_swap),
+    "wsm_level2_unpooled_gate": ("wavelet_spatial_modulator", _wsm_level2_unpooled_gate),
 }
 
 
