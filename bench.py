@@ -12,7 +12,8 @@ Prints one JSON line: frames condensed per second (value), tokens/s, the
 algorithmic HBM rate of the whole call, the roofline of the dominant kernel
 (the relevance pass, timed with HIP events on its stream), the CPU oracle's
 rate on the host as a reported baseline, (`interp`) the rate with the
-budget-guided interpolation forming the tokens instead of selection, and
+budget-guided interpolation forming the tokens instead of selection,
+(`spatial_levels_2`) the rate with the two-level spatial modulator, and
 (`batched`) the rate of wz_condense_batch on several videos of the same
 workload per call -- separate modes, not the headline value.
 """
@@ -219,6 +220,19 @@ def main():
     torch.cuda.synchronize()
     i_ms = ev0.elapsed_time(ev1) / args.steps
     interp = {"ms_per_step": i_ms, "frames_per_s": wl.T / (i_ms * 1e-3)}
+    # and with the two-level spatial modulator (cfg.spatial_levels = 2)
+    p2 = wz.problem_of(wl, out_dtype, spatial_levels=2)
+    ws2 = wz.new_workspace(p2, dev)
+    for i in range(args.warmup):
+        wz.condense(p2, Xs[i % nsets], qs[i % nsets], ws=ws2, out=out)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for i in range(args.steps):
+        wz.condense(p2, Xs[i % nsets], qs[i % nsets], ws=ws2, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    l_ms = ev0.elapsed_time(ev1) / args.steps
+    levels2 = {"ms_per_step": l_ms, "frames_per_s": wl.T / (l_ms * 1e-3)}
 
     out_bytes = 2 if out_dtype == wz.WZ_BF16 else 4
     call_bytes = algorithmic_bytes(wl, out_bytes)
@@ -251,6 +265,7 @@ def main():
                      "us_per_launch": k1_ms * 1e3},
     }
     line["interp"] = interp
+    line["spatial_levels_2"] = levels2
     if batched:
         line["batched"] = batched
     if args.cpu_seconds > 0:
