@@ -162,7 +162,9 @@ wz_status wz_temporal_budget(const wz_config* cfg, const float* frame_rel,
  * the block), invert, and write the token's reconstructed features to row
  * offset[t] + k of out_tokens ([B][C], cfg->out_dtype), k = the token's rank
  * in raster order among the frame's kept tokens; out_index gets its flat
- * index.  offset ([T+1], as produced by wz_temporal_budget) must start at 0,
+ * index.  cfg->assign = WZ_INTERP forms the frame's n_t rows by the
+ * budget-guided interpolation of the modulated map instead (see wz_assign);
+ * cfg->spatial_levels = 2 modulates with two Haar levels.  offset ([T+1], as produced by wz_temporal_budget) must start at 0,
  * be nondecreasing with steps of at most H*W and end at offset[T] <= B; rows
  * from offset[T] on are not written, and no row outside [0, B) is ever
  * written whatever offset holds.  Needs no workspace.  One kernel launch.    */

@@ -30,8 +30,15 @@
 //      mu the block mean.  It goes to out_tokens[offset_t + position],
 //      position = kept tokens before it in raster order (a wave's own
 //      ballots over the ranks), its flat index t*H*W + n to out_index.
-// Only the blocks of kept tokens are read: at most 4 * B token rows, partly
-// from the Infinity Cache right after the pass over the frames.
+// Two further ways to form the rows (kernel parameter AM): the budget-guided
+// interpolation of Eq. (17) (cfg.assign = WZ_INTERP: each of a frame's n_t
+// cells blends four modulated taps of the frame), and the two-level spatial
+// modulator (cfg.spatial_levels = 2: a kept token's row from its 4x4 level-2
+// block).  Their cells depend on the budget or read 16 rows, so they read
+// nothing ahead and share every output row out over all workgroups.
+// Only the blocks of kept tokens are read: at most 4 * B token rows (16 * B
+// for the interpolation and two levels), partly from the Infinity Cache right
+// after the pass over the frames.
 #include "wz_budget.h"
 #include "wz_rank.h"
 
