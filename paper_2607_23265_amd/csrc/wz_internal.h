@@ -81,8 +81,10 @@ inline RelPlan relevance_plan(const wz_config& c) {
   RelPlan p{};
   p.kind = relevance_kind(c);
   if (p.kind == kRelTok) {
-    // tiles of at most 64 tokens with every channel, one slice
-    p.tiles = (N + 63) / 64;
+    // tiles of at most 64 tokens with every channel, one slice; more (down to
+    // 16 tokens) while the frames alone leave CUs without a workgroup
+    const int tr = (c.T + kXcds - 1) / kXcds * kXcds;
+    p.tiles = std::max((N + 63) / 64, std::min((N + 15) / 16, (kCUs + tr - 1) / tr));
     p.tile_tokens = (N + p.tiles - 1) / p.tiles;
     p.ipc = (p.tile_tokens + 7) / 8;
     p.ntg = c.Q <= 16 ? 1 : 2;
