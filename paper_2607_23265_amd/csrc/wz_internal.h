@@ -57,8 +57,8 @@ constexpr int kTokMax = 4096;     // validated bound on tokens per frame
 inline int qpad(int Q) { return (Q + 3) & ~3; }
 
 // Streaming kernels of the relevance pass, chosen by shape:
-//   kRelTok  bf16, Q <= 32: token tiles with every channel, LDS-transposed MFMA;
-//   kRelMfma bf16, Q > 32, frames of >= 49 tokens: MFMA-layout loads;
+//   kRelTok  bf16, Q <= 64: token tiles with every channel, LDS-transposed MFMA;
+//   kRelMfma bf16, Q > 64, frames of >= 49 tokens: MFMA-layout loads;
 //   kRelValu everything else (fp32 inputs, small frames with many queries).
 enum RelKind { kRelValu = 0, kRelMfma = 1, kRelTok = 2 };
 RelKind relevance_kind(const wz_config& c);
@@ -81,13 +81,23 @@ inline RelPlan relevance_plan(const wz_config& c) {
   RelPlan p{};
   p.kind = relevance_kind(c);
   if (p.kind == kRelTok) {
-    // tiles of at most 64 tokens with every channel, one slice; more (down to
-    // 16 tokens) while the frames alone leave CUs without a workgroup
+    // tiles of 16 to 64 tokens with every channel, one slice.  A workgroup
+    // fills a CU's LDS, so a CU runs (workgroups / CUs rounded up) of them one
+    // after another, each loading its tile's tokens and the query's 16-row
+    // tiles: take the tile count with the fewest rows loaded per CU, the
+    // smaller count on a tie
     const int tr = (c.T + kXcds - 1) / kXcds * kXcds;
-    p.tiles = std::max((N + 63) / 64, std::min((N + 15) / 16, (kCUs + tr - 1) / tr));
+    const int nq = c.Q <= 16 ? 16 : c.Q <= 32 ? 32 : 64;
+    const int lo = (N + 63) / 64, hi = std::max(lo, (N + 15) / 16);
+    long best = -1;
+    for (int k = lo; k <= hi; ++k) {
+      const int rows = (N + k - 1) / k + nq;
+      const long cost = long((long(tr) * k + kCUs - 1) / kCUs) * rows;
+      if (best < 0 || cost < best) best = cost, p.tiles = k;
+    }
     p.tile_tokens = (N + p.tiles - 1) / p.tiles;
     p.ipc = (p.tile_tokens + 7) / 8;
-    p.ntg = c.Q <= 16 ? 1 : 2;
+    p.ntg = nq / 16;
     p.mt = 0;
     p.slices = 1;
     p.kc = c.C;

@@ -8,9 +8,9 @@
 // and forms r_t and delta_t (and a_{t,n} when a unit holds only some channels).
 //
 // Three decompositions, chosen by shape:
-//  * token tiles (bf16, Q <= 32; below): a workgroup owns up to 64 tokens of a
+//  * token tiles (bf16, Q <= 64; below): a workgroup owns up to 64 tokens of a
 //    frame with every channel, so a_{t,n} is final in the pass;
-//  * MFMA layout (bf16, Q > 32, frames of >= 49 tokens): a workgroup owns one
+//  * MFMA layout (bf16, Q > 64, frames of >= 49 tokens): a workgroup owns one
 //    token tile of one frame (the whole frame when H*W <= 256; each wave holds
 //    two 16-row MFMA tiles) and one slice of at most 32 x 32 channels.  It
 //    stages the slice of the query (MFMA B layout) in LDS, where every wave
@@ -314,7 +314,7 @@ constexpr uint32_t kBf16OneLo = 0x00003F80u;  // bf16 pair (1, 0)
 constexpr uint32_t kBf16OneHi = 0x3F800000u;  // bf16 pair (0, 1)
 
 // ---------------------------------------------------------------------------
-// Token-tiled path (bf16, Q <= 32)
+// Token-tiled path (bf16, Q <= 64)
 // ---------------------------------------------------------------------------
 // A workgroup owns one tile of at most 64 tokens of one frame with ALL its
 // channels, so a_{t,n} is final here and no per-slice partial scores are
@@ -349,10 +349,10 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   const uint16_t* __restrict__ query = static_cast<const uint16_t*>(f.query);
   constexpr int NQ = NTG * 16;  // query rows of the accumulators
   constexpr int QI = NQ / 8;    // query load instructions per chunk
-  // per-wave chunk buffers (16-byte units swizzled by row); after a wave's
-  // loop its row buffer holds its partial S [64 rows][NQ] (fits: NQ <= 32)
-  __shared__ __align__(16) u32x4 s_x[kTokWaves][kTokRows][8];
-  __shared__ __align__(16) u32x4 s_q[kTokWaves][NQ][8];
+  // per-wave chunk buffers (16-byte units swizzled by row): rows 0 .. 63 of a
+  // wave's region stage its tile rows, rows 64 .. 64 + NQ - 1 its query rows;
+  // after the loop the region holds the wave's partial S [64 rows][NQ] floats
+  __shared__ __align__(16) u32x4 s_xq[kTokWaves][kTokRows + NQ][8];
   __shared__ __align__(16) float s_pool[POOL ? kTokPoolMax : 4];
   __shared__ float s_xx[kTokWaves][kTokRows];
   __shared__ float s_qq[kTokWaves][NQ];
@@ -416,7 +416,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     for (int k = 0; k < IPC; ++k) {
       const int row = 8 * k + lr;
       const u32x4 v = __builtin_bit_cast(u32x4, d.x[k]);
-      s_x[wave][row][lu ^ (row & 7)] = v;
+      s_xq[wave][row][lu ^ (row & 7)] = v;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         xx[k] = dot2(v[e], v[e], xx[k]);
@@ -428,7 +428,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     for (int k = 0; k < QI; ++k) {
       const int row = 8 * k + lr;
       const u32x4 v = __builtin_bit_cast(u32x4, d.q[k]);
-      s_q[wave][row][lu ^ (row & 7)] = v;
+      s_xq[wave][kTokRows + row][lu ^ (row & 7)] = v;
 #pragma unroll
       for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
     }
@@ -455,12 +455,12 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * i + r16;
-        A[i] = __builtin_bit_cast(bf16x8, s_x[wave][row][(4 * st + grp) ^ (row & 7)]);
+        A[i] = __builtin_bit_cast(bf16x8, s_xq[wave][row][(4 * st + grp) ^ (row & 7)]);
       }
 #pragma unroll
       for (int n = 0; n < NTG; ++n) {
         const int row = 16 * n + r16;
-        B[n] = __builtin_bit_cast(bf16x8, s_q[wave][row][(4 * st + grp) ^ (row & 7)]);
+        B[n] = __builtin_bit_cast(bf16x8, s_xq[wave][kTokRows + row][(4 * st + grp) ^ (row & 7)]);
       }
 #pragma unroll
       for (int n = 0; n < NTG; ++n)
@@ -471,7 +471,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   };
 
   // rows this wave never loads (8 * IPC .. 63) are zero in its buffer
-  for (int u = 8 * IPC * 8 + lane; u < kTokRows * 8; u += kWave) (&s_x[wave][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
+  for (int u = 8 * IPC * 8 + lane; u < kTokRows * 8; u += kWave) (&s_xq[wave][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
 
   Slot A, B;
   issue(wave, A);
@@ -524,8 +524,9 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
     if (lane < 16) s_sig[wave][16 * n + r16] = v;
   }
-  // wave w's partial S sits in its own row buffer: [row][NQ] floats from &s_x[w][0][0]
-  auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_x[w][0][0])[r * NQ + j]; };
+  // wave w's partial S sits in its own region: [row][NQ] floats from &s_xq[w][0][0]
+  static_assert((kTokRows + NQ) * 8 * 16 >= kTokRows * NQ * 4, "partial S fits the wave's region");
+  auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_xq[w][0][0])[r * NQ + j]; };
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -721,19 +722,23 @@ void launch_mfma(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipS
 
 template <int NTG, int IPC>
 void launch_tok(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
-  if (va.v[0].C <= kTokPoolMax)
-    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens,
-                       va);
-  else
-    hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
-                       pl.tile_tokens, va);
+  // with 64 query columns the staging regions leave no room for the gathered channel sums
+  if constexpr (NTG <= 2) {
+    if (va.v[0].C <= kTokPoolMax) {
+      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+                         pl.tile_tokens, va);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens,
+                     va);
 }
 
 }  // namespace
 
 RelKind relevance_kind(const wz_config& c) {
   if (c.in_dtype != WZ_BF16) return kRelValu;
-  if (c.Q <= 32) return kRelTok;
+  if (c.Q <= 64) return kRelTok;
   // two 16-row MFMA tiles per wave, at least 2 waves: frames of at least 49 tokens
   return c.H * c.W >= 49 ? kRelMfma : kRelValu;
 }
@@ -761,7 +766,7 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
     case 7: launch_tok<NTG, 7>(pl, va, V, s); break; \
     default: launch_tok<NTG, 8>(pl, va, V, s); break; \
   }
-    if (pl.ntg == 1) { WZ_TOK(1) } else { WZ_TOK(2) }
+    if (pl.ntg == 1) { WZ_TOK(1) } else if (pl.ntg == 2) { WZ_TOK(2) } else { WZ_TOK(4) }
 #undef WZ_TOK
   } else if (pl.kind == kRelMfma) {
     // queries of more than 32 tokens take several passes of 32 over the slice:

@@ -240,6 +240,12 @@ EDGE = {
     "many_frames": dict(T=512, H=2, W=2, C=16, Q=16, B=1900),
     "max_channels": dict(T=2, H=7, W=7, C=65536, Q=16, B=20),
     "max_query": dict(T=3, H=7, W=7, C=256, Q=1024, B=30),
+    # four 16-column query tiles in the token-tiled pass: ragged query and
+    # channels, a full 64-token tile, one-token frames, the most channels
+    "query_47_ragged": dict(T=6, H=7, W=9, C=200, Q=47, B=60),
+    "query_64_full_tile": dict(T=3, H=8, W=8, C=136, Q=64, B=40),
+    "query_33_single_token": dict(T=5, H=1, W=1, C=72, Q=33, B=3),
+    "query_64_max_channels": dict(T=2, H=7, W=7, C=65536, Q=64, B=20),
 }
 
 
