@@ -15,7 +15,9 @@ rate on the host as a reported baseline, (`interp`) the rate with the
 budget-guided interpolation forming the tokens instead of selection,
 (`spatial_levels_2`) the rate with the two-level spatial modulator, and
 (`batched`) the rate of wz_condense_batch on several videos of the same
-workload per call -- separate modes, not the headline value.
+workload per call, and (`queries`) the rate of wz_condense_queries with
+several queries over each video per call -- separate modes, not the
+headline value.
 """
 import argparse
 import hashlib
@@ -44,6 +46,8 @@ def parse():
                     help="approximate CPU time spent timing the oracle (0 disables)")
     ap.add_argument("--videos", type=int, default=4,
                     help="also time wz_condense_batch on this many videos of the workload per call (0 disables)")
+    ap.add_argument("--queries", type=int, default=2,
+                    help="also time wz_condense_queries with this many queries per video per call (0 disables)")
     ap.add_argument("--copy-calib", type=int, default=0,
                     help="only run this many plain device copies of a frame tensor (the known-size kernel that "
                          "scales HBM byte counters) and exit")
@@ -208,6 +212,31 @@ def main():
                    "hbm_gbps": V * algorithmic_bytes(wl, 2 if out_dtype == wz.WZ_BF16 else 4) / (b_ms * 1e-3) / 1e9}
         del XB, QB, wsb, outb
 
+    queries = None
+    if args.queries > 1:
+        # several queries over each video per call (wz_condense_queries): query g is the
+        # workload's query with its channels rotated by 8 g
+        G = args.queries
+        QG = [torch.stack([qs[i % nsets].roll(8 * g, dims=-1) for g in range(G)]).contiguous()
+              for i in range(nsets)]
+        wsq = torch.empty(G * ws.numel(), dtype=torch.uint8, device=dev)
+        dt = torch.float32 if out_dtype == wz.WZ_F32 else torch.bfloat16
+        outq = (torch.empty((G, p.B, p.C), dtype=dt, device=dev), torch.empty((G, p.B), dtype=torch.int32, device=dev))
+        for i in range(args.warmup):
+            wz.condense_queries(p, Xs[i % nsets], QG[i % nsets], ws=wsq, out=outq)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(args.steps):
+            wz.condense_queries(p, Xs[i % nsets], QG[i % nsets], ws=wsq, out=outq)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        q_ms = ev0.elapsed_time(ev1) / args.steps
+        queries = {"queries": G, "calls": args.steps, "ms_per_call": q_ms,
+                   "shared_pass": wl.dtype == "bf16" and G * wl.Q <= 64,
+                   "query_frames_per_s": G * wl.T / (q_ms * 1e-3),
+                   "vs_separate_calls": G * ms_step / q_ms}
+        del QG, wsq, outq
+
     # the same pass with the budget-guided interpolation forming the tokens (cfg.assign = WZ_INTERP)
     pi = wz.problem_of(wl, out_dtype, assign=wz.WZ_INTERP)
     for i in range(args.warmup):
@@ -268,6 +297,8 @@ def main():
     line["spatial_levels_2"] = levels2
     if batched:
         line["batched"] = batched
+    if queries:
+        line["queries"] = queries
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -16,7 +16,8 @@
  *                           saliency-gated 2-D Haar modulation, compacted in
  *                           temporal order (Eq. (7), Eq. (12)-(15), Eq. (19));
  *   wz_condense             the three stages in sequence;
- *   wz_condense_batch       the same for several videos at once.
+ *   wz_condense_batch       the same for several videos at once;
+ *   wz_condense_queries     the same for several queries over one video.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -185,7 +186,6 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query,
                       void* out_tokens, int32_t* out_index, int32_t* budget,
                       int32_t* offset, void* ws, size_t ws_bytes, void* stream);
 
-/* Static, human-readable name of a status code.                               */
 /* Several videos of one shape condensed in one call: the whole pass of
  * wz_condense for each of `videos` videos (1 <= videos <= 8, else
  * WZ_ERR_SHAPE), every kernel launched once for all of them, so launch and
@@ -203,6 +203,26 @@ wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X,
                             int32_t* offset, void* ws, size_t ws_bytes,
                             void* stream);
 
+/* Several queries over one video in one call: the whole pass of wz_condense
+ * for each of `queries` queries of Q tokens (1 <= queries <= 8, else
+ * WZ_ERR_SHAPE) on the same X, each with its own budgets and outputs.  The
+ * paper scores every query afresh; here, when the inputs are bf16 and
+ * queries * Q <= 64, one pass over X serves every query: the query tokens
+ * are the columns of one relevance contraction, and a_{t,n}, r_t and the
+ * selection are taken per query.  Otherwise each query takes its own pass
+ * over X (launched together, as in wz_condense_batch).  Layouts:
+ * X [T][H][W][C], query [G][Q][C], out_tokens [G][B][C], out_index [G][B],
+ * budget [G][T] and offset [G][T+1] (optional, NULL: kept in the
+ * workspace).  ws: at least queries * wz_workspace_bytes(cfg) bytes, query g
+ * using the g-th slice of that size.  Query g's outputs are bitwise those of
+ * wz_condense with query g alone.                                            */
+wz_status wz_condense_queries(const wz_config* cfg, int32_t queries,
+                              const void* X, const void* query,
+                              void* out_tokens, int32_t* out_index,
+                              int32_t* budget, int32_t* offset, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/* Static, human-readable name of a status code.                               */
 const char* wz_status_str(wz_status s);
 
 #ifdef __cplusplus

@@ -45,9 +45,10 @@ wz_status from_hip(hipError_t e) { return e == hipSuccess ? WZ_OK : WZ_ERR_DEVIC
 namespace {
 
 // The whole pass for V videos of one shape (wz_condense, wz_condense_batch).
-wz_status condense_videos(const wz_config* cfg, int V, const void* X, const void* query, void* out_tokens,
-                          int32_t* out_index, int32_t* budget, int32_t* offset, void* ws, size_t ws_bytes,
-                          void* stream) {
+// V videos (shared_x false) or V queries over one video (shared_x true)
+wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void* X, const void* query,
+                          void* out_tokens, int32_t* out_index, int32_t* budget, int32_t* offset, void* ws,
+                          size_t ws_bytes, void* stream) {
   WZ_TRY(check_config(cfg));
   WZ_TRY(check_ptr(X, 16));
   WZ_TRY(check_ptr(query, 16));
@@ -64,7 +65,8 @@ wz_status condense_videos(const wz_config* cfg, int V, const void* X, const void
   const long long TN = (long long)cfg->T * cfg->H * cfg->W;
   Videos vs;
   vs.V = V;
-  vs.x = TN * cfg->C * s_in;
+  vs.shared_x = shared_x;
+  vs.x = shared_x ? 0 : TN * cfg->C * s_in;
   vs.q = (long long)cfg->Q * cfg->C * s_in;
   vs.ws = (long long)w.bytes;
   vs.out = cfg->B * cfg->C * s_out;
@@ -168,14 +170,23 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
 wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
                       int32_t* out_index, int32_t* budget, int32_t* offset, void* ws, size_t ws_bytes,
                       void* stream) {
-  return condense_videos(cfg, 1, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes, stream);
+  return condense_videos(cfg, 1, false, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes, stream);
 }
 
 wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X, const void* query,
                             void* out_tokens, int32_t* out_index, int32_t* budget, int32_t* offset, void* ws,
                             size_t ws_bytes, void* stream) {
   if (videos < 1 || videos > kMaxVideos) return WZ_ERR_SHAPE;
-  return condense_videos(cfg, videos, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes, stream);
+  return condense_videos(cfg, videos, false, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes,
+                         stream);
+}
+
+wz_status wz_condense_queries(const wz_config* cfg, int32_t queries, const void* X, const void* query,
+                              void* out_tokens, int32_t* out_index, int32_t* budget, int32_t* offset, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (queries < 1 || queries > kMaxVideos) return WZ_ERR_SHAPE;
+  return condense_videos(cfg, queries, true, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes,
+                         stream);
 }
 
 }  // extern "C"

@@ -315,11 +315,13 @@ hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_scor
   const RelPlan pl = relevance_plan(c);
   const int N = c.H * c.W;
   const int roles = (pl.slices > 1 || order) ? 2 : 1;
+  // queries sharing one pass over X find the video's channel sums in the first workspace
+  const bool shared = vs.shared_x && shared_pass(c, vs.V);
   VideoArgs<FrameArgs> va{};
   for (int v = 0; v < vs.V; ++v) {
     const Workspace w = advance(ws, v * vs.ws);
     va.v[v] = FrameArgs{w.s_part,   w.g_part,  w.qg_part,
-                        w.sig_part, w.pool_part, advance(tok_score, v * vs.ws),
+                        w.sig_part, shared ? ws.pool_part : w.pool_part, advance(tok_score, v * vs.ws),
                         advance(frame_rel, v * vs.ws), advance(frame_delta, v * vs.ws), w.rank,
                         w.byrank,   w.gate,    c.spatial_levels == 2 && order ? w.gate2 : nullptr, c.T,
                         N,          c.H,       c.W,

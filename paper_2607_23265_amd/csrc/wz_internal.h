@@ -201,13 +201,19 @@ constexpr int kMaxVideos = 8;
 struct Videos {
   int V = 1;
   long long x = 0, q = 0, ws = 0, out = 0, idx = 0, bud = 0, off = 0;
+  // the V problems are V queries over one video (x = 0): when shared_pass
+  // holds they share one pass over X, and problem v > 0 reads the channel
+  // sums of problem 0's workspace
+  bool shared_x = false;
 };
+// queries of one video whose columns fit one token-tiled pass (64 at most)
+inline bool shared_pass(const wz_config& c, int V) { return relevance_kind(c) == kRelTok && c.Q * V <= 64; }
 template <typename A>
 struct VideoArgs {
   A v[kMaxVideos];
 };
 template <typename P>
-inline P* advance(P* p, long long bytes) {
+__host__ __device__ inline P* advance(P* p, long long bytes) {
   return p ? reinterpret_cast<P*>(reinterpret_cast<uintptr_t>(p) + bytes) : p;
 }
 inline Workspace advance(const Workspace& w, long long bytes) {

@@ -47,6 +47,11 @@ struct StreamArgs {
   float* pool_part;
   float* tok_score;  // written here when there is one slice
   int T, N, C, Q, QP, tiles, slices;
+  // several queries in one pass (token-tiled path): `query` holds groups x qg
+  // rows (Q = groups * qg); query g's scores, column sums and norms go to the
+  // buffers above advanced by g * gws bytes, its channel sums are query 0's
+  int groups = 1, qg = 0;
+  long long gws = 0;
 };
 static_assert(sizeof(VideoArgs<StreamArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
@@ -342,7 +347,9 @@ constexpr int kTokPoolMax = 8192;  // channels whose sums are gathered in LDS
 
 // POOL: the tile's channel sums are gathered in LDS (C <= kTokPoolMax) and
 // stored once at the end; otherwise a few lanes store them chunk by chunk.
-template <int NTG, int IPC, bool POOL>
+// GR: the query columns are f.groups queries of f.qg tokens each, a_{t,n}
+// taken per query.
+template <int NTG, int IPC, bool POOL, bool GR>
 __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_tokens, const VideoArgs<StreamArgs> va) {
   const StreamArgs f = va.v[blockIdx.y];
   const uint16_t* __restrict__ X = static_cast<const uint16_t*>(f.X);
@@ -541,8 +548,14 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
       v += s_sig[w][tid];
       qv += s_qq[w][tid];
     }
-    f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
-    if (tile == 0) f.qg_part[size_t(t) * Q + tid] = qv;
+    if constexpr (GR) {
+      const int g = tid / f.qg, j = tid - g * f.qg;
+      advance(f.sig_part, g * f.gws)[(size_t(t) * f.tiles + tile) * f.qg + j] = v;
+      if (tile == 0) advance(f.qg_part, g * f.gws)[size_t(t) * f.qg + j] = qv;
+    } else {
+      f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
+      if (tile == 0) f.qg_part[size_t(t) * Q + tid] = qv;
+    }
   }
   if (tid < NQ) {
     float qv = 0.f;
@@ -566,16 +579,33 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   lds_barrier();  // 1 / |q_j| in s_rq
 #pragma unroll
   for (int e = 0; e < CPT; ++e) rq[e] = s_rq[cg + e];
-  float best = -INFINITY;
+  if constexpr (GR) {
+    // the row's S_nj / |q_j| into LDS (wave 0's region: every read of the
+    // partials is behind the last barrier); thread g of the row's eight takes
+    // the maximum over query g's columns
+    float* s_cos = reinterpret_cast<float*>(&s_xq[0][0][0]);  // [64 rows][NQ]
 #pragma unroll
-  for (int e = 0; e < CPT; ++e)
-    if (cg + e < Q) best = fmaxf(best, sv[e] * rq[e]);
-  best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
-  best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
-  best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
-  if ((tid & 7) == 0 && row < TM) {
-    const float xn = sqrtf(x2);
-    f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+    for (int e = 0; e < CPT; ++e) s_cos[row * NQ + cg + e] = sv[e] * rq[e];
+    lds_barrier();
+    const int g = tid & 7;
+    if (g < f.groups && row < TM) {
+      float best = -INFINITY;
+      for (int j = 0; j < f.qg; ++j) best = fmaxf(best, s_cos[row * NQ + g * f.qg + j]);
+      const float xn = sqrtf(x2);
+      advance(f.tok_score, g * f.gws)[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+    }
+  } else {
+    float best = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < CPT; ++e)
+      if (cg + e < Q) best = fmaxf(best, sv[e] * rq[e]);
+    best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
+    best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
+    best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
+    if ((tid & 7) == 0 && row < TM) {
+      const float xn = sqrtf(x2);
+      f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+    }
   }
   if (POOL) {
     const __amdgpu_buffer_rsrc_t pres =
@@ -720,18 +750,25 @@ void launch_mfma(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipS
                      pl.kc, va);
 }
 
-template <int NTG, int IPC>
-void launch_tok(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
+template <int NTG, int IPC, bool GR>
+void launch_tok_gr(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
   // with 64 query columns the staging regions leave no room for the gathered channel sums
   if constexpr (NTG <= 2) {
     if (va.v[0].C <= kTokPoolMax) {
-      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true, GR>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
                          pl.tile_tokens, va);
       return;
     }
   }
-  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false>), dim3(pl.grid, V), dim3(pl.threads), 0, s, pl.tile_tokens,
-                     va);
+  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false, GR>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+                     pl.tile_tokens, va);
+}
+template <int NTG, int IPC>
+void launch_tok(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
+  if (va.v[0].groups > 1)
+    launch_tok_gr<NTG, IPC, true>(pl, va, V, s);
+  else
+    launch_tok_gr<NTG, IPC, false>(pl, va, V, s);
 }
 
 }  // namespace
@@ -745,15 +782,25 @@ RelKind relevance_kind(const wz_config& c) {
 
 hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void* query, float* tok_score,
                                    const Workspace& ws, hipStream_t s, const Videos& vs) {
-  const RelPlan pl = relevance_plan(c);
+  RelPlan pl = relevance_plan(c);
   VideoArgs<StreamArgs> va{};
-  for (int v = 0; v < vs.V; ++v) {
-    const Workspace w = advance(ws, v * vs.ws);
-    va.v[v] = StreamArgs{advance(X, v * vs.x), advance(query, v * vs.q), w.s_part, w.g_part, w.qg_part,
-                         w.sig_part, w.pool_part, advance(tok_score, v * vs.ws), c.T, c.H * c.W, c.C, c.Q,
-                         qpad(c.Q), pl.tiles, pl.slices};
+  int V = vs.V;
+  if (vs.shared_x && shared_pass(c, vs.V)) {
+    // every query's columns in one pass over X: the per-query plan's tiles,
+    // query tiles for all the columns
+    const int QT = c.Q * vs.V;
+    pl.ntg = QT <= 16 ? 1 : QT <= 32 ? 2 : 4;
+    va.v[0] = StreamArgs{X, query, ws.s_part, ws.g_part, ws.qg_part, ws.sig_part, ws.pool_part, tok_score,
+                         c.T, c.H * c.W, c.C, QT, qpad(QT), pl.tiles, pl.slices, vs.V, c.Q, vs.ws};
+    V = 1;
+  } else {
+    for (int v = 0; v < vs.V; ++v) {
+      const Workspace w = advance(ws, v * vs.ws);
+      va.v[v] = StreamArgs{advance(X, v * vs.x), advance(query, v * vs.q), w.s_part, w.g_part, w.qg_part,
+                           w.sig_part, w.pool_part, advance(tok_score, v * vs.ws), c.T, c.H * c.W, c.C, c.Q,
+                           qpad(c.Q), pl.tiles, pl.slices};
+    }
   }
-  const int V = vs.V;
   if (pl.kind == kRelTok) {
 #define WZ_TOK(NTG)                                 \
   switch (pl.ipc) {                                 \

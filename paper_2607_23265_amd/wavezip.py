@@ -20,7 +20,8 @@ WZ_SELECT, WZ_INTERP = 0, 1
 _STATUS = {0: "WZ_OK", 1: "WZ_ERR_NULL", 2: "WZ_ERR_ALIGN", 3: "WZ_ERR_SHAPE", 4: "WZ_ERR_DTYPE",
            5: "WZ_ERR_PARAM", 6: "WZ_ERR_BUDGET", 7: "WZ_ERR_WORKSPACE", 8: "WZ_ERR_DEVICE"}
 EXPORTS = ("wz_workspace_bytes", "wz_relevance", "wz_relevance_pass", "wz_temporal_budget",
-           "wz_spatial_dwt_condense", "wz_condense", "wz_condense_batch", "wz_status_str")
+           "wz_spatial_dwt_condense", "wz_condense", "wz_condense_batch", "wz_condense_queries",
+           "wz_status_str")
 
 
 class WZError(RuntimeError):
@@ -56,11 +57,12 @@ def lib():
     L.wz_relevance.argtypes = [cfgp, P, P, P, P, P, P, S, P]
     L.wz_relevance_pass.argtypes = [cfgp, P, P, P, P, S, P]
     L.wz_condense_batch.argtypes = [cfgp, ctypes.c_int32, P, P, P, P, P, P, P, S, P]
+    L.wz_condense_queries.argtypes = [cfgp, ctypes.c_int32, P, P, P, P, P, P, P, S, P]
     L.wz_temporal_budget.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_spatial_dwt_condense.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_condense.argtypes = [cfgp, P, P, P, P, P, P, P, S, P]
     for f in ("wz_relevance", "wz_relevance_pass", "wz_temporal_budget", "wz_spatial_dwt_condense", "wz_condense",
-              "wz_condense_batch"):
+              "wz_condense_batch", "wz_condense_queries"):
         getattr(L, f).restype = ctypes.c_int
     L.wz_status_str.argtypes = [ctypes.c_int]
     L.wz_status_str.restype = ctypes.c_char_p
@@ -208,6 +210,26 @@ def condense_batch(p: Problem, X, query, ws=None, out=None):
     cfg = p.config()
     _check(lib().wz_condense_batch(ctypes.byref(cfg), V, _ptr(X), _ptr(query), _ptr(tok), _ptr(idx), _ptr(b),
                                    _ptr(o), _ptr(ws), ws.numel(), _stream(dev)), "wz_condense_batch")
+    return tok, idx, b, o
+
+
+def condense_queries(p: Problem, X, query, ws=None, out=None):
+    """wz_condense_queries: G queries over one video, X [T, H, W, C], query [G, Q, C] ->
+    (tokens [G, B, C], index [G, B], budget [G, T], offset [G, T+1])."""
+    _require_device(X, query)
+    dev = X.device
+    G = query.shape[0]
+    ws = torch.empty(G * workspace_bytes(p), dtype=torch.uint8, device=dev) if ws is None else ws
+    dt = torch.float32 if p.out_dtype == WZ_F32 else torch.bfloat16
+    if out is None:
+        out = (torch.empty((G, max(p.B, 1), p.C), dtype=dt, device=dev),
+               torch.empty((G, max(p.B, 1)), dtype=torch.int32, device=dev))
+    tok, idx = out
+    b = torch.empty((G, p.T), dtype=torch.int32, device=dev)
+    o = torch.empty((G, p.T + 1), dtype=torch.int32, device=dev)
+    cfg = p.config()
+    _check(lib().wz_condense_queries(ctypes.byref(cfg), G, _ptr(X), _ptr(query), _ptr(tok), _ptr(idx), _ptr(b),
+                                     _ptr(o), _ptr(ws), ws.numel(), _stream(dev)), "wz_condense_queries")
     return tok, idx, b, o
 
 

@@ -73,6 +73,7 @@ def test_invalid_config(L, kw, code):
     assert L.wz_spatial_dwt_condense(ctypes.byref(c), fake, fake, fake, fake, fake, None) == code
     assert L.wz_condense(ctypes.byref(c), fake, fake, fake, fake, None, None, fake, 1 << 30, None) == code
     assert L.wz_condense_batch(ctypes.byref(c), 2, fake, fake, fake, fake, None, None, fake, 1 << 30, None) == code
+    assert L.wz_condense_queries(ctypes.byref(c), 2, fake, fake, fake, fake, None, None, fake, 1 << 30, None) == code
 
 
 def test_pointer_checks(L):
@@ -112,6 +113,11 @@ def test_pointer_checks(L):
     assert L.wz_condense_batch(ctypes.byref(c), 3, ok, ok, ok, ok, None, None, ok, 3 * need - 1, None) == WORKSPACE
     assert L.wz_condense_batch(ctypes.byref(c), 3, nul, ok, ok, ok, None, None, ok, 3 * need, None) == NULL
     assert L.wz_condense_batch(ctypes.byref(c), 3, ok, ok, ok, odd4, None, None, ok, 3 * need, None) == ALIGN
+    assert L.wz_condense_queries(ctypes.byref(c), 0, ok, ok, ok, ok, None, None, ok, need, None) == SHAPE
+    assert L.wz_condense_queries(ctypes.byref(c), 9, ok, ok, ok, ok, None, None, ok, 9 * need, None) == SHAPE
+    assert L.wz_condense_queries(ctypes.byref(c), 3, ok, ok, ok, ok, None, None, ok, 3 * need - 1, None) == WORKSPACE
+    assert L.wz_condense_queries(ctypes.byref(c), 3, ok, nul, ok, ok, None, None, ok, 3 * need, None) == NULL
+    assert L.wz_condense_queries(ctypes.byref(c), 3, ok, ok, ok, odd4, None, None, ok, 3 * need, None) == ALIGN
 
 
 def test_binding_refuses_cpu_tensors():
