@@ -87,7 +87,8 @@ inline RelPlan relevance_plan(const wz_config& c) {
     // tiles: take the tile count with the fewest rows loaded per CU, the
     // smaller count on a tie
     const int tr = (c.T + kXcds - 1) / kXcds * kXcds;
-    const int nq = c.Q <= 16 ? 16 : c.Q <= 32 ? 32 : 64;
+    // query tiles: 1, 2 or 4 of 16 columns; above 64 columns, passes of 32
+    const int nq = c.Q <= 16 ? 16 : c.Q <= 32 ? 32 : c.Q <= 64 ? 64 : 32;
     const int lo = (N + 63) / 64, hi = std::max(lo, (N + 15) / 16);
     long best = -1;
     for (int k = lo; k <= hi; ++k) {

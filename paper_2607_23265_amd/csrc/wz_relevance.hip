@@ -344,12 +344,17 @@ constexpr int kTokWaves = 8;
 constexpr int kTokChunk = 64;      // channels per chunk (128 bytes of a bf16 row)
 constexpr int kTokRows = 64;       // tokens per tile at most (four 16-row MFMA tiles)
 constexpr int kTokPoolMax = 8192;  // channels whose sums are gathered in LDS
+constexpr int kTokQMax = 256;      // query tokens: at most four passes of 64 over a tile
 
 // POOL: the tile's channel sums are gathered in LDS (C <= kTokPoolMax) and
 // stored once at the end; otherwise a few lanes store them chunk by chunk.
-// GR: the query columns are f.groups queries of f.qg tokens each, a_{t,n}
-// taken per query.
-template <int NTG, int IPC, bool POOL, bool GR>
+// MODE kTokOne: one pass over the tile for every query column;
+// kTokGroups: the query columns are f.groups queries of f.qg tokens each,
+// a_{t,n} taken per query; kTokPasses: queries of more than NQ tokens, one
+// pass over the tile per NQ query rows (its later reads mostly from cache),
+// a_{t,n} the maximum over the passes, the channel sums taken in the first.
+enum TokMode { kTokOne = 0, kTokGroups = 1, kTokPasses = 2 };
+template <int NTG, int IPC, bool POOL, int MODE>
 __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_tokens, const VideoArgs<StreamArgs> va) {
   const StreamArgs f = va.v[blockIdx.y];
   const uint16_t* __restrict__ X = static_cast<const uint16_t*>(f.X);
@@ -379,234 +384,244 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   const int nch = (C + kTokChunk - 1) / kTokChunk;
 
   const __amdgpu_buffer_rsrc_t xres = make_rsrc_uniform(X + (size_t(t) * N + tok0) * C, uint32_t(TM) * C * 2);
-  const __amdgpu_buffer_rsrc_t qres = make_rsrc_uniform(query, uint32_t(Q) * C * 2);
+  constexpr bool GR = MODE == kTokGroups;
+  const int npass = MODE == kTokPasses ? (Q + NQ - 1) / NQ : 1;
+  float best_all = -INFINITY;
+  for (int h = 0; h < npass; ++h) {
+    const int qb = h * NQ, Qh = min(NQ, Q - qb);
+    const bool sums = h == 0;
+    const __amdgpu_buffer_rsrc_t qres = make_rsrc_uniform(query + size_t(qb) * C, uint32_t(Qh) * C * 2);
 
-  // ring slot: the tile's rows 8k + lr and the query's rows 8k + lr, unit lu
-  // of the chunk; chunks past the end, rows past the tile or the query and
-  // channels past C read zeros
-  struct Slot {
-    bf16x8 x[IPC];
-    bf16x8 q[QI];
-  };
-  auto issue = [&](int c, Slot& d) {
-    const int cc = c * kTokChunk + 8 * lu;
-    const bool ok = c < nch && cc < C;
+    // ring slot: the tile's rows 8k + lr and the query's rows 8k + lr, unit lu
+    // of the chunk; chunks past the end, rows past the tile or the query and
+    // channels past C read zeros
+    struct Slot {
+      bf16x8 x[IPC];
+      bf16x8 q[QI];
+    };
+    auto issue = [&](int c, Slot& d) {
+      const int cc = c * kTokChunk + 8 * lu;
+      const bool ok = c < nch && cc < C;
 #pragma unroll
-    for (int k = 0; k < IPC; ++k) d.x[k] = buf_load_bf16x8(xres, ok ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
+      for (int k = 0; k < IPC; ++k) d.x[k] = buf_load_bf16x8(xres, ok ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
 #pragma unroll
-    for (int k = 0; k < QI; ++k) {
-      const int j = 8 * k + lr;
-      d.q[k] = buf_load_bf16x8(qres, (ok && j < Q) ? (j * C + cc) * 2 : kOOB);
-    }
-  };
-
-  f32x4 Sacc[4][NTG];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int n = 0; n < NTG; ++n) Sacc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float xx[IPC], qq[QI];
-#pragma unroll
-  for (int k = 0; k < IPC; ++k) xx[k] = 0.f;
-#pragma unroll
-  for (int k = 0; k < QI; ++k) qq[k] = 0.f;
-  uint32_t one_lo = kBf16OneLo, one_hi = kBf16OneHi;
-  asm volatile("" : "+v"(one_lo), "+v"(one_hi));  // opaque: keeps them out of inline constants
-  float* pool = POOL ? s_pool : f.pool_part + (size_t(t) * f.tiles + tile) * C;
-
-  auto consume = [&](int c, const Slot& d) {
-    // rows to LDS; |x|^2, |q_j|^2 and channel sums from the registers
-    float cs[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) cs[e] = 0.f;
-#pragma unroll
-    for (int k = 0; k < IPC; ++k) {
-      const int row = 8 * k + lr;
-      const u32x4 v = __builtin_bit_cast(u32x4, d.x[k]);
-      s_xq[wave][row][lu ^ (row & 7)] = v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        xx[k] = dot2(v[e], v[e], xx[k]);
-        cs[2 * e] = dot2(v[e], one_lo, cs[2 * e]);
-        cs[2 * e + 1] = dot2(v[e], one_hi, cs[2 * e + 1]);
+      for (int k = 0; k < QI; ++k) {
+        const int j = 8 * k + lr;
+        d.q[k] = buf_load_bf16x8(qres, (ok && j < Qh) ? (j * C + cc) * 2 : kOOB);
       }
-    }
-#pragma unroll
-    for (int k = 0; k < QI; ++k) {
-      const int row = 8 * k + lr;
-      const u32x4 v = __builtin_bit_cast(u32x4, d.q[k]);
-      s_xq[wave][kTokRows + row][lu ^ (row & 7)] = v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
-    }
-    // channel sums over the wave's rows: lanes lu, lu + 8, ..., lu + 56 in a fixed order
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v = cs[e];
-      v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
-      const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-      v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-      const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-      cs[e] = __uint_as_float(b[0]) + __uint_as_float(b[1]);
-    }
-    const int c0 = c * kTokChunk + 8 * lu;
-    if (lane < 8 && c0 < C) {
-      *reinterpret_cast<f32x4*>(pool + c0) = f32x4{cs[0], cs[1], cs[2], cs[3]};
-      *reinterpret_cast<f32x4*>(pool + c0 + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
-    }
-  };
-  auto contract = [&]() {
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      bf16x8 A[4], B[NTG];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 16 * i + r16;
-        A[i] = __builtin_bit_cast(bf16x8, s_xq[wave][row][(4 * st + grp) ^ (row & 7)]);
-      }
-#pragma unroll
-      for (int n = 0; n < NTG; ++n) {
-        const int row = 16 * n + r16;
-        B[n] = __builtin_bit_cast(bf16x8, s_xq[wave][kTokRows + row][(4 * st + grp) ^ (row & 7)]);
-      }
-#pragma unroll
-      for (int n = 0; n < NTG; ++n)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[i], B[n], Sacc[i][n], 0, 0, 0);
-    }
-  };
+    };
 
-  // rows this wave never loads (8 * IPC .. 63) are zero in its buffer
-  for (int u = 8 * IPC * 8 + lane; u < kTokRows * 8; u += kWave) (&s_xq[wave][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
-
-  Slot A, B;
-  issue(wave, A);
-  issue(wave + kTokWaves, B);
-  for (int c = wave; c < nch; c += 2 * kTokWaves) {
-    __builtin_amdgcn_sched_barrier(0);
-    consume(c, A);
-    contract();
-    issue(c + 2 * kTokWaves, A);
-    __builtin_amdgcn_sched_barrier(0);
-    if (c + kTokWaves < nch) {
-      consume(c + kTokWaves, B);
-      contract();
-    }
-    issue(c + 3 * kTokWaves, B);
-  }
-
-  // ---- epilogue: waves added in order; LDS-only barriers, so nothing waits
-  // for outstanding global accesses ----
-  auto row8_sum = [](float v) {  // the 8 lanes of a load-layout row
-    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0xB1, 0xF, 0xF, false));   // lane ^ 1
-    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x4E, 0xF, 0xF, false));   // lane ^ 2
-    v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x141, 0xF, 0xF, false));  // 7 - i in 8
-    return v;
-  };
-#pragma unroll
-  for (int k = 0; k < IPC; ++k) {
-    const float v = row8_sum(xx[k]);
-    if (lu == 0) s_xx[wave][8 * k + lr] = v;
-  }
-  for (int r = 8 * IPC + lane; r < kTokRows; r += kWave) s_xx[wave][r] = 0.f;
-#pragma unroll
-  for (int k = 0; k < QI; ++k) {
-    const float v = row8_sum(qq[k]);
-    if (lu == 0) s_qq[wave][8 * k + lr] = v;
-  }
-  // sigma_j of the wave: its accumulator column j = 16 n + r16 summed over the
-  // wave's 64 rows (rows past the tile hold zeros), the four lane groups by
-  // lane swaps
-#pragma unroll
-  for (int n = 0; n < NTG; ++n) {
-    float v = 0.f;
+    f32x4 Sacc[4][NTG];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v += Sacc[i][n][e];
-    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
-    if (lane < 16) s_sig[wave][16 * n + r16] = v;
-  }
-  // wave w's partial S sits in its own region: [row][NQ] floats from &s_xq[w][0][0]
-  static_assert((kTokRows + NQ) * 8 * 16 >= kTokRows * NQ * 4, "partial S fits the wave's region");
-  auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_xq[w][0][0])[r * NQ + j]; };
+      for (int n = 0; n < NTG; ++n) Sacc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float xx[IPC], qq[QI];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int k = 0; k < IPC; ++k) xx[k] = 0.f;
 #pragma unroll
-    for (int n = 0; n < NTG; ++n)
+    for (int k = 0; k < QI; ++k) qq[k] = 0.f;
+    uint32_t one_lo = kBf16OneLo, one_hi = kBf16OneHi;
+    asm volatile("" : "+v"(one_lo), "+v"(one_hi));  // opaque: keeps them out of inline constants
+    float* pool = POOL ? s_pool : f.pool_part + (size_t(t) * f.tiles + tile) * C;
+
+    auto consume = [&](int c, const Slot& d) {
+      // rows to LDS; |x|^2, |q_j|^2 and channel sums from the registers
+      float cs[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) s_part(wave, 16 * i + 4 * grp + e, 16 * n + r16) = Sacc[i][n][e];
-  lds_barrier();  // every sum below reads the waves' partials in wave order
-  if (tid < Q) {
-    float v = 0.f, qv = 0.f;
+      for (int e = 0; e < 8; ++e) cs[e] = 0.f;
 #pragma unroll
-    for (int w = 0; w < kTokWaves; ++w) {
-      v += s_sig[w][tid];
-      qv += s_qq[w][tid];
+      for (int k = 0; k < IPC; ++k) {
+        const int row = 8 * k + lr;
+        const u32x4 v = __builtin_bit_cast(u32x4, d.x[k]);
+        s_xq[wave][row][lu ^ (row & 7)] = v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xx[k] = dot2(v[e], v[e], xx[k]);
+          cs[2 * e] = dot2(v[e], one_lo, cs[2 * e]);
+          cs[2 * e + 1] = dot2(v[e], one_hi, cs[2 * e + 1]);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < QI; ++k) {
+        const int row = 8 * k + lr;
+        const u32x4 v = __builtin_bit_cast(u32x4, d.q[k]);
+        s_xq[wave][kTokRows + row][lu ^ (row & 7)] = v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
+      }
+      // channel sums over the wave's rows: lanes lu, lu + 8, ..., lu + 56 in a fixed order
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float v = cs[e];
+        v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
+        const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+        const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        cs[e] = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+      }
+      const int c0 = c * kTokChunk + 8 * lu;
+      if (sums && lane < 8 && c0 < C) {
+        *reinterpret_cast<f32x4*>(pool + c0) = f32x4{cs[0], cs[1], cs[2], cs[3]};
+        *reinterpret_cast<f32x4*>(pool + c0 + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
+      }
+    };
+    auto contract = [&]() {
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        bf16x8 A[4], B[NTG];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * i + r16;
+          A[i] = __builtin_bit_cast(bf16x8, s_xq[wave][row][(4 * st + grp) ^ (row & 7)]);
+        }
+#pragma unroll
+        for (int n = 0; n < NTG; ++n) {
+          const int row = 16 * n + r16;
+          B[n] = __builtin_bit_cast(bf16x8, s_xq[wave][kTokRows + row][(4 * st + grp) ^ (row & 7)]);
+        }
+#pragma unroll
+        for (int n = 0; n < NTG; ++n)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[i], B[n], Sacc[i][n], 0, 0, 0);
+      }
+    };
+
+    // rows this wave never loads (8 * IPC .. 63) are zero in its buffer
+    for (int u = 8 * IPC * 8 + lane; u < kTokRows * 8; u += kWave) (&s_xq[wave][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
+
+    Slot A, B;
+    issue(wave, A);
+    issue(wave + kTokWaves, B);
+    for (int c = wave; c < nch; c += 2 * kTokWaves) {
+      __builtin_amdgcn_sched_barrier(0);
+      consume(c, A);
+      contract();
+      issue(c + 2 * kTokWaves, A);
+      __builtin_amdgcn_sched_barrier(0);
+      if (c + kTokWaves < nch) {
+        consume(c + kTokWaves, B);
+        contract();
+      }
+      issue(c + 3 * kTokWaves, B);
     }
+
+    // ---- epilogue: waves added in order; LDS-only barriers, so nothing waits
+    // for outstanding global accesses ----
+    auto row8_sum = [](float v) {  // the 8 lanes of a load-layout row
+      v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0xB1, 0xF, 0xF, false));   // lane ^ 1
+      v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x4E, 0xF, 0xF, false));   // lane ^ 2
+      v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x141, 0xF, 0xF, false));  // 7 - i in 8
+      return v;
+    };
+#pragma unroll
+    for (int k = 0; k < IPC; ++k) {
+      const float v = row8_sum(xx[k]);
+      if (lu == 0) s_xx[wave][8 * k + lr] = v;
+    }
+    for (int r = 8 * IPC + lane; r < kTokRows; r += kWave) s_xx[wave][r] = 0.f;
+#pragma unroll
+    for (int k = 0; k < QI; ++k) {
+      const float v = row8_sum(qq[k]);
+      if (lu == 0) s_qq[wave][8 * k + lr] = v;
+    }
+    // sigma_j of the wave: its accumulator column j = 16 n + r16 summed over the
+    // wave's 64 rows (rows past the tile hold zeros), the four lane groups by
+    // lane swaps
+#pragma unroll
+    for (int n = 0; n < NTG; ++n) {
+      float v = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v += Sacc[i][n][e];
+      const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+      v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+      const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+      v = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+      if (lane < 16) s_sig[wave][16 * n + r16] = v;
+    }
+    // wave w's partial S sits in its own region: [row][NQ] floats from &s_xq[w][0][0]
+    static_assert((kTokRows + NQ) * 8 * 16 >= kTokRows * NQ * 4, "partial S fits the wave's region");
+    auto s_part = [&](int w, int r, int j) -> float& { return reinterpret_cast<float*>(&s_xq[w][0][0])[r * NQ + j]; };
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int n = 0; n < NTG; ++n)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s_part(wave, 16 * i + 4 * grp + e, 16 * n + r16) = Sacc[i][n][e];
+    lds_barrier();  // every sum below reads the waves' partials in wave order
+    if (tid < Qh) {
+      float v = 0.f, qv = 0.f;
+#pragma unroll
+      for (int w = 0; w < kTokWaves; ++w) {
+        v += s_sig[w][tid];
+        qv += s_qq[w][tid];
+      }
+      if constexpr (GR) {
+        const int g = tid / f.qg, j = tid - g * f.qg;
+        advance(f.sig_part, g * f.gws)[(size_t(t) * f.tiles + tile) * f.qg + j] = v;
+        if (tile == 0) advance(f.qg_part, g * f.gws)[size_t(t) * f.qg + j] = qv;
+      } else {
+        f.sig_part[(size_t(t) * f.tiles + tile) * Q + qb + tid] = v;
+        if (tile == 0) f.qg_part[size_t(t) * Q + qb + tid] = qv;
+      }
+    }
+    if (tid < NQ) {
+      float qv = 0.f;
+      for (int w = 0; w < kTokWaves; ++w) qv += s_qq[w][tid];
+      s_rq[tid] = qv > 0.f ? 1.0f / sqrtf(qv) : 0.f;
+    }
+    // thread -> row tid / 8, columns CPT * (tid % 8) .. + CPT - 1
+    constexpr int CPT = NQ / 8;
+    const int row = tid >> 3, cg = (tid & 7) * CPT;
+    float sv[CPT], rq[CPT];
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < kTokWaves; ++w) v += s_part(w, row, cg + e);
+      sv[e] = v;
+    }
+    float x2 = 0.f;
+#pragma unroll
+    for (int w = 0; w < kTokWaves; ++w) x2 += s_xx[w][row];
+    lds_barrier();  // 1 / |q_j| in s_rq
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) rq[e] = s_rq[cg + e];
     if constexpr (GR) {
-      const int g = tid / f.qg, j = tid - g * f.qg;
-      advance(f.sig_part, g * f.gws)[(size_t(t) * f.tiles + tile) * f.qg + j] = v;
-      if (tile == 0) advance(f.qg_part, g * f.gws)[size_t(t) * f.qg + j] = qv;
+      // the row's S_nj / |q_j| into LDS (wave 0's region: every read of the
+      // partials is behind the last barrier); thread g of the row's eight takes
+      // the maximum over query g's columns
+      float* s_cos = reinterpret_cast<float*>(&s_xq[0][0][0]);  // [64 rows][NQ]
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) s_cos[row * NQ + cg + e] = sv[e] * rq[e];
+      lds_barrier();
+      const int g = tid & 7;
+      if (g < f.groups && row < TM) {
+        float best = -INFINITY;
+        for (int j = 0; j < f.qg; ++j) best = fmaxf(best, s_cos[row * NQ + g * f.qg + j]);
+        const float xn = sqrtf(x2);
+        advance(f.tok_score, g * f.gws)[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+      }
     } else {
-      f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
-      if (tile == 0) f.qg_part[size_t(t) * Q + tid] = qv;
-    }
-  }
-  if (tid < NQ) {
-    float qv = 0.f;
-    for (int w = 0; w < kTokWaves; ++w) qv += s_qq[w][tid];
-    s_rq[tid] = qv > 0.f ? 1.0f / sqrtf(qv) : 0.f;
-  }
-  // thread -> row tid / 8, columns 4 * (tid % 8) .. + 3 (NTG = 2) or 2 * (tid % 8) .. + 1 (NTG = 1)
-  constexpr int CPT = NQ / 8;
-  const int row = tid >> 3, cg = (tid & 7) * CPT;
-  float sv[CPT], rq[CPT];
-#pragma unroll
-  for (int e = 0; e < CPT; ++e) {
-    float v = 0.f;
-#pragma unroll
-    for (int w = 0; w < kTokWaves; ++w) v += s_part(w, row, cg + e);
-    sv[e] = v;
-  }
-  float x2 = 0.f;
-#pragma unroll
-  for (int w = 0; w < kTokWaves; ++w) x2 += s_xx[w][row];
-  lds_barrier();  // 1 / |q_j| in s_rq
-#pragma unroll
-  for (int e = 0; e < CPT; ++e) rq[e] = s_rq[cg + e];
-  if constexpr (GR) {
-    // the row's S_nj / |q_j| into LDS (wave 0's region: every read of the
-    // partials is behind the last barrier); thread g of the row's eight takes
-    // the maximum over query g's columns
-    float* s_cos = reinterpret_cast<float*>(&s_xq[0][0][0]);  // [64 rows][NQ]
-#pragma unroll
-    for (int e = 0; e < CPT; ++e) s_cos[row * NQ + cg + e] = sv[e] * rq[e];
-    lds_barrier();
-    const int g = tid & 7;
-    if (g < f.groups && row < TM) {
       float best = -INFINITY;
-      for (int j = 0; j < f.qg; ++j) best = fmaxf(best, s_cos[row * NQ + g * f.qg + j]);
-      const float xn = sqrtf(x2);
-      advance(f.tok_score, g * f.gws)[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
-    }
-  } else {
-    float best = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < CPT; ++e)
-      if (cg + e < Q) best = fmaxf(best, sv[e] * rq[e]);
-    best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
-    best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
-    best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
-    if ((tid & 7) == 0 && row < TM) {
-      const float xn = sqrtf(x2);
-      f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+      for (int e = 0; e < CPT; ++e)
+        if (cg + e < Qh) best = fmaxf(best, sv[e] * rq[e]);
+      best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
+      best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
+      best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
+      best_all = fmaxf(best_all, best);
+      if (h == npass - 1 && (tid & 7) == 0 && row < TM) {
+        const float xn = sqrtf(x2);
+        f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best_all / xn : 0.f;
+      }
     }
+    if (h + 1 < npass) lds_barrier();  // the next pass rewrites every wave's region
   }
+
   if (POOL) {
     const __amdgpu_buffer_rsrc_t pres =
         make_rsrc_uniform(f.pool_part + (size_t(t) * f.tiles + tile) * C, uint32_t(C) * 4);
@@ -750,32 +765,35 @@ void launch_mfma(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipS
                      pl.kc, va);
 }
 
-template <int NTG, int IPC, bool GR>
-void launch_tok_gr(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
+template <int NTG, int IPC, int MODE>
+void launch_tok_mode(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
   // with 64 query columns the staging regions leave no room for the gathered channel sums
   if constexpr (NTG <= 2) {
     if (va.v[0].C <= kTokPoolMax) {
-      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true, GR>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true, MODE>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
                          pl.tile_tokens, va);
       return;
     }
   }
-  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false, GR>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false, MODE>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
                      pl.tile_tokens, va);
 }
 template <int NTG, int IPC>
 void launch_tok(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
-  if (va.v[0].groups > 1)
-    launch_tok_gr<NTG, IPC, true>(pl, va, V, s);
-  else
-    launch_tok_gr<NTG, IPC, false>(pl, va, V, s);
+  if (va.v[0].groups > 1) {
+    launch_tok_mode<NTG, IPC, kTokGroups>(pl, va, V, s);
+  } else if (va.v[0].Q > 16 * NTG) {
+    if constexpr (NTG == 2) launch_tok_mode<NTG, IPC, kTokPasses>(pl, va, V, s);
+  } else {
+    launch_tok_mode<NTG, IPC, kTokOne>(pl, va, V, s);
+  }
 }
 
 }  // namespace
 
 RelKind relevance_kind(const wz_config& c) {
   if (c.in_dtype != WZ_BF16) return kRelValu;
-  if (c.Q <= 64) return kRelTok;
+  if (c.Q <= kTokQMax) return kRelTok;
   // two 16-row MFMA tiles per wave, at least 2 waves: frames of at least 49 tokens
   return c.H * c.W >= 49 ? kRelMfma : kRelValu;
 }

@@ -246,6 +246,12 @@ EDGE = {
     "query_64_full_tile": dict(T=3, H=8, W=8, C=136, Q=64, B=40),
     "query_33_single_token": dict(T=5, H=1, W=1, C=72, Q=33, B=3),
     "query_64_max_channels": dict(T=2, H=7, W=7, C=65536, Q=64, B=20),
+    # more than 64 query tokens in the token-tiled pass: passes of 32 columns
+    # over each tile, the last one ragged; up to the most the pass takes
+    "query_65_passes": dict(T=4, H=5, W=9, C=200, Q=65, B=40),
+    "query_128_passes": dict(T=5, H=9, W=9, C=136, Q=128, B=60),
+    "query_256_passes": dict(T=3, H=8, W=8, C=72, Q=256, B=30),
+    "query_100_large_c": dict(T=2, H=7, W=7, C=16384, Q=100, B=20),
 }
 
 
