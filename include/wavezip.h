@@ -177,7 +177,7 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X,
 /* The whole pass C(X, Q) of Eq. (4)/(6): stage 1, 2 and 3 in sequence on one
  * stream, intermediates kept in `ws`.  Three kernel launches: the pass over
  * X, the per-frame scores, and one kernel that computes the budgets (every
- * workgroup alike) and performs stage 3; for T > 256 the budgets get a
+ * workgroup alike) and performs stage 3; for T > 64 the budgets get a
  * launch of their own.  out_tokens [B][C] (cfg->out_dtype) and
  * out_index [B] receive offset[T] rows (= B unless the frame filter leaves
  * fewer than B tokens).  budget [T] and offset [T+1] are optional outputs

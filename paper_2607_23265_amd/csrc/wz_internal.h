@@ -145,7 +145,10 @@ __device__ __forceinline__ void unit_of_block(int b, int tiles, int slices, int&
 }
 
 constexpr int kMaxFrames = 2048;
-constexpr int kFusedTMax = 256;  // frames up to which the budget is folded into the selection kernel
+// frames up to which the budget is folded into the selection kernel (one
+// wave computes it); above, one workgroup of its own computes it once, which
+// costs less than every selection workgroup repeating a workgroup-wide budget
+constexpr int kFusedTMax = 64;
 
 // Workspace carve-up (all offsets 256-byte aligned).
 struct Workspace {

@@ -49,7 +49,7 @@ constexpr int kThreads = 1024;
 constexpr int kNW = kThreads / kWave;
 constexpr int kVecPerLane = 2;  // 16-byte vectors per lane, block row and channel part
 
-enum BudgetSrc : int { kOffsets = 0, kWaveBudget = 1, kBlockBudget = 2 };
+enum BudgetSrc : int { kOffsets = 0, kWaveBudget = 1 };
 
 struct AssignArgs {
   const void* X;            // [T][H][W][C]
@@ -203,12 +203,10 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
       bd = double(f.delta[lane]);
       br = double(f.rel[lane]);
     }
-  } else if constexpr (MODE == kOffsets) {
+  } else {
     o_base = f.offset_in[t];
     o_next = f.offset_in[t + 1];
     o_last = f.offset_in[T];
-  } else {
-    budget_body<kThreads, kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
   }
   // The gated 2x2 Haar round trip of a token, for the channel part in x:
   // the orthonormal butterflies of its block (Eq. (12)), the three detail
@@ -303,12 +301,6 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
     }
     if (lane == 0) s_ext[0] = 0;
   };
-  if constexpr (MODE == kBlockBudget) {
-    if (given) {
-      lds_barrier();  // budgets of budget_body visible to wave 0
-      if (wave == 0) extra_prefix();
-    }
-  }
 
   // read-ahead item of this wave (waves G0.., item wave - G0): its block and
   // gate are read and the row formed while the budgets are computed
@@ -643,8 +635,7 @@ hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* 
     a.tau = c.tau;
   }
   if (offset_in) launch_mode<kOffsets>(c, va, vs.V, s);
-  else if (c.T <= kWave) launch_mode<kWaveBudget>(c, va, vs.V, s);
-  else if (c.T <= kFusedTMax) launch_mode<kBlockBudget>(c, va, vs.V, s);
+  else if (c.T <= kFusedTMax) launch_mode<kWaveBudget>(c, va, vs.V, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
