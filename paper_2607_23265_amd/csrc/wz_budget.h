@@ -270,17 +270,18 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
       for (int i = tid; i < L; i += NT) {
         if (sh.state[i] != kActive) continue;
         const double f = w[i];
+        // branch-free counting, eight loads in flight at a time
         int rank = 0, j = 0;
         for (; j + 8 <= L; j += 8) {
+          double fj[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const double fj = w[j + e];
-            rank += (fj > f) || (fj == f && j + e < i);
-          }
+          for (int e = 0; e < 8; ++e) fj[e] = w[j + e];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) rank += int(fj[e] > f) | (int(fj[e] == f) & int(j + e < i));
         }
         for (; j < L; ++j) {
           const double fj = w[j];
-          rank += (fj > f) || (fj == f && j < i);
+          rank += int(fj > f) | (int(fj == f) & int(j < i));
         }
         if (rank < left) sh.n[i] += 1;
       }
