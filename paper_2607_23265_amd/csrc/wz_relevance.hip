@@ -783,6 +783,7 @@ void launch_tok(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipSt
   if (va.v[0].groups > 1) {
     launch_tok_mode<NTG, IPC, kTokGroups>(pl, va, V, s);
   } else if (va.v[0].Q > 16 * NTG) {
+    // the plan takes two query tiles for passes (checked by the caller)
     if constexpr (NTG == 2) launch_tok_mode<NTG, IPC, kTokPasses>(pl, va, V, s);
   } else {
     launch_tok_mode<NTG, IPC, kTokOne>(pl, va, V, s);
@@ -820,6 +821,8 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
     }
   }
   if (pl.kind == kRelTok) {
+    // columns beyond the query tiles are served by passes of two tiles only
+    if (va.v[0].Q > 16 * pl.ntg && (pl.ntg != 2 || va.v[0].groups > 1)) return hipErrorInvalidValue;
 #define WZ_TOK(NTG)                                 \
   switch (pl.ipc) {                                 \
     case 1: launch_tok<NTG, 1>(pl, va, V, s); break; \
