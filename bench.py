@@ -232,7 +232,7 @@ def main():
         torch.cuda.synchronize()
         q_ms = ev0.elapsed_time(ev1) / args.steps
         queries = {"queries": G, "calls": args.steps, "ms_per_call": q_ms,
-                   "shared_pass": wl.dtype == "bf16" and G * wl.Q <= 64,
+                   "queries_per_pass_over_x": min(G, 64 // wl.Q) if wl.dtype == "bf16" and wl.Q <= 64 else 1,
                    "query_frames_per_s": G * wl.T / (q_ms * 1e-3),
                    "vs_separate_calls": G * ms_step / q_ms}
         del QG, wsq, outq

@@ -207,10 +207,10 @@ wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X,
  * for each of `queries` queries of Q tokens (1 <= queries <= 8, else
  * WZ_ERR_SHAPE) on the same X, each with its own budgets and outputs.  The
  * paper scores every query afresh; here, when the inputs are bf16 and
- * queries * Q <= 64, one pass over X serves every query: the query tokens
- * are the columns of one relevance contraction, and a_{t,n}, r_t and the
- * selection are taken per query.  Otherwise each query takes its own pass
- * over X (launched together, as in wz_condense_batch).  Layouts:
+ * Q <= 32, each pass over X serves a group of up to 64 / Q queries: their
+ * tokens are the columns of one relevance contraction, and a_{t,n}, r_t and
+ * the selection are taken per query.  Otherwise each query takes its own
+ * pass over X (launched together, as in wz_condense_batch).  Layouts:
  * X [T][H][W][C], query [G][Q][C], out_tokens [G][B][C], out_index [G][B],
  * budget [G][T] and offset [G][T+1] (optional, NULL: kept in the
  * workspace).  ws: at least queries * wz_workspace_bytes(cfg) bytes, query g

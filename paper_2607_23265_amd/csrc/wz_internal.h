@@ -210,8 +210,10 @@ struct Videos {
   // sums of problem 0's workspace
   bool shared_x = false;
 };
-// queries of one video whose columns fit one token-tiled pass (64 at most)
-inline bool shared_pass(const wz_config& c, int V) { return relevance_kind(c) == kRelTok && c.Q * V <= 64; }
+// queries of one video that one token-tiled pass serves together (its 64
+// query columns at most); passes over X share them when this is 2 or more
+inline int queries_per_pass(const wz_config& c) { return relevance_kind(c) == kRelTok ? 64 / c.Q : 1; }
+inline bool shared_pass(const wz_config& c, int V) { return V > 1 && queries_per_pass(c) >= 2; }
 template <typename A>
 struct VideoArgs {
   A v[kMaxVideos];

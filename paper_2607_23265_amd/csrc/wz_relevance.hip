@@ -805,13 +805,19 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
   VideoArgs<StreamArgs> va{};
   int V = vs.V;
   if (vs.shared_x && shared_pass(c, vs.V)) {
-    // every query's columns in one pass over X: the per-query plan's tiles,
-    // query tiles for all the columns
-    const int QT = c.Q * vs.V;
+    // queries in groups of up to 64 columns, one pass over X per group (grid
+    // y = group): the per-query plan's tiles, query tiles for a group's columns
+    const int G = std::min(vs.V, queries_per_pass(c));
+    const int QT = c.Q * G;
     pl.ntg = QT <= 16 ? 1 : QT <= 32 ? 2 : 4;
-    va.v[0] = StreamArgs{X, query, ws.s_part, ws.g_part, ws.qg_part, ws.sig_part, ws.pool_part, tok_score,
-                         c.T, c.H * c.W, c.C, QT, qpad(QT), pl.tiles, pl.slices, vs.V, c.Q, vs.ws};
-    V = 1;
+    V = (vs.V + G - 1) / G;
+    for (int e = 0; e < V; ++e) {
+      const int q0 = e * G, n = std::min(G, vs.V - q0);
+      const Workspace w = advance(ws, q0 * vs.ws);
+      va.v[e] = StreamArgs{X, advance(query, q0 * vs.q), w.s_part, w.g_part, w.qg_part, w.sig_part, w.pool_part,
+                           advance(tok_score, q0 * vs.ws), c.T, c.H * c.W, c.C, c.Q * n, qpad(c.Q * n), pl.tiles,
+                           pl.slices, n, c.Q, vs.ws};
+    }
   } else {
     for (int v = 0; v < vs.V; ++v) {
       const Workspace w = advance(ws, v * vs.ws);

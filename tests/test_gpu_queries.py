@@ -2,7 +2,8 @@
 query's outputs must be bitwise those of wz_condense with that query alone,
 and (at the parity bar) the oracle's.  Covers the shared pass over X (bf16,
 queries x Q <= 64: query columns split across 16-column MFMA tiles, a query
-boundary inside a tile) and the separate passes otherwise.  Marked gpu."""
+boundary inside a tile; groups of queries sharing several passes, the last
+group smaller) and the separate passes otherwise.  Marked gpu."""
 import numpy as np
 import pytest
 import torch
@@ -53,7 +54,10 @@ def _case(name):
 @pytest.mark.parametrize("name,n,out_dtype", [("t64_14x14_c3584", 2, wz.WZ_BF16), ("t32_14x14_c3584", 4, wz.WZ_F32),
                                               ("odd_3x5", 3, wz.WZ_F32), ("q20_x3", 3, wz.WZ_F32),
                                               ("small_query_bf16", 8, wz.WZ_BF16), ("q40_x2", 2, wz.WZ_F32),
-                                              ("tiny", 3, wz.WZ_F32), ("t128_13x13_c3584", 2, wz.WZ_F32)])
+                                              ("tiny", 3, wz.WZ_F32), ("t128_13x13_c3584", 2, wz.WZ_F32),
+                                              # several passes over X, each shared by a group of queries
+                                              ("t64_14x14_c3584", 4, wz.WZ_BF16), ("odd_3x5", 5, wz.WZ_F32),
+                                              ("q20_x3", 5, wz.WZ_F32)])
 def test_condense_queries_matches_single(name, n, out_dtype):
     wl, inp, out = _case(name)
     p = wz.problem_of(wl, out_dtype)
