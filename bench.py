@@ -8,10 +8,18 @@ B=1254, 2 temporal levels).  Inputs are resident in HBM before timing; the
 call cycles through enough separate copies of the input (>= 512 MB in all)
 that the 256 MB Infinity Cache cannot serve a repeated frame tensor.
 
+The K timed steps run as R back-to-back groups (default 5) with a HIP event
+between groups and no synchronisation inside; `ms_per_step` is the median
+group's time per step, `ms_per_step_groups` lists every group.
+
 Prints one JSON line: frames condensed per second (value), tokens/s, the
 algorithmic HBM rate of the whole call, the roofline of the dominant kernel
-(the relevance pass, timed with HIP events on its stream), the CPU oracle's
-rate on the host as a reported baseline, (`interp`) the rate with the
+(the relevance pass, timed with HIP events on its stream, with the HBM bytes
+and MFMA busy share that rocprofv3 counters recorded for the same sources),
+the rate of a plain read of the frame tensor on the same device
+(`read_ceiling`, the achievable streaming rate beside the 8 TB/s peak), the
+CPU oracle's rate on the host (all cores and one thread) as a reported
+baseline, (`interp`) the rate with the
 budget-guided interpolation forming the tokens instead of selection,
 (`spatial_levels_2`) the rate with the two-level spatial modulator, and
 (`batched`) the rate of wz_condense_batch on several videos of the same
@@ -42,12 +50,16 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="t64_14x14_c3584")
     ap.add_argument("--out-dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="timed groups the K steps are split into (median reported)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle (0 disables)")
     ap.add_argument("--videos", type=int, default=4,
                     help="also time wz_condense_batch on this many videos of the workload per call (0 disables)")
     ap.add_argument("--queries", type=int, default=2,
                     help="also time wz_condense_queries with this many queries per video per call (0 disables)")
+    ap.add_argument("--read-calib", type=int, default=0,
+                    help="only run this many plain reads of the frame tensor (the read ceiling) and exit")
     ap.add_argument("--copy-calib", type=int, default=0,
                     help="only run this many plain device copies of a frame tensor (the known-size kernel that "
                          "scales HBM byte counters) and exit")
@@ -73,17 +85,19 @@ def kernel_sources_sha256():
     return h.hexdigest()
 
 
-def recorded_traffic(workload):
-    """HBM bytes per launch of the relevance pass measured with rocprofv3 byte counters (profiles/), or
-    None when there is no record for the workload or the kernels changed since it was taken."""
-    path = os.path.join(HERE, "profiles", f"relevance_pass_traffic_{workload}.json")
+def recorded_counters(workload):
+    """rocprofv3 counter figures of the relevance pass for the workload (profiles/), or None when there is
+    no record or the kernel sources changed since it was taken: HBM bytes per launch (FETCH_SIZE and
+    WRITE_SIZE, scaled by a plain device copy) and the MFMA busy share (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE times the SIMD count)."""
+    path = os.path.join(HERE, "profiles", f"relevance_pass_counters_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         rec = json.load(fh)
     if rec.get("kernel_sources_sha256") != kernel_sources_sha256():
         return None
-    return rec["traffic_bytes_per_launch"]
+    return rec
 
 
 def relevance_bytes(wl):
@@ -93,26 +107,73 @@ def relevance_bytes(wl):
     return wl.T * wl.N * wl.C * s_in + wl.Q * wl.C * s_in + 4 * wl.T * wl.N
 
 
-def cpu_baseline(inp, wl, seconds):
-    """Time the CPU oracle (as written) on whole passes over the same input until ~`seconds` elapse."""
-    import numpy as np  # noqa: F401
-    import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:  # noqa: BLE001
-        threads = len(os.sched_getaffinity(0))
-    X, q = inp.X_f64(), inp.query_f64()
+def _time_oracle(oracle, X, q, wl, seconds):
+    """Whole oracle passes over the same input until ~`seconds` elapse; returns seconds per pass."""
     calls, t0 = 0, time.perf_counter()
     while True:
         oracle.condense(X, q, wl.B, wl.levels, wl.lam, wl.tau)
         calls += 1
         el = time.perf_counter() - t0
         if el >= seconds:
-            break
-    return {"value": wl.T * calls / el, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{calls} full passes of the float64 NumPy oracle over the same {wl.name} input "
-                      f"({wl.T} frames each), {el:.1f} s"}
+            return el / calls, calls
+
+
+def cpu_baseline(inp, wl, seconds):
+    """Time the CPU oracle (as written) on whole passes over the same input: three timed runs on all the
+    host's BLAS threads (median reported) and one run on a single thread, ~`seconds` of CPU time in all."""
+    import numpy as np  # noqa: F401
+    import oracle
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    X, q = inp.X_f64(), inp.query_f64()
+    runs = [_time_oracle(oracle, X, q, wl, seconds / 4) for _ in range(3)]
+    per_pass = sorted(r[0] for r in runs)[1]
+    with threadpool_limits(limits=1):
+        one, one_calls = _time_oracle(oracle, X, q, wl, seconds / 4)
+    return {"value": wl.T / per_pass, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
+            "single_thread": {"value": wl.T / one, "unit": "frames/s", "cores": 1, "passes": one_calls},
+            "sample": f"median of 3 timed runs of whole passes of the float64 NumPy oracle over the same {wl.name} "
+                      f"input ({wl.T} frames each; {sum(r[1] for r in runs)} passes, "
+                      f"{sum(r[0] * r[1] for r in runs):.1f} s) on {threads} BLAS threads, and "
+                      f"{one_calls} passes on one thread"}
+
+
+def timed_groups(stream, fn, steps, groups):
+    """Run fn(i) for i < steps as `groups` back-to-back groups on `stream`, a HIP event between groups and
+    no synchronisation inside; returns (median ms per call over the groups, per-group ms per call)."""
+    import torch
+    groups = max(1, min(groups, steps))
+    sizes = [steps // groups + (1 if g < steps % groups else 0) for g in range(groups)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(groups + 1)]
+    ev[0].record(stream)
+    i = 0
+    for g, n in enumerate(sizes):
+        for _ in range(n):
+            fn(i)
+            i += 1
+        ev[g + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[g].elapsed_time(ev[g + 1]) / sizes[g] for g in range(groups)]
+    return sorted(per)[(groups - 1) // 2], per
+
+
+def read_ceiling(Xs, stream, steps):
+    """Plain read of the frame tensor: a device-wide sum of its 32-bit words, cycling through the input
+    copies; returns (us per read, GB/s)."""
+    import torch
+    n = len(Xs)
+    views = [x.view(torch.float32).view(-1) for x in Xs]
+    out = torch.empty((), dtype=torch.float32, device=Xs[0].device)
+    for i in range(8):
+        torch.sum(views[i % n], dim=0, out=out)
+    ms, _ = timed_groups(stream, lambda i: torch.sum(views[i % n], dim=0, out=out), steps, 5)
+    nbytes = Xs[0].numel() * Xs[0].element_size()
+    return ms * 1e3, nbytes / (ms * 1e-3) / 1e9
+
+
+def stream_of(dev):
+    import torch
+    return torch.cuda.current_stream(dev)
 
 
 def main():
@@ -135,6 +196,11 @@ def main():
     nsets = max(1, math.ceil(2 * MALL_BYTES / X0.numel() / X0.element_size()))
     Xs = [X0] + [X0.clone() for _ in range(nsets - 1)]
     qs = [q0] + [q0.clone() for _ in range(nsets - 1)]
+    if args.read_calib:
+        us, gbps = read_ceiling(Xs, stream_of(dev), args.read_calib)
+        print(json.dumps({"calibration": "plain read", "bytes_read": X0.numel() * X0.element_size(),
+                          "us_per_read": us, "gbps": gbps, "reads": args.read_calib}), flush=True)
+        return
     if args.copy_calib:
         dst = [torch.empty_like(X0) for _ in range(2)]
         for i in range(args.copy_calib):
@@ -147,18 +213,15 @@ def main():
     out = wz._out_tokens(p, dev)
     stream = torch.cuda.current_stream(dev)
 
+    def step(i):
+        wz.condense(p, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
+
     for i in range(args.warmup):
-        wz.condense(p, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
+        step(i)
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for i in range(args.steps):
-        wz.condense(p, Xs[i % nsets], qs[i % nsets], ws=ws, out=out)
-    ev1.record(stream)
-    torch.cuda.synchronize()
+    ms_step, ms_groups = timed_groups(stream, step, args.steps, args.repeats)
     wall = time.perf_counter() - t0
-    ms_step = ev0.elapsed_time(ev1) / args.steps
 
     # dominant kernel: the relevance pass over X (k_relevance_tok), launched alone through
     # wz_relevance_pass, back to back on the same stream
@@ -177,14 +240,11 @@ def main():
     for i in range(args.warmup):
         rel(i)
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for i in range(args.steps):
-        rel(i)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    k1_ms = ev0.elapsed_time(ev1) / args.steps
+    k1_ms, k1_groups = timed_groups(stream, rel, args.steps, args.repeats)
     k1_bytes = relevance_bytes(wl)
     k1_gbps = k1_bytes / (k1_ms * 1e-3) / 1e9
+    rc_us, rc_gbps = read_ceiling(Xs, stream, args.steps)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     batched = None
     if args.videos > 1:
@@ -265,6 +325,7 @@ def main():
 
     out_bytes = 2 if out_dtype == wz.WZ_BF16 else 4
     call_bytes = algorithmic_bytes(wl, out_bytes)
+    counters = recorded_counters(wl.name)
     frames_s = wl.T / (ms_step * 1e-3)
     line = {
         "metric": METRIC,
@@ -287,11 +348,16 @@ def main():
         "hbm_frac": call_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "bytes_per_step": call_bytes,
         "wall_s": wall,
+        "ms_per_step_groups": ms_groups,
         "roofline": {"kernel": "k_relevance_tok (wz_relevance_pass: the one pass over the frames)",
                      "bound": "hbm", "achieved": k1_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": k1_gbps / HBM_PEAK_GBPS,
-                     "traffic": recorded_traffic(wl.name), "bytes_per_launch": k1_bytes,
-                     "us_per_launch": k1_ms * 1e3},
+                     "traffic": counters["traffic_bytes_per_launch"] if counters else None,
+                     "mfma_busy": counters["mfma_busy_frac"] if counters else None,
+                     "bytes_per_launch": k1_bytes, "us_per_launch": k1_ms * 1e3,
+                     "us_per_launch_groups": [m * 1e3 for m in k1_groups]},
+        "read_ceiling": {"what": "torch.sum over the frame tensor's 32-bit words (a plain streaming read)",
+                         "us": rc_us, "gbps": rc_gbps, "frac_of_peak": rc_gbps / HBM_PEAK_GBPS},
     }
     line["interp"] = interp
     line["spatial_levels_2"] = levels2

@@ -11,7 +11,8 @@
  *                           visual change delta_t (Sec. 3.2.1, Eq. (8));
  *   wz_temporal_budget      gate gamma, frame filter, gated temporal Haar DWT
  *                           and its inverse, and integer budgets
- *                           (Sec. 3.2.2, Eq. (9)-(11), Eq. (16) with Eq. (5));
+ *                           (Sec. 3.2.2-3.2.3, Eq. (9)-(11); Sec. 3.2.4,
+ *                           Eq. (16) with Eq. (5));
  *   wz_spatial_dwt_condense saliency map, per-frame selection and the
  *                           saliency-gated 2-D Haar modulation, compacted in
  *                           temporal order (Eq. (7), Eq. (12)-(15), Eq. (19));
@@ -129,7 +130,7 @@ wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
 /* The pass over X that stage 1 starts with -- the one kernel of the whole
  * pass that reads the frames -- on its own.  It writes the per-token scores
  * a_{t,n} to tok_score [T*H*W] where one workgroup sees every channel of a
- * token (always for bf16 inputs with at most 32 query tokens and for fp32
+ * token (always for bf16 inputs with at most 256 query tokens and for fp32
  * inputs; for bf16 with more query tokens, when the grid has no channel
  * slices), and leaves in ws the per-work-unit partial sums that
  * wz_relevance's per-frame step completes r_t, delta_t (and, with channel
@@ -140,8 +141,8 @@ wz_status wz_relevance(const wz_config* cfg, const void* X, const void* query,
 wz_status wz_relevance_pass(const wz_config* cfg, const void* X, const void* query,
                             float* tok_score, void* ws, size_t ws_bytes, void* stream);
 
-/* Stage 2 -- Wavelet Temporal Allocator and budget (Sec. 3.2.2; Eq. (9)-(11);
- * Eq. (16) under Eq. (5)).  From r and delta (as produced by wz_relevance):
+/* Stage 2 -- Wavelet Temporal Allocator and budget (gate and frame filter of
+ * Sec. 3.2.2; Sec. 3.2.3, Eq. (9)-(11); Sec. 3.2.4, Eq. (16) under Eq. (5)).  From r and delta (as produced by wz_relevance):
  * gamma = min-max(delta) over all T frames; retained set M = {0} U
  * {t : delta_t >= tau}; J-level orthonormal Haar DWT of r over M with every
  * detail level multiplied by gamma pair-averaged to its resolution; inverse

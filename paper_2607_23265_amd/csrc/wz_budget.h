@@ -1,5 +1,6 @@
-// Integer frame budgets of the Wavelet Temporal Allocator (Sec. 3.2.2 gate
-// and frame filter, Eq. (9)-(11)) under Eq. (16) and Eq. (5), as device code
+// Integer frame budgets of the Wavelet Temporal Allocator (gate and frame
+// filter of Sec. 3.2.2; Sec. 3.2.3, Eq. (9)-(11)) under Eq. (16) and Eq. (5)
+// (Sec. 3.2.4), as device code
 // run by ONE workgroup (or one wave) from r_t and delta_t.  Included by the
 // standalone budget kernel and by the fused selection and gather kernel.
 //

@@ -57,8 +57,9 @@ constexpr int kTokMax = 4096;     // validated bound on tokens per frame
 inline int qpad(int Q) { return (Q + 3) & ~3; }
 
 // Streaming kernels of the relevance pass, chosen by shape:
-//   kRelTok  bf16, Q <= 64: token tiles with every channel, LDS-transposed MFMA;
-//   kRelMfma bf16, Q > 64, frames of >= 49 tokens: MFMA-layout loads;
+//   kRelTok  bf16, Q <= 256: token tiles with every channel, LDS-transposed
+//            MFMA (above 64 query tokens, passes of 32 columns per tile);
+//   kRelMfma bf16, Q > 256, frames of >= 49 tokens: MFMA-layout loads;
 //   kRelValu everything else (fp32 inputs, small frames with many queries).
 enum RelKind { kRelValu = 0, kRelMfma = 1, kRelTok = 2 };
 RelKind relevance_kind(const wz_config& c);

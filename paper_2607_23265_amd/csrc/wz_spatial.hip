@@ -7,7 +7,8 @@
 // bit and no kernel boundary separates the budget from its use.
 //
 // Workgroup (t, p), p < P, 1024 threads, works on frame t:
-//   A. wave 0 computes the budgets (T <= 64; all waves up to T = 256) while
+//   A. wave 0 computes the budgets (T <= 64; above, they come from the budget
+//      kernel launched before this one) while
 //      the other waves take the frame's selection ranks and block gates
 //      (from the per-frame kernel, or formed here from the scores when the
 //      stage runs on its own, wz_rank.h) and form the rows of the first
@@ -20,7 +21,7 @@
 //      higher rank of ALL frames are then shared out evenly over all
 //      workgroups (every workgroup knows every budget), so frames with large
 //      budgets do not leave a few CUs working alone.  With the offsets given
-//      (T > 256, or the stage on its own) each workgroup emits its frame's
+//      (T > 64, or the stage on its own) each workgroup emits its frame's
 //      kept tokens of rank p, p + P, ... instead, the next part's block reads
 //      in flight while one is finished.  A token's row is its 2x2 Haar block
 //      (the last row / column repeated when H or W is odd) through the

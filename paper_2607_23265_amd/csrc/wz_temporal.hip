@@ -1,6 +1,6 @@
-// Stage 2 on its own: the Wavelet Temporal Allocator (Sec. 3.2.2 gate and
-// frame filter, Eq. (9)-(11)) and the integer frame budgets (Eq. (16) under
-// Eq. (5)) in ONE workgroup: one wave when T <= 64, 256 threads up to
+// Stage 2 on its own: the Wavelet Temporal Allocator (gate and frame
+// filter of Sec. 3.2.2; Sec. 3.2.3, Eq. (9)-(11)) and the integer frame budgets (Sec. 3.2.4, Eq. (16)
+// under Eq. (5)) in ONE workgroup: one wave when T <= 64, 256 threads up to
 // T = 256, 1024 beyond.  The arithmetic lives in wz_budget.h, which the fused
 // selection and gather kernel runs too.
 #include "wz_budget.h"

@@ -2,8 +2,8 @@
 
 Each mutation replaces one oracle function by a copy with a plausible slip (a
 dropped term, a wrong sign or index, a swapped operand).  The pins of
-pins.py are then run; the test passes when some pin fails.  Everything runs on
-the CPU.
+pins.py are then run; the test passes when some pin fails an assertion (a pin
+that merely crashes on the mutant does not count).  Everything runs on the CPU.
 """
 import numpy as np
 import pytest
@@ -75,11 +75,21 @@ def _bands_swapped(F):
     return LL, HL, LH, HH
 
 
-def _wsm_gate_all(F, Mhw, lam):
-    H, Wd = Mhw.shape
-    LL, LH, HL, HH = W.haar_analysis_2d(F)
-    G = (lam * W.block_average(Mhw))[:, :, None]
-    return W.haar_synthesis_2d(G * LL, G * LH, G * HL, G * HH, H, Wd)
+def _wsm_gate_all(F, Mhw, lam, levels=1):
+    # the approximation band gated too, at every level
+    LL = np.asarray(F, dtype=np.float64)
+    M = np.asarray(Mhw, dtype=np.float64)
+    shapes, gated = [], []
+    for _ in range(levels):
+        shapes.append(LL.shape[:2])
+        LL, LH, HL, HH = W.haar_analysis_2d(LL)
+        M = W.block_average(M)
+        G = (lam * M)[:, :, None]
+        LL = G * LL
+        gated.append((G * LH, G * HL, G * HH))
+    for (h, w), (LH, HL, HH) in zip(reversed(shapes), reversed(gated)):
+        LL = W.haar_synthesis_2d(LL, LH, HL, HH, h, w)
+    return LL
 
 
 def _block_max(Mhw):
@@ -133,15 +143,18 @@ def _grid_swap(n, H, Wd):
 
 
 def _wsm_level2_unpooled_gate(F, Mhw, lam, levels=1):
-    # level 2 gated by the level-1 gate (the saliency map pooled only once)
-    H, W = Mhw.shape
+    # level 2 gated by the level-1 gate subsampled (every other entry) instead
+    # of the saliency map pooled a second time
     LL = np.asarray(F, dtype=np.float64)
-    M1 = W.block_average(Mhw)
+    M = W.block_average(Mhw)
     shapes, gated = [], []
     for j in range(levels):
         shapes.append(LL.shape[:2])
         LL, LH, HL, HH = W.haar_analysis_2d(LL)
-        G = (lam * (M1 if j == 0 else W.block_average(M1) * 0 + M1[:LL.shape[0], :LL.shape[1]]))[:, :, None]
+        if j > 0:
+            Me = W._extend_even(W._extend_even(M, 0), 1)
+            M = Me[0::2, 0::2]
+        G = (lam * M)[:, :, None]
         gated.append((G * LH, G * HL, G * HH))
     for (h, w), (LH, HL, HH) in zip(reversed(shapes), reversed(gated)):
         LL = W.haar_synthesis_2d(LL, LH, HL, HH, h, w)
@@ -187,10 +200,13 @@ def test_mutation_is_caught(name, monkeypatch):
     monkeypatch.setattr(W, attr, fn)
     if hasattr(oracle, attr):
         monkeypatch.setattr(oracle, attr, fn)
-    caught = []
+    caught, crashed = [], []
     for pin in pins.ALL_PINS:
         try:
             pin()
-        except Exception as e:  # noqa: BLE001 - any failure means the pin noticed
-            caught.append((pin.__name__, type(e).__name__))
-    assert caught, f"planted mistake {name!r} in {attr} went unnoticed by every pin"
+        except AssertionError:
+            caught.append(pin.__name__)
+        except Exception as e:  # noqa: BLE001 - a crash is not a caught mistake
+            crashed.append((pin.__name__, f"{type(e).__name__}: {e}"))
+    # only a failed assertion counts: a mutant that merely crashes a pin proves nothing
+    assert caught, f"planted mistake {name!r} in {attr} went unnoticed by every pin (crashes: {crashed})"
