@@ -65,7 +65,9 @@ typedef enum {
   WZ_ERR_PARAM = 5,      /* levels, lambda or tau out of range                */
   WZ_ERR_BUDGET = 6,     /* B < 0 or B > T*H*W                                */
   WZ_ERR_WORKSPACE = 7,  /* workspace smaller than wz_workspace_bytes()       */
-  WZ_ERR_DEVICE = 8      /* a HIP call or kernel launch failed                */
+  WZ_ERR_DEVICE = 8,     /* a HIP call or kernel launch failed                */
+  WZ_ERR_SCRATCH = 9     /* wz_condense_noalloc: the problem needs more than
+                            wz_noalloc_scratch_bytes() of scratch             */
 } wz_status;
 
 typedef enum { WZ_F32 = 0, WZ_BF16 = 1 } wz_dtype;
@@ -222,6 +224,27 @@ wz_status wz_condense_queries(const wz_config* cfg, int32_t queries,
                               void* out_tokens, int32_t* out_index,
                               int32_t* budget, int32_t* offset, void* ws,
                               size_t ws_bytes, void* stream);
+
+/* wz_condense without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, outputs and results as wz_condense
+ * (bitwise), minus ws / ws_bytes: the intermediates live in a static device
+ * array of wz_noalloc_scratch_bytes() = 32 MiB that the library holds on each
+ * GPU it runs on until the process ends.  A problem whose
+ * wz_workspace_bytes(cfg) exceeds that returns WZ_ERR_SCRATCH before anything
+ * is enqueued.  The call allocates and frees nothing; its first call on a
+ * device looks up that device's array (hipGetSymbolAddress) under a lock.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU
+ * (other streams, other host threads) race and must be serialised by the
+ * caller.  Nothing in the array needs clearing between calls (every value is
+ * written before it is read in the same call).                              */
+wz_status wz_condense_noalloc(const wz_config* cfg, const void* X,
+                              const void* query, void* out_tokens,
+                              int32_t* out_index, int32_t* budget,
+                              int32_t* offset, void* stream);
+
+/* Bytes of the static scratch array behind wz_condense_noalloc (32 MiB).     */
+size_t wz_noalloc_scratch_bytes(void);
 
 /* Static, human-readable name of a status code.                               */
 const char* wz_status_str(wz_status s);

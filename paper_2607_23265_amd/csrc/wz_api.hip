@@ -2,10 +2,43 @@
 // the launch sequence.  Declarations and contracts are in include/wavezip.h.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "wz_internal.h"
 
 using namespace wz;
+
+namespace {
+
+// Scratch for wz_condense_noalloc: a file-scope device array in place of a
+// caller's workspace.  Every GPU the library runs on holds its own copy for
+// the life of the process.  Host code never uses the array's name as an
+// address (on the host it is only a stand-in for the symbol): the device
+// address comes from hipGetSymbolAddress, once per device, with that device
+// current.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+__device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (looked up on the
+// first call on that device).
+wz_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return WZ_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return WZ_ERR_DEVICE;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return WZ_OK;
+}
+
+}  // namespace
 
 namespace {
 
@@ -109,6 +142,8 @@ const char* wz_status_str(wz_status s) {
     case WZ_ERR_BUDGET: return "WZ_ERR_BUDGET: B must satisfy 0 <= B <= T*H*W";
     case WZ_ERR_WORKSPACE: return "WZ_ERR_WORKSPACE: workspace too small or misaligned";
     case WZ_ERR_DEVICE: return "WZ_ERR_DEVICE: a HIP call or kernel launch failed";
+    case WZ_ERR_SCRATCH:
+      return "WZ_ERR_SCRATCH: the problem needs more scratch than wz_condense_noalloc's 32 MiB (use wz_condense)";
   }
   return "unknown wz_status";
 }
@@ -171,6 +206,18 @@ wz_status wz_condense(const wz_config* cfg, const void* X, const void* query, vo
                       int32_t* out_index, int32_t* budget, int32_t* offset, void* ws, size_t ws_bytes,
                       void* stream) {
   return condense_videos(cfg, 1, false, X, query, out_tokens, out_index, budget, offset, ws, ws_bytes, stream);
+}
+
+size_t wz_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+wz_status wz_condense_noalloc(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
+                              int32_t* out_index, int32_t* budget, int32_t* offset, void* stream) {
+  WZ_TRY(check_config(cfg));
+  const size_t need = workspace_layout(*cfg, nullptr).bytes;
+  if (need > kScratchBytes) return WZ_ERR_SCRATCH;
+  void* ws = nullptr;
+  WZ_TRY(scratch_of_current_device(&ws));
+  return condense_videos(cfg, 1, false, X, query, out_tokens, out_index, budget, offset, ws, kScratchBytes, stream);
 }
 
 wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X, const void* query,

@@ -18,10 +18,11 @@ LIB_PATH = os.path.join(_HERE, "libwavezip.so")
 WZ_F32, WZ_BF16 = 0, 1
 WZ_SELECT, WZ_INTERP = 0, 1
 _STATUS = {0: "WZ_OK", 1: "WZ_ERR_NULL", 2: "WZ_ERR_ALIGN", 3: "WZ_ERR_SHAPE", 4: "WZ_ERR_DTYPE",
-           5: "WZ_ERR_PARAM", 6: "WZ_ERR_BUDGET", 7: "WZ_ERR_WORKSPACE", 8: "WZ_ERR_DEVICE"}
+           5: "WZ_ERR_PARAM", 6: "WZ_ERR_BUDGET", 7: "WZ_ERR_WORKSPACE", 8: "WZ_ERR_DEVICE",
+           9: "WZ_ERR_SCRATCH"}
 EXPORTS = ("wz_workspace_bytes", "wz_relevance", "wz_relevance_pass", "wz_temporal_budget",
            "wz_spatial_dwt_condense", "wz_condense", "wz_condense_batch", "wz_condense_queries",
-           "wz_status_str")
+           "wz_condense_noalloc", "wz_noalloc_scratch_bytes", "wz_status_str")
 
 
 class WZError(RuntimeError):
@@ -61,8 +62,11 @@ def lib():
     L.wz_temporal_budget.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_spatial_dwt_condense.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_condense.argtypes = [cfgp, P, P, P, P, P, P, P, S, P]
+    L.wz_condense_noalloc.argtypes = [cfgp, P, P, P, P, P, P, P]
+    L.wz_noalloc_scratch_bytes.argtypes = []
+    L.wz_noalloc_scratch_bytes.restype = S
     for f in ("wz_relevance", "wz_relevance_pass", "wz_temporal_budget", "wz_spatial_dwt_condense", "wz_condense",
-              "wz_condense_batch", "wz_condense_queries"):
+              "wz_condense_batch", "wz_condense_queries", "wz_condense_noalloc"):
         getattr(L, f).restype = ctypes.c_int
     L.wz_status_str.argtypes = [ctypes.c_int]
     L.wz_status_str.restype = ctypes.c_char_p
@@ -190,6 +194,19 @@ def condense(p: Problem, X, query, ws=None, out=None):
     cfg = p.config()
     _check(lib().wz_condense(ctypes.byref(cfg), _ptr(X), _ptr(query), _ptr(tok), _ptr(idx), _ptr(b), _ptr(o),
                              _ptr(ws), ws.numel(), _stream(dev)), "wz_condense")
+    return tok, idx, b, o
+
+
+def condense_noalloc(p: Problem, X, query, out=None):
+    """wz_condense_noalloc (no workspace: the library's static scratch) -> (tokens, index, budget, offset)."""
+    _require_device(X, query)
+    dev = X.device
+    tok, idx = _out_tokens(p, dev) if out is None else out
+    b = torch.empty(p.T, dtype=torch.int32, device=dev)
+    o = torch.empty(p.T + 1, dtype=torch.int32, device=dev)
+    cfg = p.config()
+    _check(lib().wz_condense_noalloc(ctypes.byref(cfg), _ptr(X), _ptr(query), _ptr(tok), _ptr(idx), _ptr(b), _ptr(o),
+                                     _stream(dev)), "wz_condense_noalloc")
     return tok, idx, b, o
 
 
