@@ -21,6 +21,11 @@ Points where the paper is silent or ambiguous follow these readings:
     per decomposition level; J temporal levels gate every detail level;
   * odd-length signals are extended by repeating the last sample before every
     Haar step (half-point symmetric extension), and cropped after synthesis;
+  * db4 and bior4.4 (the paper's spatial default and its basis ablation) use
+    the filter-bank conventions stated above `filter_bank`: half-sample
+    symmetric extension, floor((L + F - 1) / 2) coefficients a level, outputs
+    cropped; the gate is pooled to a subband's length by adaptive average
+    pooling (bins floor(i L / n) .. ceil((i + 1) L / n) - 1);
   * the orthonormal Haar filters are used in 1-D and, separably, in 2-D; the
     2-D transform is the single-level Haar version of Eq. (12)-(15); the
     multi-level variant (spatial_levels > 1) gates level j's details by the
@@ -318,6 +323,200 @@ def wavelet_spatial_modulator(F, Mhw, lam, levels=1):
 
 
 # ---------------------------------------------------------------------------
+# Wavelet bases beyond Haar: db4 (the paper's spatial default, Sec. 3.2.3 and
+# Sec. 4.1) and bior4.4 (the basis ablation of Sec. 4.3)
+# ---------------------------------------------------------------------------
+# A filter bank is (dec_lo, dec_hi, rec_lo, rec_hi), all of one even length F.
+# One analysis step of a signal x of length L gives n = floor((L + F - 1) / 2)
+# coefficients per band,
+#     a[k] = sum_j dec_lo[j] x~[2k + 1 - j],   d[k] = sum_j dec_hi[j] x~[2k + 1 - j],
+# x~ the half-sample symmetric extension of x (x~[-1-i] = x[i],
+# x~[L+i] = x[L-1-i], repeated with period 2L).  Synthesis rebuilds
+#     x[i] = sum_k rec_lo[i + F - 2 - 2k] a[k] + rec_hi[i + F - 2 - 2k] d[k]
+# (terms with the filter index outside [0, F) dropped) for i < 2n - F + 2,
+# which is L or L + 1 and is cropped to L.  For Haar this is the step above
+# (d[k] = (x[2k] - x[2k+1]) / sqrt 2, an odd length repeating its last sample).
+# The high-pass filters follow from the low-pass ones:
+#     rec_hi[k] = (-1)^k dec_lo[k],   dec_hi[k] = -(-1)^k rec_lo[k].
+
+def daubechies_lowpass(N):
+    """Daubechies' minimum-phase low-pass filter with N vanishing moments (2N taps, sum sqrt 2).
+
+    Its squared frequency response is cos^2N(w/2) P(sin^2(w/2)) with
+    P(y) = sum_{k<N} C(N-1+k, k) y^k; each root y of P gives the pair of zeros
+    z, 1/z of z^2 - (2 - 4y) z + 1, and the one inside the unit circle is kept.
+    Taps in the order h_0, h_1, ... of the published tables.
+    """
+    from math import comb
+    roots_y = np.roots([comb(N - 1 + k, k) for k in range(N)][::-1])
+    poly = np.array([1.0 + 0j])
+    for _ in range(N):
+        poly = np.convolve(poly, [1.0, 1.0])
+    for y in roots_y:
+        pair = np.roots([1.0, -(2.0 - 4.0 * y), 1.0])
+        poly = np.convolve(poly, [1.0, -pair[np.argmin(np.abs(pair))]])
+    h = np.real(poly)
+    return h * np.sqrt(2.0) / h.sum()
+
+
+def cdf_lowpasses():
+    """The Cohen-Daubechies-Feauveau 9/7 pair behind bior4.4: (analysis 9 taps, synthesis 7 taps).
+
+    The same polynomial P(y) with N = 4 splits between the two filters: the
+    complex pair of roots (four zeros) goes with (1 + z)^4 into the analysis
+    low-pass, the real root (two zeros) with (1 + z)^4 into the synthesis
+    low-pass; both symmetric, each normalised to sum sqrt 2.
+    """
+    from math import comb
+    roots_y = np.roots([comb(3 + k, k) for k in range(4)][::-1])
+    ana, syn = np.array([1.0 + 0j]), np.array([1.0 + 0j])
+    for _ in range(4):
+        ana, syn = np.convolve(ana, [1.0, 1.0]), np.convolve(syn, [1.0, 1.0])
+    for y in roots_y:
+        quad = [1.0, -(2.0 - 4.0 * y), 1.0]
+        if abs(y.imag) > 1e-12:
+            ana = np.convolve(ana, quad)
+        else:
+            syn = np.convolve(syn, quad)
+    ana, syn = np.real(ana), np.real(syn)
+    return ana * np.sqrt(2.0) / ana.sum(), syn * np.sqrt(2.0) / syn.sum()
+
+
+def filter_bank(basis):
+    """(dec_lo, dec_hi, rec_lo, rec_hi) of "haar", "db4" or "bior4.4" (conventions above)."""
+    if basis == "haar":
+        rec_lo = np.array([1.0, 1.0]) * _INV_SQRT2
+        dec_lo = rec_lo[::-1].copy()
+    elif basis == "db4":
+        rec_lo = daubechies_lowpass(4)
+        dec_lo = rec_lo[::-1].copy()
+    elif basis == "bior4.4":
+        ana, syn = cdf_lowpasses()
+        dec_lo, rec_lo = np.zeros(10), np.zeros(10)
+        dec_lo[1:10] = ana
+        rec_lo[1:8] = syn
+    else:
+        raise ValueError(f"unknown wavelet basis {basis!r}")
+    sign = (-1.0) ** np.arange(len(dec_lo))
+    return dec_lo, -sign * rec_lo, rec_lo, sign * dec_lo
+
+
+def _symmetric_index(i, L):
+    """Index into x of position i of its half-sample symmetric extension."""
+    i = np.mod(i, 2 * L)
+    return np.where(i < L, i, 2 * L - 1 - i)
+
+
+def dwt_step(x, bank, axis=0, mode="symmetric"):
+    """One analysis step along `axis` -> (approximation, detail) (Eq. (9), Eq. (12) per axis).
+
+    mode "symmetric": the extension above (floor((L + F - 1) / 2) coefficients);
+    mode "periodization": x~ periodic with period L (L even, L / 2 coefficients),
+    the orthogonal form used only to check energy preservation.
+    """
+    dec_lo, dec_hi = bank[0], bank[1]
+    x = np.asarray(x, dtype=np.float64)
+    L, F = x.shape[axis], len(dec_lo)
+    n = (L + F - 1) // 2 if mode == "symmetric" else L // 2
+    a = np.zeros(x.shape[:axis] + (n,) + x.shape[axis + 1:])
+    d = np.zeros_like(a)
+    for j in range(F):
+        pos = 2 * np.arange(n) + 1 - j
+        idx = _symmetric_index(pos, L) if mode == "symmetric" else np.mod(pos, L)
+        xs = np.take(x, idx, axis=axis)
+        a += dec_lo[j] * xs
+        d += dec_hi[j] * xs
+    return a, d
+
+
+def idwt_step(a, d, bank, length, axis=0):
+    """Synthesis step inverting `dwt_step` (mode symmetric), cropped to `length` (Eq. (11), Eq. (15))."""
+    rec_lo, rec_hi = bank[2], bank[3]
+    a = np.asarray(a, dtype=np.float64)
+    d = np.asarray(d, dtype=np.float64)
+    n, F = a.shape[axis], len(rec_lo)
+    m = 2 * n - F + 2
+    out = np.zeros(a.shape[:axis] + (m,) + a.shape[axis + 1:])
+    idx = [slice(None)] * out.ndim
+    for i in range(m):
+        acc = np.zeros(np.take(a, [0], axis=axis).shape)
+        for k in range(n):
+            f = i + F - 2 - 2 * k
+            if 0 <= f < F:
+                acc = acc + rec_lo[f] * np.take(a, [k], axis=axis) + rec_hi[f] * np.take(d, [k], axis=axis)
+        idx[axis] = slice(i, i + 1)
+        out[tuple(idx)] = acc
+    idx[axis] = slice(0, length)
+    return out[tuple(idx)]
+
+
+def adaptive_average(v, n, axis=0):
+    """Average pooling of `axis` (length L) to n outputs: output i is the mean of
+    positions floor(i L / n) .. ceil((i + 1) L / n) - 1 (the down-sampling of
+    Eq. (10) and Eq. (13) to a subband's resolution)."""
+    v = np.asarray(v, dtype=np.float64)
+    L = v.shape[axis]
+    parts = []
+    for i in range(n):
+        lo, hi = (i * L) // n, -((-(i + 1) * L) // n)
+        parts.append(np.take(v, np.arange(lo, hi), axis=axis).mean(axis=axis, keepdims=True))
+    return np.concatenate(parts, axis=axis)
+
+
+def wavelet_temporal_allocator_bank(R, Gamma, levels, basis):
+    """Eq. (9)-(11) with the filter bank of `basis` (the Haar case is `wavelet_temporal_allocator`).
+
+    Level j = 1..J: (A_j, D_j) = dwt_step(A_{j-1}); the gate is pooled to the
+    detail length by `adaptive_average` of the previous level's gate (Gamma at
+    level 0); D~_j = Gamma-bar_j * D_j; synthesis from the coarsest level, each
+    level cropped to the length it had.
+    """
+    bank = filter_bank(basis)
+    A = np.asarray(R, dtype=np.float64)
+    g = np.asarray(Gamma, dtype=np.float64)
+    lengths, details = [], []
+    for _ in range(levels):
+        lengths.append(A.shape[0])
+        A, D = dwt_step(A, bank)
+        g = adaptive_average(g, D.shape[0])
+        details.append(g * D)
+    for j in reversed(range(levels)):
+        A = idwt_step(A, details[j], bank, lengths[j])
+    return A
+
+
+def dwt2_step(F, bank):
+    """Single-level separable 2-D analysis of F [H, W, ...] -> (LL, LH, HL, HH) (Eq. (12)),
+    the first letter the filter along the height, the second along the width."""
+    lo_w, hi_w = dwt_step(F, bank, axis=1)
+    LL, HL = dwt_step(lo_w, bank, axis=0)
+    LH, HH = dwt_step(hi_w, bank, axis=0)
+    return LL, LH, HL, HH
+
+
+def idwt2_step(LL, LH, HL, HH, bank, H, W):
+    """Inverse of `dwt2_step`, cropped to H x W (Eq. (15))."""
+    lo_w = idwt_step(LL, HL, bank, H, axis=0)
+    hi_w = idwt_step(LH, HH, bank, H, axis=0)
+    return idwt_step(lo_w, hi_w, bank, W, axis=1)
+
+
+def wavelet_spatial_modulator_bank(F, Mhw, lam, basis):
+    """X-tilde of Eq. (12)-(15) with the filter bank of `basis`, one level.
+
+    G = lam * P(M), P the adaptive average pooling of the H x W saliency map to
+    the subband grid (n_h x n_w); LH, HL and HH are multiplied by G, LL kept,
+    and the frame rebuilt and cropped to H x W.
+    """
+    bank = filter_bank(basis)
+    H, W = Mhw.shape
+    LL, LH, HL, HH = dwt2_step(F, bank)
+    G = lam * adaptive_average(adaptive_average(Mhw, LL.shape[0], axis=0), LL.shape[1], axis=1)
+    G = G[:, :, None]
+    return idwt2_step(LL, G * LH, G * HL, G * HH, bank, H, W)
+
+
+# ---------------------------------------------------------------------------
 # Token Assigner: selection and concatenation (Eq. (17) replaced, Eq. (19))
 # ---------------------------------------------------------------------------
 
@@ -373,12 +572,15 @@ def select_tokens(a_t, n_t):
     return np.sort(order[:n_t])
 
 
-def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select", spatial_levels=1):
+def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select", spatial_levels=1,
+             temporal_basis="haar", spatial_basis="haar"):
     """The whole pass C(X, Q) of Eq. (4)/(6); returns every intermediate.
 
     assign: "select" keeps each frame's n_t most salient modulated tokens,
     "interp" interpolates the modulated frame to n_t tokens (Psi of Eq. (17)).
     spatial_levels: levels of the spatial Haar modulator (1 as in Eq. (12)-(15)).
+    temporal_basis / spatial_basis: "haar" (the transforms above), "db4" or
+    "bior4.4" (the filter banks above; one spatial level, selection only).
     Keys: a [T,N], vbar [T,C], r [T], delta [T], gamma [T], retained (list),
     r_tilde [L], budget [T] (0 for dropped frames), offset [T+1], M [T,N],
     tokens [offset[T], C], index [offset[T]] (flat t*N + h*W + w).
@@ -393,7 +595,10 @@ def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select", spatial_l
     delta = visual_change(vbar)
     gamma = temporal_gate(delta)
     kept_frames = retained_frames(delta, tau)
-    r_tilde = wavelet_temporal_allocator(r[kept_frames], gamma[kept_frames], levels)
+    if temporal_basis == "haar":
+        r_tilde = wavelet_temporal_allocator(r[kept_frames], gamma[kept_frames], levels)
+    else:
+        r_tilde = wavelet_temporal_allocator_bank(r[kept_frames], gamma[kept_frames], levels, temporal_basis)
     n_kept = allocate_budget(r_tilde, B, N)
     budget = np.zeros(T, dtype=np.int64)
     budget[kept_frames] = n_kept
@@ -404,7 +609,10 @@ def condense(X, query, B, levels=1, lam=1.5, tau=0.0, assign="select", spatial_l
     for t in range(T):
         if budget[t] == 0:
             continue
-        Xt = wavelet_spatial_modulator(X[t], M[t].reshape(H, W), lam, spatial_levels)
+        if spatial_basis == "haar":
+            Xt = wavelet_spatial_modulator(X[t], M[t].reshape(H, W), lam, spatial_levels)
+        else:
+            Xt = wavelet_spatial_modulator_bank(X[t], M[t].reshape(H, W), lam, spatial_basis)
         if assign == "interp":
             tok_t, near = budget_guided_interpolation(Xt, int(budget[t]))
             tokens[offset[t]:offset[t + 1]] = tok_t

@@ -149,3 +149,40 @@ def condense(X, query, B, levels=1, lam=1.5, tau=0.0):
             out_index.append(t * N + n)
     return dict(a=a, r=r, delta=delta, gamma=gamma, retained=kept, r_tilde=r_tilde,
                 budget=budget, tokens=out_tokens, index=out_index)
+
+
+# ---------------------------------------------------------------------------
+# One level of a filter-bank DWT, for the db4 / bior4.4 modulators: scalar
+# loops over an explicitly built extended list (the oracle indexes an
+# extension rule instead), synthesis by scattering each coefficient's
+# filter-weighted contribution (the oracle gathers per output sample).
+# ---------------------------------------------------------------------------
+
+def dwt_bank(x, dec_lo, dec_hi):
+    """(a, d) of list x: a[k] = sum_j dec_lo[j] * e[2k + 1 - j + pad], e the list x
+    mirrored (half-sample) by pad = len(filter) - 1 samples at each end."""
+    L, F = len(x), len(dec_lo)
+    pad = F - 1
+    e = []
+    for i in range(-pad, L + pad):
+        j = i
+        while j < 0 or j >= L:  # reflect about the half-sample points -1/2 and L - 1/2
+            j = -1 - j if j < 0 else 2 * L - 1 - j
+        e.append(x[j])
+    n = (L + F - 1) // 2
+    a = [sum(dec_lo[j] * e[2 * k + 1 - j + pad] for j in range(F)) for k in range(n)]
+    d = [sum(dec_hi[j] * e[2 * k + 1 - j + pad] for j in range(F)) for k in range(n)]
+    return a, d
+
+
+def idwt_bank(a, d, rec_lo, rec_hi, length):
+    """Inverse of dwt_bank: coefficient k adds rec_lo[f] * a[k] + rec_hi[f] * d[k] to
+    sample 2k + f - (F - 2) for every filter position f; samples outside [0, length) dropped."""
+    F = len(rec_lo)
+    out = [0.0] * length
+    for k in range(len(a)):
+        for f in range(F):
+            i = 2 * k + f - (F - 2)
+            if 0 <= i < length:
+                out[i] += rec_lo[f] * a[k] + rec_hi[f] * d[k]
+    return out

@@ -407,4 +407,202 @@ def pin_wsm_two_levels():
         assert np.abs(flat - _two_level_closed_form(F, np.zeros((H, W)), 1.5)).max() < 1e-12
 
 
+# ---------------------------------------------------------------------------
+# Longer wavelet bases: db4 and bior4.4 (Sec. 3.2.3, Sec. 4.3)
+# ---------------------------------------------------------------------------
+
+BANKS = ("haar", "db4", "bior4.4")
+
+
+def pin_wavelet_taps_published():
+    """The constructed low-pass filters equal the published tables (tests/golden/wavelet_taps.json)."""
+    fix = _load("wavelet_taps.json")
+    h = oracle.daubechies_lowpass(4)
+    assert np.abs(h - np.array(fix["db4_lowpass"]["values"])).max() < 1e-12
+    ana, syn = oracle.cdf_lowpasses()
+    a = np.array(fix["cdf97_analysis_lowpass"]["center_out"]) * math.sqrt(2.0)
+    g = np.array(fix["cdf97_synthesis_lowpass"]["center_out"]) / math.sqrt(2.0)
+    assert np.abs(ana - np.concatenate([a[:0:-1], a])).max() < 1e-12
+    assert np.abs(syn - np.concatenate([g[:0:-1], g])).max() < 1e-12
+    dec_lo, _, rec_lo, _ = oracle.filter_bank("db4")
+    assert np.array_equal(rec_lo, h) and np.array_equal(dec_lo, h[::-1])
+
+
+def pin_wavelet_filter_algebra():
+    """db4: orthonormal (sum_k h_k h_(k+2m) = delta_m), sum sqrt 2; bior4.4: symmetric low-passes,
+    biorthogonal (sum_k dec_lo[k] rec_lo[k + 2m] reversed-aligned = delta_m); every high-pass of the
+    longer bases kills polynomials of degree < 4 (four vanishing moments), Haar's constants."""
+    for basis, moments in (("haar", 1), ("db4", 4), ("bior4.4", 4)):
+        dec_lo, dec_hi, rec_lo, rec_hi = oracle.filter_bank(basis)
+        F = len(dec_lo)
+        assert F % 2 == 0 and len(dec_hi) == len(rec_lo) == len(rec_hi) == F
+        assert abs(dec_lo.sum() - math.sqrt(2.0)) < 1e-13 and abs(rec_lo.sum() - math.sqrt(2.0)) < 1e-13
+        k = np.arange(F, dtype=np.float64)
+        for p in range(moments):
+            assert abs(np.sum(dec_hi * k ** p)) < 1e-10 * F ** p, (basis, p)
+            assert abs(np.sum(rec_hi * k ** p)) < 1e-10 * F ** p, (basis, p)
+        # biorthogonality of the analysis and synthesis low-passes: with the
+        # analysis filter reversed, sum_k rev(dec_lo)[k] rec_lo[k + 2m] = delta_m
+        rd = dec_lo[::-1]
+        for m in range(-(F // 2) + 1, F // 2):
+            v = sum(rd[i] * rec_lo[i + 2 * m] for i in range(F) if 0 <= i + 2 * m < F)
+            assert abs(v - (1.0 if m == 0 else 0.0)) < 1e-12, (basis, m)
+    h = oracle.daubechies_lowpass(4)
+    for m in range(4):
+        assert abs(sum(h[i] * h[i + 2 * m] for i in range(8 - 2 * m)) - (1.0 if m == 0 else 0.0)) < 1e-13
+    ana, syn = oracle.cdf_lowpasses()
+    assert np.abs(ana - ana[::-1]).max() < 1e-14 and np.abs(syn - syn[::-1]).max() < 1e-14
+
+
+def pin_dwt_bank_perfect_reconstruction():
+    """dwt_step then idwt_step is the identity for every basis, every length 1..40, along any axis;
+    the 2-D step likewise on odd and even grids."""
+    rng = np.random.default_rng(71)
+    for basis in BANKS:
+        bank = oracle.filter_bank(basis)
+        for L in range(1, 41):
+            x = rng.standard_normal((L, 2))
+            a, d = oracle.dwt_step(x, bank)
+            assert a.shape[0] == (L + len(bank[0]) - 1) // 2
+            assert np.abs(oracle.idwt_step(a, d, bank, L) - x).max() < 1e-12, (basis, L)
+        y = rng.standard_normal((3, 9, 2))
+        a, d = oracle.dwt_step(y, bank, axis=1)
+        assert np.abs(oracle.idwt_step(a, d, bank, 9, axis=1) - y).max() < 1e-12
+        for H, W in ((14, 14), (13, 13), (27, 27), (1, 5), (6, 3)):
+            F = rng.standard_normal((H, W, 3))
+            assert np.abs(oracle.idwt2_step(*oracle.dwt2_step(F, bank), bank, H, W) - F).max() < 1e-12
+
+
+def pin_dwt_bank_matches_brute():
+    """The vectorised steps equal the scalar brute force of tests/brute.py (explicit mirrored list,
+    scatter-form synthesis) on tiny signals of every basis."""
+    rng = np.random.default_rng(72)
+    for basis in BANKS:
+        dec_lo, dec_hi, rec_lo, rec_hi = (list(map(float, v)) for v in oracle.filter_bank(basis))
+        bank = oracle.filter_bank(basis)
+        for L in (1, 2, 3, 4, 7, 10, 14):
+            x = rng.standard_normal(L)
+            a, d = oracle.dwt_step(x, bank)
+            ba, bd = brute.dwt_bank(list(x), dec_lo, dec_hi)
+            assert np.abs(a - ba).max() < 1e-13 and np.abs(d - bd).max() < 1e-13
+            g = rng.standard_normal((2, len(ba)))
+            assert np.abs(oracle.idwt_step(g[0], g[1], bank, L)
+                          - brute.idwt_bank(list(g[0]), list(g[1]), rec_lo, rec_hi, L)).max() < 1e-13
+
+
+def pin_dwt_bank_haar_is_haar():
+    """With the Haar bank the general steps are the Haar steps (odd lengths too), in 1-D and 2-D."""
+    rng = np.random.default_rng(73)
+    bank = oracle.filter_bank("haar")
+    for L in range(1, 12):
+        x = rng.standard_normal((L, 2))
+        A, D = oracle.haar_analysis(x)
+        a, d = oracle.dwt_step(x, bank)
+        assert np.abs(A - a).max() < 1e-15 and np.abs(D - d).max() < 1e-15
+        assert np.abs(oracle.idwt_step(a, d, bank, L) - oracle.haar_synthesis(A, D, L)).max() < 1e-15
+    F = rng.standard_normal((5, 6, 2))
+    for u, v in zip(oracle.dwt2_step(F, bank), oracle.haar_analysis_2d(F)):
+        assert np.abs(u - v).max() < 1e-15
+
+
+def pin_dwt_bank_periodic_parseval():
+    """Periodised, the orthonormal bases keep energy (sum a^2 + sum d^2 = sum x^2) and are invertible by
+    their transpose; the biorthogonal bior4.4 does not keep energy (its rows are not orthonormal)."""
+    rng = np.random.default_rng(74)
+    for basis in ("haar", "db4"):
+        bank = oracle.filter_bank(basis)
+        for L in (8, 14, 16, 30):
+            x = rng.standard_normal(L)
+            a, d = oracle.dwt_step(x, bank, mode="periodization")
+            assert abs(np.sum(a * a) + np.sum(d * d) - np.sum(x * x)) < 1e-12 * np.sum(x * x), (basis, L)
+            Wm = np.stack([np.concatenate(oracle.dwt_step(e, bank, mode="periodization")) for e in np.eye(L)], 1)
+            assert np.abs(Wm @ Wm.T - np.eye(L)).max() < 1e-12
+    x = rng.standard_normal(16)
+    a, d = oracle.dwt_step(x, oracle.filter_bank("bior4.4"), mode="periodization")
+    assert abs(np.sum(a * a) + np.sum(d * d) - np.sum(x * x)) > 1e-6 * np.sum(x * x)
+
+
+def pin_dwt_bank_constants_and_cubics():
+    """A constant signal has no detail anywhere (the symmetric extension of a constant is constant) and
+    approximation sqrt 2 times it; the details of a cubic vanish wherever the analysis filter does not reach
+    past the ends (four vanishing moments of db4 and bior4.4)."""
+    for basis in BANKS:
+        bank = oracle.filter_bank(basis)
+        F = len(bank[0])
+        for L in (1, 5, 14):
+            a, d = oracle.dwt_step(np.full(L, 3.0), bank)
+            assert np.abs(d).max() < 1e-13 and np.abs(a - 3.0 * math.sqrt(2.0)).max() < 1e-12
+        if basis == "haar":
+            continue
+        L = 40
+        t = np.arange(L, dtype=np.float64)
+        x = 0.5 * t ** 3 - 4.0 * t ** 2 + t - 7.0
+        _, d = oracle.dwt_step(x, bank)
+        # d[k] reads x~[2k + 1 - j], j < F: inside [0, L) for F - 1 <= 2k + 1 <= L - 1
+        inner = [k for k in range(len(d)) if 2 * k + 1 - (F - 1) >= 0 and 2 * k + 1 <= L - 1]
+        assert len(inner) > 5
+        assert np.abs(d[inner]).max() < 1e-8 * np.abs(x).max(), basis
+        assert np.abs(d).max() > 1e-3  # the ends do feel the extension
+
+
+def pin_adaptive_average_torch():
+    """`adaptive_average` equals torch's adaptive average pooling (an independent implementation), 1-D and
+    2-D, for shrinking and equal sizes; pairs of an even length are pair averages."""
+    import torch
+    rng = np.random.default_rng(75)
+    for L in range(1, 30):
+        for n in range(1, L + 1):
+            v = rng.standard_normal(L)
+            want = torch.nn.functional.adaptive_avg_pool1d(torch.tensor(v)[None, None], n)[0, 0].numpy()
+            assert np.abs(oracle.adaptive_average(v, n) - want).max() < 1e-12, (L, n)
+    M = rng.random((14, 13))
+    want = torch.nn.functional.adaptive_avg_pool2d(torch.tensor(M)[None, None], (10, 10))[0, 0].numpy()
+    got = oracle.adaptive_average(oracle.adaptive_average(M, 10, axis=0), 10, axis=1)
+    assert np.abs(got - want).max() < 1e-12
+    g = rng.standard_normal(12)
+    assert np.abs(oracle.adaptive_average(g, 6) - oracle.pair_average(g)).max() < 1e-15
+
+
+def pin_wta_bank_cases():
+    """Temporal allocator with a filter bank: gate 1 rebuilds r exactly (every basis, J = 1..3, odd lengths);
+    with the Haar bank and lengths divisible by 2^J it is the Haar allocator; gate 0 keeps only the coarsest
+    approximation, which for a constant sequence is the sequence itself."""
+    rng = np.random.default_rng(76)
+    for basis in ("db4", "bior4.4"):
+        for J in (1, 2, 3):
+            for L in (1, 7, 16, 33, 64):
+                r = rng.standard_normal(L)
+                assert np.abs(oracle.wavelet_temporal_allocator_bank(r, np.ones(L), J, basis) - r).max() < 1e-12
+            c = np.full(21, -0.7)
+            assert np.abs(oracle.wavelet_temporal_allocator_bank(c, np.zeros(21), J, basis) - c).max() < 1e-12
+    for J in (1, 2, 3):
+        L = 8 * 2 ** J
+        r, g = rng.standard_normal(L), rng.random(L)
+        want = oracle.wavelet_temporal_allocator(r, g, J)
+        assert np.abs(oracle.wavelet_temporal_allocator_bank(r, g, J, "haar") - want).max() < 1e-13
+
+
+def pin_wsm_bank_cases():
+    """Spatial modulator with a filter bank: a unit gate rebuilds the frame (odd and even grids); with the
+    Haar bank on even grids it is the Haar modulator; the result is affine in lambda with the approximation-only
+    frame at lambda = 0; a constant frame is left unchanged by any gate."""
+    rng = np.random.default_rng(77)
+    for basis in ("db4", "bior4.4"):
+        for H, W in ((14, 14), (13, 13), (27, 27), (3, 8)):
+            F = rng.standard_normal((H, W, 2))
+            M = rng.random((H, W))
+            assert np.abs(oracle.wavelet_spatial_modulator_bank(F, np.full((H, W), 0.5), 2.0, basis) - F).max() < 1e-12
+            x0 = oracle.wavelet_spatial_modulator_bank(F, M, 0.0, basis)
+            x1 = oracle.wavelet_spatial_modulator_bank(F, M, 1.0, basis)
+            x15 = oracle.wavelet_spatial_modulator_bank(F, M, 1.5, basis)
+            assert np.abs(x15 - (x0 + 1.5 * (x1 - x0))).max() < 1e-12
+            C = np.full((H, W, 2), 1.25)
+            assert np.abs(oracle.wavelet_spatial_modulator_bank(C, M, 1.5, basis) - C).max() < 1e-12
+    for H, W in ((14, 14), (4, 6)):
+        F = rng.standard_normal((H, W, 3))
+        M = rng.random((H, W))
+        want = oracle.wavelet_spatial_modulator(F, M, 1.5)
+        assert np.abs(oracle.wavelet_spatial_modulator_bank(F, M, 1.5, "haar") - want).max() < 1e-13
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -161,6 +161,103 @@ def _wsm_level2_unpooled_gate(F, Mhw, lam, levels=1):
     return LL
 
 
+def _daub_max_phase(N):
+    # the zeros outside the unit circle (maximum phase) instead of inside
+    h = W._orig["daubechies_lowpass"](N)
+    return h[::-1].copy()
+
+
+def _bank_highpass_sign(basis):
+    dec_lo, dec_hi, rec_lo, rec_hi = W._orig["filter_bank"](basis)
+    return dec_lo, dec_hi, rec_lo, -rec_hi
+
+
+def _dwt_zero_extension(x, bank, axis=0, mode="symmetric"):
+    # zero padding instead of the symmetric extension
+    dec_lo, dec_hi = bank[0], bank[1]
+    x = np.asarray(x, dtype=np.float64)
+    L, F = x.shape[axis], len(dec_lo)
+    n = (L + F - 1) // 2 if mode == "symmetric" else L // 2
+    a = np.zeros(x.shape[:axis] + (n,) + x.shape[axis + 1:])
+    d = np.zeros_like(a)
+    for j in range(F):
+        pos = 2 * np.arange(n) + 1 - j
+        ok = (pos >= 0) & (pos < L)
+        xs = np.take(x, np.clip(pos, 0, L - 1), axis=axis)
+        shape = [1] * x.ndim
+        shape[axis] = n
+        xs = xs * ok.reshape(shape)
+        a += dec_lo[j] * xs
+        d += dec_hi[j] * xs
+    return a, d
+
+
+def _dwt_even_phase(x, bank, axis=0, mode="symmetric"):
+    # coefficients taken at the even positions 2k - j instead of 2k + 1 - j
+    dec_lo, dec_hi = bank[0], bank[1]
+    x = np.asarray(x, dtype=np.float64)
+    L, F = x.shape[axis], len(dec_lo)
+    n = (L + F - 1) // 2 if mode == "symmetric" else L // 2
+    a = np.zeros(x.shape[:axis] + (n,) + x.shape[axis + 1:])
+    d = np.zeros_like(a)
+    for j in range(F):
+        pos = 2 * np.arange(n) - j
+        idx = W._symmetric_index(pos, L) if mode == "symmetric" else np.mod(pos, L)
+        xs = np.take(x, idx, axis=axis)
+        a += dec_lo[j] * xs
+        d += dec_hi[j] * xs
+    return a, d
+
+
+def _adaptive_floor_both(v, n, axis=0):
+    v = np.asarray(v, dtype=np.float64)
+    L = v.shape[axis]
+    parts = [np.take(v, np.arange((i * L) // n, max((i * L) // n + 1, ((i + 1) * L) // n)), axis=axis)
+             .mean(axis=axis, keepdims=True) for i in range(n)]
+    return np.concatenate(parts, axis=axis)
+
+
+def _wta_bank_gate_approx(R, Gamma, levels, basis):
+    # the gate applied to the approximation instead of the detail
+    bank = W.filter_bank(basis)
+    A = np.asarray(R, dtype=np.float64)
+    g = np.asarray(Gamma, dtype=np.float64)
+    lengths, details = [], []
+    for _ in range(levels):
+        lengths.append(A.shape[0])
+        A, D = W.dwt_step(A, bank)
+        g = W.adaptive_average(g, D.shape[0])
+        A = g * A
+        details.append(D)
+    for j in reversed(range(levels)):
+        A = W.idwt_step(A, details[j], bank, lengths[j])
+    return A
+
+
+def _wsm_bank_gate_ll(F, Mhw, lam, basis):
+    bank = W.filter_bank(basis)
+    H, Wd = Mhw.shape
+    LL, LH, HL, HH = W.dwt2_step(F, bank)
+    G = lam * W.adaptive_average(W.adaptive_average(Mhw, LL.shape[0], axis=0), LL.shape[1], axis=1)
+    G = G[:, :, None]
+    return W.idwt2_step(G * LL, G * LH, G * HL, G * HH, bank, H, Wd)
+
+
+def _wsm_bank_gate_axes_swapped(F, Mhw, lam, basis):
+    bank = W.filter_bank(basis)
+    H, Wd = Mhw.shape
+    LL, LH, HL, HH = W.dwt2_step(F, bank)
+    G = lam * W.adaptive_average(W.adaptive_average(Mhw, LL.shape[1], axis=0), LL.shape[0], axis=1)
+    G = G[:, :, None]
+    if G.shape[:2] != LL.shape[:2]:
+        G = G.transpose(1, 0, 2)
+    return W.idwt2_step(LL, G * LH, G * HL, G * HH, bank, H, Wd)
+
+
+def _idwt2_bands_swapped(LL, LH, HL, HH, bank, H, Wd):
+    return W._orig["idwt2_step"](LL, HL, LH, HH, bank, H, Wd)
+
+
 MUTATIONS = {
     "haar_detail_sign": ("haar_analysis", _analysis_detail_sign),
     "haar_synthesis_swapped": ("haar_synthesis", _synthesis_swapped),
@@ -182,6 +279,15 @@ MUTATIONS = {
     "interp_align_corners": ("_sample", _sample_corners),
     "interp_grid_transposed": ("interpolation_grid", _grid_swap),
     "wsm_level2_unpooled_gate": ("wavelet_spatial_modulator", _wsm_level2_unpooled_gate),
+    "daubechies_max_phase": ("daubechies_lowpass", _daub_max_phase),
+    "bank_highpass_sign": ("filter_bank", _bank_highpass_sign),
+    "dwt_zero_extension": ("dwt_step", _dwt_zero_extension),
+    "dwt_even_phase": ("dwt_step", _dwt_even_phase),
+    "adaptive_average_floor_ends": ("adaptive_average", _adaptive_floor_both),
+    "wta_bank_gate_on_approximation": ("wavelet_temporal_allocator_bank", _wta_bank_gate_approx),
+    "wsm_bank_gates_LL": ("wavelet_spatial_modulator_bank", _wsm_bank_gate_ll),
+    "wsm_bank_gate_axes_swapped": ("wavelet_spatial_modulator_bank", _wsm_bank_gate_axes_swapped),
+    "idwt2_bands_swapped": ("idwt2_step", _idwt2_bands_swapped),
 }
 
 
@@ -189,7 +295,7 @@ MUTATIONS = {
 def _originals():
     W._orig = {name: getattr(W, name) for name, _ in
                [(n, None) for n in ("haar_analysis", "haar_synthesis", "allocate_budget_trace", "haar_analysis_2d",
-                                    "interpolation_grid")]}
+                                    "interpolation_grid", "daubechies_lowpass", "filter_bank", "idwt2_step")]}
     yield
     del W._orig
 
