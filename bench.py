@@ -21,7 +21,8 @@ the rate of a plain read of the frame tensor on the same device
 CPU oracle's rate on the host (all cores and one thread) as a reported
 baseline, (`interp`) the rate with the
 budget-guided interpolation forming the tokens instead of selection,
-(`spatial_levels_2`) the rate with the two-level spatial modulator, and
+(`bases`) the rates with db4 or bior4.4 spatial modulators and a bior4.4
+temporal allocator, (`spatial_levels_2`) the rate with the two-level spatial modulator, and
 (`batched`) the rate of wz_condense_batch on several videos of the same
 workload per call, and (`queries`) the rate of wz_condense_queries with
 several queries over each video per call -- separate modes, not the
@@ -309,6 +310,19 @@ def main():
     torch.cuda.synchronize()
     i_ms = ev0.elapsed_time(ev1) / args.steps
     interp = {"ms_per_step": i_ms, "frames_per_s": wl.T / (i_ms * 1e-3)}
+    # and with the longer wavelet bases: db4 / bior4.4 spatial modulators, a bior4.4 temporal allocator
+    def mode_rate(pm):
+        wsm = wz.new_workspace(pm, dev)
+        for i in range(args.warmup):
+            wz.condense(pm, Xs[i % nsets], qs[i % nsets], ws=wsm, out=out)
+        torch.cuda.synchronize()
+        m_ms, _ = timed_groups(stream, lambda i: wz.condense(pm, Xs[i % nsets], qs[i % nsets], ws=wsm, out=out),
+                               args.steps, args.repeats)
+        return {"ms_per_step": m_ms, "frames_per_s": wl.T / (m_ms * 1e-3)}
+
+    bases = {"spatial_db4": mode_rate(wz.problem_of(wl, out_dtype, spatial_basis=wz.WZ_DB4)),
+             "spatial_bior4.4": mode_rate(wz.problem_of(wl, out_dtype, spatial_basis=wz.WZ_BIOR44)),
+             "temporal_bior4.4": mode_rate(wz.problem_of(wl, out_dtype, temporal_basis=wz.WZ_BIOR44))}
     # and with the two-level spatial modulator (cfg.spatial_levels = 2)
     p2 = wz.problem_of(wl, out_dtype, spatial_levels=2)
     ws2 = wz.new_workspace(p2, dev)
@@ -360,6 +374,7 @@ def main():
                          "us": rc_us, "gbps": rc_gbps, "frac_of_peak": rc_gbps / HBM_PEAK_GBPS},
     }
     line["interp"] = interp
+    line["bases"] = bases
     line["spatial_levels_2"] = levels2
     if batched:
         line["batched"] = batched

@@ -72,6 +72,19 @@ typedef enum {
 
 typedef enum { WZ_F32 = 0, WZ_BF16 = 1 } wz_dtype;
 
+/* Wavelet basis of the temporal allocator (Eq. (9)-(11)) or of the spatial
+ * modulator (Eq. (12)-(15)).  WZ_HAAR is the orthonormal Haar transform the
+ * equations are written with; WZ_DB4 (the paper's spatial default, Sec. 4.1)
+ * and WZ_BIOR44 (its basis ablation, Sec. 4.3) use filter banks of 8 and 10
+ * taps: Daubechies' minimum-phase N = 4 filter, and the CDF 9/7 pair of
+ * JPEG 2000's irreversible transform.  Conventions for the longer banks: one
+ * analysis step on L samples extends them half-sample symmetrically and
+ * gives floor((L + F - 1) / 2) coefficients per band, a[k] = sum_j
+ * dec_lo[j] x~[2k + 1 - j]; synthesis is cropped back to L; a gate is pooled
+ * to a subband's length by adaptive average pooling (output i averages
+ * inputs floor(i L / n) .. ceil((i + 1) L / n) - 1).                        */
+typedef enum { WZ_HAAR = 0, WZ_DB4 = 1, WZ_BIOR44 = 2 } wz_basis;
+
 /* How a frame's n_t output tokens are formed from its modulated map
  * (Token Assigner, Eq. (17)).                                                 */
 typedef enum {
@@ -91,7 +104,9 @@ typedef enum {
  * WZ_ERR_PARAM): 1 <= T <= 2048; 1 <= H, W and H*W <= 4096; 1 <= Q <= 1024;
  * 8 <= C <= 65536 with C % 8 == 0; 1 <= levels <= 16; lambda_ finite and
  * >= 0; tau in [0, 2]; assign a wz_assign value; spatial_levels 0, 1 or 2
- * (2 only with WZ_SELECT).                                                    */
+ * (2 only with WZ_SELECT); temporal_basis and spatial_basis wz_basis values;
+ * a spatial_basis other than WZ_HAAR needs WZ_SELECT, spatial_levels <= 1,
+ * H, W <= 64 and H*W <= 1024.                                                  */
 typedef struct {
   int32_t T, H, W, C, Q;
   int32_t in_dtype;   /* wz_dtype of X and query                               */
@@ -106,6 +121,8 @@ typedef struct {
                          levels -- the approximation decomposed once more, level
                          2's details gated by lambda times M pooled twice (the
                          multi-level variant of the ablations); selection only */
+  int32_t temporal_basis; /* wz_basis of the temporal allocator (0: Haar)   */
+  int32_t spatial_basis;  /* wz_basis of the spatial modulator (0: Haar)    */
 } wz_config;
 
 /* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`

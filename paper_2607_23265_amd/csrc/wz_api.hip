@@ -53,8 +53,11 @@ wz_status check_config(const wz_config* c) {
     return WZ_ERR_SHAPE;
   if (c->levels < 1 || c->levels > 16 || !std::isfinite(c->lambda_) || c->lambda_ < 0.f ||
       !std::isfinite(c->tau) || c->tau < 0.f || c->tau > 2.f || (c->assign != WZ_SELECT && c->assign != WZ_INTERP) ||
-      c->spatial_levels < 0 || c->spatial_levels > 2 || (c->spatial_levels == 2 && c->assign != WZ_SELECT))
+      c->spatial_levels < 0 || c->spatial_levels > 2 || (c->spatial_levels == 2 && c->assign != WZ_SELECT) ||
+      c->temporal_basis < WZ_HAAR || c->temporal_basis > WZ_BIOR44 || c->spatial_basis < WZ_HAAR ||
+      c->spatial_basis > WZ_BIOR44 || (c->spatial_basis != WZ_HAAR && (c->assign != WZ_SELECT || c->spatial_levels > 1)))
     return WZ_ERR_PARAM;
+  if (c->spatial_basis != WZ_HAAR && !filter_assign_supported(*c)) return WZ_ERR_SHAPE;
   if (c->B < 0 || c->B > int64_t(c->T) * c->H * c->W) return WZ_ERR_BUDGET;
   return WZ_OK;
 }
@@ -105,11 +108,14 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   vs.out = cfg->B * cfg->C * s_out;
   vs.idx = cfg->B * 4;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // a filter-bank spatial basis ranks each frame in its own kernel: the
+  // per-frame kernel then forms r and delta only
+  const bool filt = cfg->spatial_basis != WZ_HAAR;
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s, vs)));
-  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s, vs)));
+  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, !filt, s, vs)));
   vs.bud = budget ? (long long)cfg->T * 4 : vs.ws;
   vs.off = offset ? ((long long)cfg->T + 1) * 4 : vs.ws;
-  if (cfg->T <= kFusedTMax) {  // budgets computed inside the selection kernel
+  if (cfg->T <= kFusedTMax && cfg->temporal_basis == WZ_HAAR && !filt) {  // budgets inside the selection kernel
     vs.bud = (long long)cfg->T * 4;
     vs.off = ((long long)cfg->T + 1) * 4;
     return from_hip(launch_assign_gather(*cfg, X, w.tok_score, w.frame_rel, w.frame_delta, nullptr, &w, budget,
@@ -118,6 +124,7 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
   WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s, vs)));
+  if (filt) return from_hip(launch_filter_assign(*cfg, X, w.tok_score, off, out_tokens, out_index, s, vs));
   return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, &w, nullptr, nullptr, out_tokens,
                                        out_index, s, vs));
 }
@@ -198,6 +205,9 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
     WZ_TRY(check_ptr(out_tokens, 16));
     WZ_TRY(check_ptr(out_index, 4));
   }
+  if (cfg->spatial_basis != WZ_HAAR)
+    return from_hip(
+        launch_filter_assign(*cfg, X, tok_score, offset, out_tokens, out_index, static_cast<hipStream_t>(stream)));
   return from_hip(launch_assign_gather(*cfg, X, tok_score, nullptr, nullptr, offset, nullptr, nullptr, nullptr,
                                        out_tokens, out_index, static_cast<hipStream_t>(stream)));
 }

@@ -17,9 +17,13 @@
 //            rest re-apportioned; leftover tokens go to the largest
 //            fractional parts (ties: smaller frame index); uniform weights if
 //            every w is 0; every frame full when B >= |M| * H * W.
+//   (db4 / bior4.4 temporal bases: the same steps with the filter bank of
+//   wz_wavelets.h, the gate pooled to each level's detail length by adaptive
+//   average pooling; workgroup version only)
 #pragma once
 
 #include "wz_device.h"
+#include "wz_wavelets.h"
 
 namespace wz {
 namespace {
@@ -33,7 +37,7 @@ template <int TV>
 struct Shared {
   double a[2][TV];              // approximation (ping-pong), then r~ in a[0]
   double g[2][TV];              // gate pooled alongside (ping-pong); g[0] reused for weights
-  double det[TV + kMaxLevels];  // gated detail coefficients of every level
+  double det[TV + 8 * kMaxLevels];  // gated detail coefficients of every level
   int idx[TV];                  // frame index of each retained position
   int n[TV];                    // budget of each retained position
   int fb[TV];                   // budget of each frame
@@ -131,10 +135,11 @@ __device__ int bscan_excl(int v, int& total, Sh& sh) {
 }
 
 // NT threads handle up to TV frames; thread tid owns frames tid*kPer .. tid*kPer+kPer-1.
+// bank: the temporal filter bank (null: Haar).
 template <int NT, int TV>
 __device__ void budget_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
                             long long B, int levels, float tau, int32_t* __restrict__ budget,
-                            int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
+                            int32_t* __restrict__ offset, float* __restrict__ rel_rect, const Bank* bank = nullptr) {
   constexpr int kPer = (TV + NT - 1) / NT;  // frames per thread (contiguous run)
   static_assert(kPer <= 32 && TV <= kTMax, "frame mask holds 32 frames per thread");
   __shared__ Shared<TV> sh;
@@ -173,8 +178,58 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
   }
   bsync<NT>();
 
-  // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)) ------------------------
   int len = L, doff = 0, cur = 0;
+  if (bank) {
+    // ---- WTA with a filter bank: analysis, gate pooled to the detail length,
+    // gated details (Eq. (9)-(10)); every level's coefficients stay within TV
+    // entries (n <= max(len, 8) for F <= 10) ----
+    const int F = bank->F;
+    for (int lev = 0; lev < levels; ++lev) {
+      const int n = bank_len(len, F);
+      if (tid == 0) { sh.lens[lev] = len; sh.doffs[lev] = doff; }
+      const double* A0 = sh.a[cur];
+      const double* G0 = sh.g[cur];
+      for (int k = tid; k < n; k += NT) {
+        double a = 0.0, d = 0.0;
+        for (int j = 0; j < F; ++j) {
+          const double x = A0[sym_index(2 * k + 1 - j, len)];
+          a += bank->dec_lo[j] * x;
+          d += bank->dec_hi[j] * x;
+        }
+        // gate: the mean of G0 over inputs floor(k len / n) .. ceil((k + 1) len / n) - 1
+        const int lo = (k * len) / n, hi = ((k + 1) * len + n - 1) / n;
+        double gs = 0.0;
+        for (int i = lo; i < hi; ++i) gs += G0[i];
+        const double gp = gs / double(hi - lo);
+        sh.a[cur ^ 1][k] = a;
+        sh.g[cur ^ 1][k] = gp;
+        sh.det[doff + k] = gp * d;
+      }
+      bsync<NT>();
+      cur ^= 1;
+      doff += n;
+      len = n;
+    }
+    // ---- inverse (Eq. (11)): each level rebuilt and cropped to its length ----
+    for (int lev = levels - 1; lev >= 0; --lev) {
+      const int plen = sh.lens[lev], n = bank_len(plen, F);
+      const double* A0 = sh.a[cur];
+      const double* D0 = sh.det + sh.doffs[lev];
+      double* A1 = sh.a[cur ^ 1];
+      for (int i = tid; i < plen; i += NT) {
+        double s = 0.0;
+        for (int k = max(0, (i - 1) / 2); k < n; ++k) {  // rec index i + F - 2 - 2k in [0, F)
+          const int f = i + F - 2 - 2 * k;
+          if (f < 0) break;
+          if (f < F) s += bank->rec_lo[f] * A0[k] + bank->rec_hi[f] * D0[k];
+        }
+        A1[i] = s;
+      }
+      bsync<NT>();
+      cur ^= 1;
+    }
+  } else {
+  // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)) ------------------------
   for (int lev = 0; lev < levels; ++lev) {
     const int half = (len + 1) / 2;
     if (tid == 0) { sh.lens[lev] = len; sh.doffs[lev] = doff; }
@@ -206,6 +261,7 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
     }
     bsync<NT>();
     cur ^= 1;
+  }
   }
   const double* rt = sh.a[cur];  // r~ over the retained positions
   double* w = sh.g[cur ^ 1];      // free buffer: weights, then fractional parts

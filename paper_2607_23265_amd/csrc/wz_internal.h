@@ -269,5 +269,12 @@ hipError_t launch_assign_gather(const wz_config& c, const void* X, const float* 
                                 hipStream_t s, const Videos& vs = Videos{});
 // Workgroups per frame of launch_assign_gather for V videos at once.
 int assign_groups_per_frame(const wz_config& c, int V = 1);
+// Selection, spatial modulation with the db4 / bior4.4 filter bank of
+// c.spatial_basis, and compaction, from the scores and the frames' row
+// offsets (each workgroup ranks its frame itself).  Needs
+// filter_assign_supported(c).
+bool filter_assign_supported(const wz_config& c);
+hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
+                                void* out_tokens, int32_t* out_index, hipStream_t s, const Videos& vs = Videos{});
 
 }  // namespace wz

@@ -2,7 +2,9 @@
 // filter of Sec. 3.2.2; Sec. 3.2.3, Eq. (9)-(11)) and the integer frame budgets (Sec. 3.2.4, Eq. (16)
 // under Eq. (5)) in ONE workgroup: one wave when T <= 64, 256 threads up to
 // T = 256, 1024 beyond.  The arithmetic lives in wz_budget.h, which the fused
-// selection and gather kernel runs too.
+// selection and gather kernel runs too.  With a db4 or bior4.4 temporal basis
+// the workgroup version runs at every T (one wave's worth of threads up to
+// T = 64).
 #include "wz_budget.h"
 
 namespace wz {
@@ -17,18 +19,28 @@ struct BudgetArgs {
 };
 static_assert(sizeof(VideoArgs<BudgetArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
-template <int NT, int TV>
+// GENERAL: the filter-bank allocator (bank) instead of the Haar one.
+template <int NT, int TV, bool GENERAL>
 __global__ __launch_bounds__(NT) void k_budget(const VideoArgs<BudgetArgs> va, int T, int N, long long B, int levels,
-                                               float tau) {
+                                               float tau, const Bank bank) {
   const BudgetArgs& a = va.v[blockIdx.y];
-  if constexpr (NT == kWave) budget_wave_body(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
-  else budget_body<NT, TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
+  if constexpr (GENERAL)
+    budget_body<NT, TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect, &bank);
+  else if constexpr (NT == kWave)
+    budget_wave_body(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
+  else
+    budget_body<NT, TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
 }
 
 template <int NT, int TV>
 void launch_k(const wz_config& c, const VideoArgs<BudgetArgs>& va, int V, hipStream_t s) {
-  hipLaunchKernelGGL((k_budget<NT, TV>), dim3(1, V), dim3(NT), 0, s, va, c.T, c.H * c.W, (long long)c.B, c.levels,
-                     c.tau);
+  const Bank bank = c.temporal_basis == WZ_HAAR ? Bank{} : make_bank(c.temporal_basis);
+  if (c.temporal_basis == WZ_HAAR)
+    hipLaunchKernelGGL((k_budget<NT, TV, false>), dim3(1, V), dim3(NT), 0, s, va, c.T, c.H * c.W, (long long)c.B,
+                       c.levels, c.tau, bank);
+  else
+    hipLaunchKernelGGL((k_budget<NT, TV, true>), dim3(1, V), dim3(NT), 0, s, va, c.T, c.H * c.W, (long long)c.B,
+                       c.levels, c.tau, bank);
 }
 
 }  // namespace

@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libwavezip.so")
 
 WZ_F32, WZ_BF16 = 0, 1
 WZ_SELECT, WZ_INTERP = 0, 1
+WZ_HAAR, WZ_DB4, WZ_BIOR44 = 0, 1, 2
+BASIS = {"haar": WZ_HAAR, "db4": WZ_DB4, "bior4.4": WZ_BIOR44}
 _STATUS = {0: "WZ_OK", 1: "WZ_ERR_NULL", 2: "WZ_ERR_ALIGN", 3: "WZ_ERR_SHAPE", 4: "WZ_ERR_DTYPE",
            5: "WZ_ERR_PARAM", 6: "WZ_ERR_BUDGET", 7: "WZ_ERR_WORKSPACE", 8: "WZ_ERR_DEVICE",
            9: "WZ_ERR_SCRATCH"}
@@ -37,7 +39,8 @@ class Config(ctypes.Structure):
                 ("C", ctypes.c_int32), ("Q", ctypes.c_int32), ("in_dtype", ctypes.c_int32),
                 ("out_dtype", ctypes.c_int32), ("levels", ctypes.c_int32), ("B", ctypes.c_int64),
                 ("lambda_", ctypes.c_float), ("tau", ctypes.c_float), ("assign", ctypes.c_int32),
-                ("spatial_levels", ctypes.c_int32)]
+                ("spatial_levels", ctypes.c_int32), ("temporal_basis", ctypes.c_int32),
+                ("spatial_basis", ctypes.c_int32)]
 
 
 _lib = None
@@ -89,10 +92,13 @@ class Problem:
     tau: float = 0.0
     assign: int = 0  # WZ_SELECT; WZ_INTERP for the budget-guided interpolation
     spatial_levels: int = 1  # 2: the two-level spatial modulator (selection only)
+    temporal_basis: int = WZ_HAAR  # WZ_DB4 / WZ_BIOR44: filter bank of the temporal allocator
+    spatial_basis: int = WZ_HAAR   # WZ_DB4 / WZ_BIOR44: filter bank of the spatial modulator
 
     def config(self):
         return Config(self.T, self.H, self.W, self.C, self.Q, self.in_dtype, self.out_dtype, self.levels,
-                      self.B, self.lam, self.tau, self.assign, self.spatial_levels)
+                      self.B, self.lam, self.tau, self.assign, self.spatial_levels, self.temporal_basis,
+                      self.spatial_basis)
 
     @property
     def N(self):
@@ -261,8 +267,9 @@ def to_device(inp, device="cuda:0"):
     return X.contiguous(), q.contiguous()
 
 
-def problem_of(wl, out_dtype=WZ_F32, assign=0, spatial_levels=1):
+def problem_of(wl, out_dtype=WZ_F32, assign=0, spatial_levels=1, temporal_basis=WZ_HAAR, spatial_basis=WZ_HAAR):
     """Problem description of a workload (paper_2607_23265_amd.synth.Workload)."""
     return Problem(T=wl.T, H=wl.H, W=wl.W, C=wl.C, Q=wl.Q, B=wl.B,
                    in_dtype=WZ_BF16 if wl.dtype == "bf16" else WZ_F32, out_dtype=out_dtype,
-                   levels=wl.levels, lam=wl.lam, tau=wl.tau, assign=assign, spatial_levels=spatial_levels)
+                   levels=wl.levels, lam=wl.lam, tau=wl.tau, assign=assign, spatial_levels=spatial_levels,
+                   temporal_basis=temporal_basis, spatial_basis=spatial_basis)

@@ -42,9 +42,10 @@ def test_status_strings(L):
 
 
 def test_config_struct_layout():
-    assert ctypes.sizeof(wz.Config) == 56
+    assert ctypes.sizeof(wz.Config) == 64
     assert wz.Config.B.offset == 32 and wz.Config.lambda_.offset == 40 and wz.Config.tau.offset == 44
     assert wz.Config.assign.offset == 48 and wz.Config.spatial_levels.offset == 52
+    assert wz.Config.temporal_basis.offset == 56 and wz.Config.spatial_basis.offset == 60
 
 
 def test_workspace_bytes(L):
@@ -63,6 +64,9 @@ def test_workspace_bytes(L):
     (dict(B=-1), BUDGET), (dict(B=64 * 196 + 1), BUDGET), (dict(assign=2), PARAM), (dict(assign=-1), PARAM),
     (dict(spatial_levels=3), PARAM), (dict(spatial_levels=-1), PARAM),
     (dict(spatial_levels=2, assign=1), PARAM),
+    (dict(temporal_basis=3), PARAM), (dict(temporal_basis=-1), PARAM), (dict(spatial_basis=3), PARAM),
+    (dict(spatial_basis=1, assign=1), PARAM), (dict(spatial_basis=2, spatial_levels=2), PARAM),
+    (dict(spatial_basis=1, H=65, W=2), SHAPE), (dict(spatial_basis=2, H=40, W=40, B=10), SHAPE),
 ])
 def test_invalid_config(L, kw, code):
     c = cfg(**kw)
