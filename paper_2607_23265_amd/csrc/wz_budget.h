@@ -139,7 +139,8 @@ __device__ int bscan_excl(int v, int& total, Sh& sh) {
 template <int NT, int TV>
 __device__ void budget_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
                             long long B, int levels, float tau, int32_t* __restrict__ budget,
-                            int32_t* __restrict__ offset, float* __restrict__ rel_rect, const Bank* bank = nullptr) {
+                            int32_t* __restrict__ offset, float* __restrict__ rel_rect,
+                            const Bank* bank_in = nullptr) {
   constexpr int kPer = (TV + NT - 1) / NT;  // frames per thread (contiguous run)
   static_assert(kPer <= 32 && TV <= kTMax, "frame mask holds 32 frames per thread");
   __shared__ Shared<TV> sh;
@@ -179,10 +180,14 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
   bsync<NT>();
 
   int len = L, doff = 0, cur = 0;
-  if (bank) {
+  if (bank_in) {
     // ---- WTA with a filter bank: analysis, gate pooled to the detail length,
     // gated details (Eq. (9)-(10)); every level's coefficients stay within TV
-    // entries (n <= max(len, 8) for F <= 10) ----
+    // entries (n <= max(len, 8) for F <= 10); the taps are read from LDS ----
+    __shared__ Bank s_bank;
+    if (tid == 0) s_bank = *bank_in;
+    bsync<NT>();
+    const Bank* bank = &s_bank;
     const int F = bank->F;
     for (int lev = 0; lev < levels; ++lev) {
       const int n = bank_len(len, F);

@@ -52,22 +52,26 @@ struct FilterArgs {
 };
 static_assert(sizeof(VideoArgs<FilterArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
-// 8 channels of a token row as floats.
+// 8 channels of a token row: raw 16-byte vectors (one for bf16, two for
+// fp32) and their widening to floats.
 template <typename In>
-__device__ __forceinline__ void load8(__amdgpu_buffer_rsrc_t r, int off, float (&v)[8]);
-template <>
-__device__ __forceinline__ void load8<uint16_t>(__amdgpu_buffer_rsrc_t r, int off, float (&v)[8]) {
-  const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+struct Raw8 {
+  static constexpr int kV = sizeof(In) == 2 ? 1 : 2;
+  u32x4 v[kV];
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, int off) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) { v[2 * i] = bf16_lo(x[i]); v[2 * i + 1] = bf16_hi(x[i]); }
-}
-template <>
-__device__ __forceinline__ void load8<float>(__amdgpu_buffer_rsrc_t r, int off, float (&v)[8]) {
-  const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-  const u32x4 y = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
+    for (int i = 0; i < kV; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * i, 0, 0);
+  }
+  __device__ __forceinline__ void widen(float (&x)[8]) const {
+    if constexpr (kV == 1) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) { v[i] = __uint_as_float(x[i]); v[4 + i] = __uint_as_float(y[i]); }
-}
+      for (int i = 0; i < 4; ++i) { x[2 * i] = bf16_lo(v[0][i]); x[2 * i + 1] = bf16_hi(v[0][i]); }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { x[i] = __uint_as_float(v[0][i]); x[4 + i] = __uint_as_float(v[1][i]); }
+    }
+  }
+};
 template <typename Out>
 __device__ __forceinline__ void store8(__amdgpu_buffer_rsrc_t r, int off, const float (&v)[8]);
 template <>
@@ -85,15 +89,84 @@ __device__ __forceinline__ void store8<float>(__amdgpu_buffer_rsrc_t r, int off,
                     r, off + 16);
 }
 
-// Bytes of dynamic LDS for a frame of H x W tokens and chunks of kr rows.
-__host__ __device__ inline size_t filter_lds_bytes(int H, int W, int F, int kr) {
+// Dynamic LDS of a frame of H x W tokens and chunks of kr rows: byte offsets
+// of the arrays (the operator rows 16-byte aligned) and the total.
+struct FilterLds {
+  size_t M, kept, G, AH, AW, SH, SW, B, L, bytes;
+};
+__host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr) {
   const size_t N = size_t(H) * W, nh = bank_len(H, F), nw = bank_len(W, F);
-  return N * 24                                   // ranking: key, rank, byrank, gate, order
-         + N * 4 * 2                              // saliency, kept list
-         + nh * nw * 4                            // gates
-         + (2 * nh * H + 2 * nw * W) * 4          // analysis rows, both axes
-         + size_t(kr) * 2 * kMaxAct * W * 4       // partial sums B1, B2
-         + N * kr * 4;                            // operator rows
+  FilterLds o;
+  // the ranking's key, rank, byrank, gate and bin order come first (24 N bytes)
+  o.M = N * 24;                               // saliency M [N]
+  o.kept = o.M + N * 4;                       // kept tokens in raster order [N]
+  o.G = o.kept + N * 4;                       // gates [nh][nw]
+  o.AH = o.G + nh * nw * 4;                   // analysis rows along the height [2][nh][H]
+  o.AW = o.AH + 2 * nh * H * 4;               // along the width [2][nw][W]
+  o.SH = o.AW + 2 * nw * W * 4;               // synthesis weights along the height [2][H][kMaxAct]
+  o.SW = o.SH + 2 * size_t(H) * kMaxAct * 4;  // along the width [2][W][kMaxAct]
+  o.B = o.SW + 2 * size_t(W) * kMaxAct * 4;   // partial sums B1, B2 [kr][2][kMaxAct][W]
+  o.L = (o.B + size_t(kr) * 2 * kMaxAct * W * 4 + 15) / 16 * 16;  // operator rows [N][kr], 16-byte aligned
+  o.bytes = o.L + N * kr * 4;
+  return o;
+}
+
+// The contraction of R operator rows with the frame's slice: a ring of D
+// token rows in flight per wave (16-byte vectors of 8 channels per lane),
+// fp32 accumulation, then the rows written to out_tokens (and, by slice 0,
+// their flat indices).
+struct ContractArgs {
+  __amdgpu_buffer_rsrc_t xres;
+  int xoff, rb, N, KR;
+  const float* L;  // the first row's column of the operator rows [N][KR]
+  int k0, nt;      // the first row's raster position; the frame's kept tokens
+  long long base, total;
+  int C;
+  bool vok;
+  int v, sl, lane, t;
+  const int32_t* kept;
+  void* out_tokens;
+  int32_t* out_index;
+};
+template <typename In, typename Out, int R>
+__device__ __forceinline__ void contract_rows(const ContractArgs& a) {
+  float acc[R][8];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
+  constexpr int D = 16;
+  Raw8<In> ring[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) ring[d].load(a.xres, d < a.N ? d * a.rb + a.xoff : kOOB);
+  for (int n0 = 0; n0 < a.N; n0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int n = n0 + d;
+      float xc[8];
+      ring[d].widen(xc);
+      ring[d].load(a.xres, n + D < a.N ? (n + D) * a.rb + a.xoff : kOOB);
+      if (n < a.N) {
+        const float* Ln = a.L + n * a.KR;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const float l = Ln[r];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(l, xc[e], acc[r][e]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int k = a.k0 + r;
+    if (k < a.nt && a.base + k < a.total) {
+      const __amdgpu_buffer_rsrc_t ores = make_rsrc_uniform(
+          static_cast<Out*>(a.out_tokens) + size_t(a.base + k) * a.C, uint32_t(a.C) * sizeof(Out));
+      if (a.vok) store8<Out>(ores, a.v * 8 * int(sizeof(Out)), acc[r]);
+      if (a.sl == 0 && a.lane == 0) a.out_index[a.base + k] = a.t * (a.N) + a.kept[k];
+    }
+  }
 }
 
 template <typename In, typename Out, int KR>
@@ -126,13 +199,16 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   rl.start = s_start;
   rl.fill = s_fill;
   rl.mm = s_mm;
-  float* s_M = reinterpret_cast<float*>(rl.order + N);  // [N] saliency M
-  int32_t* s_kept = reinterpret_cast<int32_t*>(s_M + N);  // [nt] kept tokens in raster order
-  float* s_G = reinterpret_cast<float*>(s_kept + N);    // [nh][nw] gates
-  float* s_AH = s_G + nh * nw;                          // [2][nh][H] analysis rows along the height
-  float* s_AW = s_AH + 2 * nh * H;                      // [2][nw][W] along the width
-  float* s_B = s_AW + 2 * nw * W;                       // [KR][2][kMaxAct][W]
-  float* s_L = s_B + KR * 2 * kMaxAct * W;              // [N][KR] operator rows, token-major
+  const FilterLds lo_ = filter_lds(H, W, F, KR);
+  float* s_M = reinterpret_cast<float*>(s_dyn + lo_.M);           // [N] saliency M
+  int32_t* s_kept = reinterpret_cast<int32_t*>(s_dyn + lo_.kept);  // [nt] kept tokens in raster order
+  float* s_G = reinterpret_cast<float*>(s_dyn + lo_.G);           // [nh][nw] gates
+  float* s_AH = reinterpret_cast<float*>(s_dyn + lo_.AH);         // [2][nh][H] analysis rows along the height
+  float* s_AW = reinterpret_cast<float*>(s_dyn + lo_.AW);         // [2][nw][W] along the width
+  float* s_SH = reinterpret_cast<float*>(s_dyn + lo_.SH);         // [2][H][kMaxAct] synthesis weights
+  float* s_SW = reinterpret_cast<float*>(s_dyn + lo_.SW);         // [2][W][kMaxAct]
+  float* s_B = reinterpret_cast<float*>(s_dyn + lo_.B);           // [KR][2][kMaxAct][W]
+  float* s_L = reinterpret_cast<float*>(s_dyn + lo_.L);           // [N][KR] operator rows, token-major
 
   // ---- 1. ranks from the scores; kept tokens in raster order ----
   {
@@ -210,17 +286,18 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
     for (int x = 0; x < len; ++x) row[x] = 0.f;
     for (int j = 0; j < F; ++j) row[sym_index(2 * i + 1 - j, len)] += float(u == 0 ? bank.dec_lo[j] : bank.dec_hi[j]);
   }
+  // synthesis weights: coefficient i = x / 2 + ii (the first of at most
+  // kMaxAct whose filter reaches x) of band u at output position x,
+  // rec_u[x + F - 2 - 2i], 0 outside the filter or past the band
+  for (int q = tid; q < 2 * (H + W) * kMaxAct; q += kFThreads) {
+    const bool height = q < 2 * H * kMaxAct;
+    const int r = height ? q : q - 2 * H * kMaxAct, len = height ? H : W, n = height ? nh : nw;
+    const int u = r / (len * kMaxAct), x = (r / kMaxAct) % len, ii = r % kMaxAct;
+    const int i = x / 2 + ii, k = x + F - 2 - 2 * i;
+    (height ? s_SH : s_SW)[r] =
+        (i < n && k >= 0 && k < F) ? float(u == 0 ? bank.rec_lo[k] : bank.rec_hi[k]) : 0.f;
+  }
   __syncthreads();
-
-  // synthesis weight of coefficient i (band u) at output position x of an
-  // axis; 0 outside the filter
-  auto syn = [&](int u, int x, int i) {
-    const int k = x + F - 2 - 2 * i;
-    return (k >= 0 && k < F) ? float(u == 0 ? bank.rec_lo[k] : bank.rec_hi[k]) : 0.f;
-  };
-  // first coefficient whose synthesis filter reaches position x (at most
-  // kMaxAct of them, up to i0 + kMaxAct - 1)
-  auto first_coef = [](int x) { return x >= 1 ? x / 2 : 0; };
 
   const int nvec = C / 8;  // 8-channel vectors of a row
   const int v = sl * kWave + lane;
@@ -237,14 +314,14 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       float b1 = 0.f, b2 = 0.f;
       if (c0 + r < nt) {
         const int p = s_kept[c0 + r], h = p / W, w = p - h * W;
-        const int i = first_coef(h) + ii;
+        const int i = h / 2 + ii;
         if (i < nh) {
-          const int j0 = first_coef(w);
+          const int j0 = w / 2;
+#pragma unroll
           for (int jj = 0; jj < kMaxAct; ++jj) {
-            const int j = j0 + jj;
-            if (j >= nw) break;
-            const float e = syn(0, w, j) * s_AW[j * W + x];
-            const float pp = e + syn(1, w, j) * s_AW[(nw + j) * W + x];
+            const int j = min(j0 + jj, nw - 1);  // weights past the band are 0
+            const float e = s_SW[(0 * W + w) * kMaxAct + jj] * s_AW[j * W + x];
+            const float pp = e + s_SW[(1 * W + w) * kMaxAct + jj] * s_AW[(nw + j) * W + x];
             const float g = s_G[i * nw + j];
             b1 += (1.f - g) * e;
             b2 += g * pp;
@@ -255,65 +332,73 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       s_B[((r * 2 + 1) * kMaxAct + ii) * W + x] = b2;
     }
     __syncthreads();
-    // ---- 3b. L_p(h', w') = sum_i E_i(h') B1_i(w') + P_i(h') B2_i(w') ----
-    for (int q = tid; q < N * KR; q += kFThreads) {
-      const int n = q / KR, r = q - n * KR, y = n / W, x = n - y * W;
-      float s = 0.f;
-      if (c0 + r < nt) {
-        const int p = s_kept[c0 + r], h = p / W;
-        const int i0 = first_coef(h);
+    // ---- 3b. L_p(h', w') = sum_i E_i(h') B1_i(w') + P_i(h') B2_i(w'): thread
+    // tid builds row tid % KR at tokens tid / KR, + 256 / KR, ... ----
+    {
+      const int r = tid % KR, nstep = kFThreads / KR;
+      const bool live = c0 + r < nt;
+      float ew[kMaxAct], pw[kMaxAct];
+      int ih[kMaxAct];
+      const int h = live ? s_kept[c0 + r] / W : 0;
+#pragma unroll
+      for (int ii = 0; ii < kMaxAct; ++ii) {
+        ih[ii] = min(h / 2 + ii, nh - 1);  // weights past the band are 0
+        ew[ii] = live ? s_SH[(0 * H + h) * kMaxAct + ii] : 0.f;
+        pw[ii] = live ? s_SH[(1 * H + h) * kMaxAct + ii] : 0.f;
+      }
+      const float* B1 = s_B + (r * 2 + 0) * kMaxAct * W;
+      const float* B2 = s_B + (r * 2 + 1) * kMaxAct * W;
+      int n = tid / KR, y = n / W, x = n - y * W;
+      const int dy = nstep / W, dx = nstep - dy * W;
+      for (; n < N; n += nstep) {
+        float acc = 0.f;
+#pragma unroll
         for (int ii = 0; ii < kMaxAct; ++ii) {
-          const int i = i0 + ii;
-          if (i >= nh) break;
-          const float e = syn(0, h, i) * s_AH[i * H + y];
-          const float pp = e + syn(1, h, i) * s_AH[(nh + i) * H + y];
-          s += e * s_B[((r * 2 + 0) * kMaxAct + ii) * W + x] + pp * s_B[((r * 2 + 1) * kMaxAct + ii) * W + x];
+          const float e = ew[ii] * s_AH[ih[ii] * H + y];
+          const float pp = e + pw[ii] * s_AH[(nh + ih[ii]) * H + y];
+          acc += e * B1[ii * W + x] + pp * B2[ii * W + x];
+        }
+        s_L[n * KR + r] = acc;
+        x += dx;
+        y += dy;
+        if (x >= W) {
+          x -= W;
+          ++y;
         }
       }
-      s_L[q] = s;
     }
     __syncthreads();
-    // ---- 3c. the wave's RW rows against the frame's slice ----
-    float acc[RW][8];
-#pragma unroll
-    for (int r = 0; r < RW; ++r)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
-    constexpr int D = 4;  // tokens whose loads are in flight ahead
-    float xv[D][8];
-#pragma unroll
-    for (int d = 0; d < D; ++d) load8<In>(xres, d < N ? d * rb + xoff : kOOB, xv[d]);
-    for (int n0 = 0; n0 < N; n0 += D) {
-#pragma unroll
-      for (int d = 0; d < D; ++d) {
-        const int n = n0 + d;
-        float xc[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) xc[e] = xv[d][e];
-        load8<In>(xres, n + D < N ? (n + D) * rb + xoff : kOOB, xv[d]);
-        if (n < N) {
-          const float* Lr = s_L + n * KR + wave * RW;
-#pragma unroll
-          for (int r = 0; r < RW; ++r) {
-            const float l = Lr[r];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(l, xc[e], acc[r][e]);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      const int k = c0 + wave * RW + r;
-      if (k < nt && base + k < total) {
-        const __amdgpu_buffer_rsrc_t ores = make_rsrc_uniform(
-            static_cast<Out*>(f.out_tokens) + size_t(base + k) * C, uint32_t(C) * sizeof(Out));
-        if (vok) store8<Out>(ores, v * 8 * int(sizeof(Out)), acc[r]);
-        if (sl == 0 && lane == 0) f.out_index[base + k] = t * N + s_kept[k];
+    // ---- 3c. the chunk's rows against the frame's slice, spread evenly over
+    // the waves (a wave with R rows runs the R-row contraction) ----
+    {
+      const int nr = min(KR, nt - c0), rw = (nr + kFWaves - 1) / kFWaves;
+      const int row0 = wave * rw, mine = max(0, min(rw, nr - row0));
+      ContractArgs ca{xres, xoff, rb, N, KR, s_L + row0, c0 + row0, nt, base, total, C, vok, v, sl, lane, t,
+                      s_kept, f.out_tokens, f.out_index};
+      switch (mine) {
+        case 1: contract_rows<In, Out, 1>(ca); break;
+        case 2: contract_rows<In, Out, 2>(ca); break;
+        case 3: contract_rows<In, Out, 3>(ca); break;
+        case 4: contract_rows<In, Out, 4>(ca); break;
+        case 5: if constexpr (RW >= 5) contract_rows<In, Out, 5>(ca); break;
+        case 6: if constexpr (RW >= 6) contract_rows<In, Out, 6>(ca); break;
+        case 7: if constexpr (RW >= 7) contract_rows<In, Out, 7>(ca); break;
+        case 8: if constexpr (RW >= 8) contract_rows<In, Out, 8>(ca); break;
+        default: break;
       }
     }
     __syncthreads();  // the next chunk rewrites B and L
   }
+}
+
+// dynamic LDS a workgroup may take (the static arrays use about 2 KB)
+constexpr size_t kFilterLdsMax = (160 - 4) * 1024;
+
+// rows per chunk: the most (32, 16 or 8) whose LDS fits
+int filter_rows(int H, int W, int F) {
+  for (int kr = 32; kr >= 8; kr /= 2)
+    if (filter_lds(H, W, F, kr).bytes <= kFilterLdsMax) return kr;
+  return 0;
 }
 
 template <typename In, typename Out>
@@ -321,18 +406,17 @@ void launch_filter_typed(const wz_config& c, const VideoArgs<FilterArgs>& va, in
                          hipStream_t s) {
   const int S = (c.C + kFSlice - 1) / kFSlice;
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
-  if (c.H * c.W <= 512)
-    hipLaunchKernelGGL((k_filter_assign<In, Out, 32>), grid, block, filter_lds_bytes(c.H, c.W, bank.F, 32), s, va,
-                       bank);
-  else
-    hipLaunchKernelGGL((k_filter_assign<In, Out, 16>), grid, block, filter_lds_bytes(c.H, c.W, bank.F, 16), s, va,
-                       bank);
+  const int kr = filter_rows(c.H, c.W, bank.F);
+  const size_t lds = filter_lds(c.H, c.W, bank.F, kr).bytes;
+  if (kr == 32) hipLaunchKernelGGL((k_filter_assign<In, Out, 32>), grid, block, lds, s, va, bank);
+  else if (kr == 16) hipLaunchKernelGGL((k_filter_assign<In, Out, 16>), grid, block, lds, s, va, bank);
+  else hipLaunchKernelGGL((k_filter_assign<In, Out, 8>), grid, block, lds, s, va, bank);
 }
 
 }  // namespace
 
 bool filter_assign_supported(const wz_config& c) {
-  return c.H <= 64 && c.W <= 64 && c.H * c.W <= 1024;
+  return c.H <= 64 && c.W <= 64 && c.H * c.W <= 1024 && filter_rows(c.H, c.W, kMaxTaps) > 0;
 }
 
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,

@@ -63,12 +63,12 @@ __host__ __device__ inline Bank make_bank(int basis) {
   return b;
 }
 
-// Position of sample i of the half-sample symmetric extension of L samples.
+// Position of sample i of the half-sample symmetric extension of L samples
+// (reflections about -1/2 and L - 1/2; more than one only when L is shorter
+// than the filter).
 __host__ __device__ inline int sym_index(int i, int L) {
-  const int P = 2 * L;
-  i %= P;
-  if (i < 0) i += P;
-  return i < L ? i : P - 1 - i;
+  while (i < 0 || i >= L) i = i < 0 ? -1 - i : 2 * L - 1 - i;
+  return i;
 }
 
 // Analysis coefficients per band for L samples.
