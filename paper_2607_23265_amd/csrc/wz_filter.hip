@@ -22,11 +22,14 @@
 //      n_t kept tokens (rank < n_t) in raster order;
 //   2. forms G and the per-axis analysis rows a_u in LDS;
 //   3. per chunk of KR kept tokens builds their rows L_p in LDS (fp32,
-//      through the partial sums B_i(w') = sum_j over the width), then each of
-//      the 4 waves contracts KR / 4 of them with the frame's slice, one
-//      16-byte vector of 8 channels per lane (fp32 accumulation), and writes
-//      the rows to out_tokens[offset_t + k] (k = raster position among the
-//      kept tokens), their flat indices to out_index.
+//      through the partial sums B_i(w') = sum_j over the width) and
+//      contracts them with the frame's slice, a dense product of KR rows,
+//      H*W tokens and 512 channels: for bf16 inputs on MFMA (the rows split
+//      into bf16 high and low parts, fp32 accumulation; each wave takes 128
+//      channels), for fp32 inputs on the vector ALU (each wave takes a
+//      quarter of the rows, fp32); then writes the rows to
+//      out_tokens[offset_t + k] (k = raster position among the kept tokens),
+//      their flat indices to out_index.
 // The frame's slice is read once per chunk of KR kept tokens (from L2 after
 // the first).  Supported: H, W <= 64, H*W <= 1024 (the host checks).
 #include "wz_rank.h"
@@ -94,7 +97,15 @@ __device__ __forceinline__ void store8<float>(__amdgpu_buffer_rsrc_t r, int off,
 struct FilterLds {
   size_t M, kept, G, AH, AW, SH, SW, B, L, bytes;
 };
-__host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr) {
+// Tokens padded to whole MFMA K steps, and the row stride (bf16 elements) of
+// the operator rows in their MFMA form: 8 more than the padded length, so the
+// 16 rows that 16 lanes read at once fall in distinct LDS banks.
+__host__ __device__ inline int pad_tokens(int N) { return (N + 31) / 32 * 32; }
+__host__ __device__ inline int mfma_row_stride(int N) { return pad_tokens(N) + 8; }
+// mfma: the operator rows as bf16 high and low parts
+// [2][max(kr, 16)][mfma_row_stride] (bf16 inputs; whole 16-row MFMA tiles)
+// instead of fp32 [N][kr].
+__host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr, bool mfma) {
   const size_t N = size_t(H) * W, nh = bank_len(H, F), nw = bank_len(W, F);
   FilterLds o;
   // the ranking's key, rank, byrank, gate and bin order come first (24 N bytes)
@@ -107,7 +118,7 @@ __host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr) {
   o.SW = o.SH + 2 * size_t(H) * kMaxAct * 4;  // along the width [2][W][kMaxAct]
   o.B = o.SW + 2 * size_t(W) * kMaxAct * 4;   // partial sums B1, B2 [kr][2][kMaxAct][W]
   o.L = (o.B + size_t(kr) * 2 * kMaxAct * W * 4 + 15) / 16 * 16;  // operator rows [N][kr], 16-byte aligned
-  o.bytes = o.L + N * kr * 4;
+  o.bytes = o.L + (mfma ? size_t(2) * (kr < 16 ? 16 : kr) * mfma_row_stride(int(N)) * 2 : N * kr * 4);
   return o;
 }
 
@@ -199,7 +210,8 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   rl.start = s_start;
   rl.fill = s_fill;
   rl.mm = s_mm;
-  const FilterLds lo_ = filter_lds(H, W, F, KR);
+  constexpr bool MF = sizeof(In) == 2;  // bf16 inputs: the contraction runs on MFMA
+  const FilterLds lo_ = filter_lds(H, W, F, KR, MF);
   float* s_M = reinterpret_cast<float*>(s_dyn + lo_.M);           // [N] saliency M
   int32_t* s_kept = reinterpret_cast<int32_t*>(s_dyn + lo_.kept);  // [nt] kept tokens in raster order
   float* s_G = reinterpret_cast<float*>(s_dyn + lo_.G);           // [nh][nw] gates
@@ -209,6 +221,9 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   float* s_SW = reinterpret_cast<float*>(s_dyn + lo_.SW);         // [2][W][kMaxAct]
   float* s_B = reinterpret_cast<float*>(s_dyn + lo_.B);           // [KR][2][kMaxAct][W]
   float* s_L = reinterpret_cast<float*>(s_dyn + lo_.L);           // [N][KR] operator rows, token-major
+  uint16_t* s_Lh = reinterpret_cast<uint16_t*>(s_dyn + lo_.L);    // MFMA form: [2][LR][LS] bf16 high, low
+  constexpr int LR = KR < 16 ? 16 : KR;                            // rows of a part: whole 16-row tiles
+  const int LS = mfma_row_stride(N), NP = pad_tokens(N);
 
   // ---- 1. ranks from the scores; kept tokens in raster order ----
   {
@@ -299,6 +314,12 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   }
   __syncthreads();
 
+  if constexpr (MF && KR < LR) {  // rows KR .. 15 of each part stay zero
+    for (int q = tid; q < 2 * (LR - KR) * LS; q += kFThreads) {
+      const int part = q / ((LR - KR) * LS), rem = q - part * (LR - KR) * LS;
+      s_Lh[(part * LR + KR) * LS + rem] = 0;
+    }
+  }
   const int nvec = C / 8;  // 8-channel vectors of a row
   const int v = sl * kWave + lane;
   const bool vok = v < nvec;
@@ -350,15 +371,25 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       const float* B2 = s_B + (r * 2 + 1) * kMaxAct * W;
       int n = tid / KR, y = n / W, x = n - y * W;
       const int dy = nstep / W, dx = nstep - dy * W;
-      for (; n < N; n += nstep) {
+      for (; n < (MF ? NP : N); n += nstep) {
         float acc = 0.f;
+        if (n < N) {
 #pragma unroll
-        for (int ii = 0; ii < kMaxAct; ++ii) {
-          const float e = ew[ii] * s_AH[ih[ii] * H + y];
-          const float pp = e + pw[ii] * s_AH[(nh + ih[ii]) * H + y];
-          acc += e * B1[ii * W + x] + pp * B2[ii * W + x];
+          for (int ii = 0; ii < kMaxAct; ++ii) {
+            const float e = ew[ii] * s_AH[ih[ii] * H + y];
+            const float pp = e + pw[ii] * s_AH[(nh + ih[ii]) * H + y];
+            acc += e * B1[ii * W + x] + pp * B2[ii * W + x];
+          }
         }
-        s_L[n * KR + r] = acc;
+        if constexpr (MF) {
+          // bf16 high part and the rounded remainder: together about 16
+          // significant bits of the row entry (tokens past N are 0)
+          const uint32_t hi = f32_to_bf16_rne(acc);
+          s_Lh[r * LS + n] = uint16_t(hi);
+          s_Lh[(LR + r) * LS + n] = uint16_t(f32_to_bf16_rne(acc - __uint_as_float(hi << 16)));
+        } else {
+          s_L[n * KR + r] = acc;
+        }
         x += dx;
         y += dy;
         if (x >= W) {
@@ -368,9 +399,91 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       }
     }
     __syncthreads();
-    // ---- 3c. the chunk's rows against the frame's slice, spread evenly over
-    // the waves (a wave with R rows runs the R-row contraction) ----
-    {
+    // ---- 3c. the chunk's rows against the frame's slice ----
+    if constexpr (MF) {
+      // MFMA: C[rows][channels] += L[rows][tokens] X[tokens][channels] with
+      // v_mfma_f32_16x16x32_bf16, the wave's 128 channels in 8 MFMAs per
+      // 16-row tile and 32-token step.  Lane (r16, g) = (lane % 16, lane / 16)
+      // loads tokens 8g .. 8g+7 of the step for its 8 channels 8 r16 .. 8 r16+7
+      // and transposes the 8 x 8 block in registers: w[c'] holds the 8 tokens
+      // of channel 8 r16 + c', which is exactly the B operand (8 K values of
+      // column r16) of MFMA c', whose columns are channels 8 r16 + c'.  The A
+      // operand is the rows' bf16 high or low part, 8 tokens from LDS.  Lane
+      // (r16, g) ends with rows 4g .. 4g+3 of each tile for its 8 consecutive
+      // channels.
+      const int nr = min(KR, nt - c0);
+      constexpr int RT = (KR + 15) / 16;  // 16-row tiles
+      const int rtiles = (nr + 15) / 16;
+      const int r16 = lane & 15, g = lane >> 4;
+      const int cw = sl * kFSlice + wave * 128 + 8 * r16;  // the lane's first channel
+      const int coff = cw < C ? cw * 2 : kOOB;
+      f32x4 acc[RT][8];
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      u32x4 xr[8];  // tokens 8g + e of the current step, channels 8 r16 .. +7
+      auto load_step = [&](int k0, u32x4 (&d)[8]) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int n = k0 + 8 * g + e;
+          d[e] = __builtin_amdgcn_raw_buffer_load_b128(xres, (n < N && coff != kOOB) ? n * rb + coff : kOOB, 0, 0);
+        }
+      };
+      load_step(0, xr);
+      for (int k0 = 0; k0 < NP; k0 += 32) {
+        u32x4 xn[8];
+        load_step(k0 + 32, xn);  // past the frame: zeros
+        // 8 x 8 transpose of bf16: w[c'] dword j = tokens (2j, 2j+1) of channel c'
+        u32x4 w[8];
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            w[2 * m][j] = __builtin_amdgcn_perm(xr[2 * j + 1][m], xr[2 * j][m], 0x05040100u);
+            w[2 * m + 1][j] = __builtin_amdgcn_perm(xr[2 * j + 1][m], xr[2 * j][m], 0x07060302u);
+          }
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+          if (i >= rtiles) break;
+          const int row = 16 * i + r16;
+          const bf16x8 ah = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(s_Lh + row * LS + k0 + 8 * g));
+          const bf16x8 al =
+              __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(s_Lh + (LR + row) * LS + k0 + 8 * g));
+#pragma unroll
+          for (int c = 0; c < 8; ++c) {
+            const bf16x8 bw = __builtin_bit_cast(bf16x8, w[c]);
+            acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw, acc[i][c], 0, 0, 0);
+            acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw, acc[i][c], 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xr[e] = xn[e];
+      }
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        if (i >= rtiles) break;
+        // one descriptor per 16-row tile (the lanes' rows differ); its size
+        // stops at the last row the call may write
+        const long long row0 = base + c0 + 16 * i;
+        const long long rows = min(16LL, total - row0);
+        const __amdgpu_buffer_rsrc_t ores = make_rsrc_uniform(
+            static_cast<Out*>(f.out_tokens) + size_t(row0) * C, rows > 0 ? uint32_t(rows * C * sizeof(Out)) : 0u);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int rt = 4 * g + e, k = c0 + 16 * i + rt;
+          if (k < nt && base + k < total) {
+            float y8[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) y8[c] = acc[i][c][e];
+            if (cw < C) store8<Out>(ores, (rt * C + cw) * int(sizeof(Out)), y8);
+            if (sl == 0 && wave == 0 && r16 == 0) f.out_index[base + k] = t * N + s_kept[k];
+          }
+        }
+      }
+    } else {
+      // VALU (fp32 inputs): the chunk's rows spread evenly over the waves (a
+      // wave with R rows runs the R-row contraction)
       const int nr = min(KR, nt - c0), rw = (nr + kFWaves - 1) / kFWaves;
       const int row0 = wave * rw, mine = max(0, min(rw, nr - row0));
       ContractArgs ca{xres, xoff, rb, N, KR, s_L + row0, c0 + row0, nt, base, total, C, vok, v, sl, lane, t,
@@ -395,9 +508,9 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
 constexpr size_t kFilterLdsMax = (160 - 4) * 1024;
 
 // rows per chunk: the most (32, 16 or 8) whose LDS fits
-int filter_rows(int H, int W, int F) {
+int filter_rows(int H, int W, int F, bool mfma) {
   for (int kr = 32; kr >= 8; kr /= 2)
-    if (filter_lds(H, W, F, kr).bytes <= kFilterLdsMax) return kr;
+    if (filter_lds(H, W, F, kr, mfma).bytes <= kFilterLdsMax) return kr;
   return 0;
 }
 
@@ -406,8 +519,9 @@ void launch_filter_typed(const wz_config& c, const VideoArgs<FilterArgs>& va, in
                          hipStream_t s) {
   const int S = (c.C + kFSlice - 1) / kFSlice;
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
-  const int kr = filter_rows(c.H, c.W, bank.F);
-  const size_t lds = filter_lds(c.H, c.W, bank.F, kr).bytes;
+  constexpr bool mfma = sizeof(In) == 2;
+  const int kr = filter_rows(c.H, c.W, bank.F, mfma);
+  const size_t lds = filter_lds(c.H, c.W, bank.F, kr, mfma).bytes;
   if (kr == 32) hipLaunchKernelGGL((k_filter_assign<In, Out, 32>), grid, block, lds, s, va, bank);
   else if (kr == 16) hipLaunchKernelGGL((k_filter_assign<In, Out, 16>), grid, block, lds, s, va, bank);
   else hipLaunchKernelGGL((k_filter_assign<In, Out, 8>), grid, block, lds, s, va, bank);
@@ -416,7 +530,8 @@ void launch_filter_typed(const wz_config& c, const VideoArgs<FilterArgs>& va, in
 }  // namespace
 
 bool filter_assign_supported(const wz_config& c) {
-  return c.H <= 64 && c.W <= 64 && c.H * c.W <= 1024 && filter_rows(c.H, c.W, kMaxTaps) > 0;
+  return c.H <= 64 && c.W <= 64 && c.H * c.W <= 1024 && filter_rows(c.H, c.W, kMaxTaps, true) > 0 &&
+         filter_rows(c.H, c.W, kMaxTaps, false) > 0;
 }
 
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
