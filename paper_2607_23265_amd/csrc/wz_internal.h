@@ -57,11 +57,15 @@ constexpr int kTokMax = 4096;     // validated bound on tokens per frame
 inline int qpad(int Q) { return (Q + 3) & ~3; }
 
 // Streaming kernels of the relevance pass, chosen by shape:
-//   kRelTok  bf16, Q <= 256: token tiles with every channel, LDS-transposed
+//   kRelTok  bf16, Q <= 64 or 128 < Q <= 256: token tiles with every
+//            channel, each wave a channel stripe with its own LDS-transposed
 //            MFMA (above 64 query tokens, passes of 32 columns per tile);
+//   kRelWg   bf16, 64 < Q <= 128: token tiles with every channel, the
+//            workgroup's waves sharing each channel chunk of the tile and the
+//            query in LDS, each wave some 16-row tiles against every column;
 //   kRelMfma bf16, Q > 256, frames of >= 49 tokens: MFMA-layout loads;
 //   kRelValu everything else (fp32 inputs, small frames with many queries).
-enum RelKind { kRelValu = 0, kRelMfma = 1, kRelTok = 2 };
+enum RelKind { kRelValu = 0, kRelMfma = 1, kRelTok = 2, kRelWg = 3 };
 RelKind relevance_kind(const wz_config& c);
 
 struct RelPlan {
@@ -74,7 +78,8 @@ struct RelPlan {
   int grid;         // workgroups: frames rounded up to a multiple of kXcds, x tiles x slices
   int threads;      // threads per workgroup
   int ipc;          // kRelTok: row load instructions per chunk (tile rows / 8)
-  int ntg;          // kRelTok: 16-column query tiles
+  int ntg;          // kRelTok, kRelWg: 16-column query tiles
+  int rtw;          // kRelWg: 16-row tiles per wave (tiles of up to 64 * rtw tokens)
 };
 
 inline RelPlan relevance_plan(const wz_config& c) {
@@ -104,6 +109,26 @@ inline RelPlan relevance_plan(const wz_config& c) {
     p.slices = 1;
     p.kc = c.C;
     p.threads = 8 * 64;
+  } else if (p.kind == kRelWg) {
+    // tiles of at most 128 tokens; two workgroups share a CU.  Every
+    // workgroup streams its tile's rows and the whole query through LDS:
+    // take the tile count with the fewest rows streamed per CU slot, the
+    // smaller count on a tie
+    const int tr = (c.T + kXcds - 1) / kXcds * kXcds;
+    p.ntg = c.Q <= 16 ? 1 : c.Q <= 32 ? 2 : c.Q <= 64 ? 4 : 8;
+    const int lo = (N + 127) / 128, hi = std::max(lo, (N + 15) / 16);
+    long best = -1;
+    for (int k = lo; k <= hi; ++k) {
+      const int rows = (N + k - 1) / k + 16 * p.ntg;
+      const long cost = long((long(tr) * k + 2 * kCUs - 1) / (2 * kCUs)) * rows;
+      if (best < 0 || cost < best) best = cost, p.tiles = k;
+    }
+    p.tile_tokens = (N + p.tiles - 1) / p.tiles;
+    p.rtw = p.tile_tokens <= 64 ? 1 : 2;
+    p.mt = 0;
+    p.slices = 1;
+    p.kc = c.C;
+    p.threads = 256;
   } else if (p.kind == kRelMfma) {
     const int cap = 16 * kMaxWaves;
     p.tiles = (N + cap - 1) / cap;

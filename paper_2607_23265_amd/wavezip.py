@@ -24,7 +24,7 @@ _STATUS = {0: "WZ_OK", 1: "WZ_ERR_NULL", 2: "WZ_ERR_ALIGN", 3: "WZ_ERR_SHAPE", 4
            9: "WZ_ERR_SCRATCH"}
 EXPORTS = ("wz_workspace_bytes", "wz_relevance", "wz_relevance_pass", "wz_temporal_budget",
            "wz_spatial_dwt_condense", "wz_condense", "wz_condense_batch", "wz_condense_queries",
-           "wz_condense_noalloc", "wz_noalloc_scratch_bytes", "wz_status_str")
+           "wz_condense_noalloc", "wz_noalloc_scratch_bytes", "wz_status_str", "wz_probe_stream_read")
 
 
 class WZError(RuntimeError):
@@ -66,6 +66,8 @@ def lib():
     L.wz_spatial_dwt_condense.argtypes = [cfgp, P, P, P, P, P, P]
     L.wz_condense.argtypes = [cfgp, P, P, P, P, P, P, P, S, P]
     L.wz_condense_noalloc.argtypes = [cfgp, P, P, P, P, P, P, P]
+    L.wz_probe_stream_read.argtypes = [P, S, P, P]
+    L.wz_probe_stream_read.restype = ctypes.c_int
     L.wz_noalloc_scratch_bytes.argtypes = []
     L.wz_noalloc_scratch_bytes.restype = S
     for f in ("wz_relevance", "wz_relevance_pass", "wz_temporal_budget", "wz_spatial_dwt_condense", "wz_condense",
@@ -214,6 +216,13 @@ def condense_noalloc(p: Problem, X, query, out=None):
     _check(lib().wz_condense_noalloc(ctypes.byref(cfg), _ptr(X), _ptr(query), _ptr(tok), _ptr(idx), _ptr(b), _ptr(o),
                                      _stream(dev)), "wz_condense_noalloc")
     return tok, idx, b, o
+
+
+def probe_stream_read(data, sink):
+    """wz_probe_stream_read: one plain streaming read of a device tensor (a measurement aid)."""
+    _require_device(data, sink)
+    _check(lib().wz_probe_stream_read(_ptr(data), data.numel() * data.element_size(), _ptr(sink), _stream(data.device)),
+           "wz_probe_stream_read")
 
 
 def condense_batch(p: Problem, X, query, ws=None, out=None):

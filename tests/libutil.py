@@ -5,7 +5,7 @@ import re
 from paper_2607_23265_amd import wavezip
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "wavezip.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("wavezip.h", "wavezip_probe.h")]
 
 
 def ensure_built():
@@ -16,7 +16,7 @@ def ensure_built():
 
 
 def declared_functions():
-    """Names of the functions include/wavezip.h declares."""
-    text = open(HEADER).read()
+    """Names of the functions the headers under include/ declare."""
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(wz_[a-z_]+)\s*\(", text)))
