@@ -361,6 +361,9 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   const uint16_t* __restrict__ query = static_cast<const uint16_t*>(f.query);
   constexpr int NQ = NTG * 16;  // query rows of the accumulators
   constexpr int QI = NQ / 8;    // query load instructions per chunk
+  // chunks of loads in flight per wave: two (eight waves keep 16 chunks of
+  // the tile in flight; deeper rings measured slower)
+  constexpr int D = 2;
   // per-wave chunk buffers (16-byte units swizzled by row): rows 0 .. 63 of a
   // wave's region stage its tile rows, rows 64 .. 64 + NQ - 1 its query rows;
   // after the loop the region holds the wave's partial S [64 rows][NQ] floats
@@ -399,16 +402,15 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
       bf16x8 x[IPC];
       bf16x8 q[QI];
     };
+    // (query rows past Qh lie past the end of qres and read zeros; a per-lane
+    // row test here would become a branch around the load)
     auto issue = [&](int c, Slot& d) {
       const int cc = c * kTokChunk + 8 * lu;
       const bool ok = c < nch && cc < C;
 #pragma unroll
       for (int k = 0; k < IPC; ++k) d.x[k] = buf_load_bf16x8(xres, ok ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
 #pragma unroll
-      for (int k = 0; k < QI; ++k) {
-        const int j = 8 * k + lr;
-        d.q[k] = buf_load_bf16x8(qres, (ok && j < Qh) ? (j * C + cc) * 2 : kOOB);
-      }
+      for (int k = 0; k < QI; ++k) d.q[k] = buf_load_bf16x8(qres, ok ? (8 * k + lr) * C * 2 + cc * 2 : kOOB);
     };
 
     f32x4 Sacc[4][NTG];
@@ -491,33 +493,36 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     // rows this wave never loads (8 * IPC .. 63) are zero in its buffer
     for (int u = 8 * IPC * 8 + lane; u < kTokRows * 8; u += kWave) (&s_xq[wave][0][0])[u] = u32x4{0u, 0u, 0u, 0u};
 
-    // The loads are issued in slot order (A, then B) before and in the loop,
-    // and the norms' updates are pinned before a slot's reload: otherwise the
-    // slot needs a second register set and a copy at the end of the loop, and
-    // the compiler waits for the whole ring once per iteration.
+    // A ring of D slots: the wave's chunks c, c + 8, ..., c + 8 (D - 1) are in
+    // flight while it works on the oldest.  The loads are issued in slot
+    // order before and in the loop, and the norms' updates are pinned before
+    // a slot's reload: otherwise the slot needs a second register set and a
+    // copy at the end of the loop, and the compiler waits for the whole ring
+    // once per iteration.
     auto pin = [&]() {
 #pragma unroll
       for (int k = 0; k < IPC; ++k) asm volatile("" : "+v"(xx[k]));
 #pragma unroll
       for (int k = 0; k < QI; ++k) asm volatile("" : "+v"(qq[k]));
     };
-    Slot A, B;
-    issue(wave, A);
-    __builtin_amdgcn_sched_barrier(0);
-    issue(wave + kTokWaves, B);
-    for (int c = wave; c < nch; c += 2 * kTokWaves) {
+    Slot ring[D];
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+      issue(wave + s * kTokWaves, ring[s]);
       __builtin_amdgcn_sched_barrier(0);
-      consume(c, A);
-      pin();
-      contract();
-      issue(c + 2 * kTokWaves, A);
-      __builtin_amdgcn_sched_barrier(0);
-      if (c + kTokWaves < nch) {
-        consume(c + kTokWaves, B);
-        pin();
-        contract();
+    }
+    for (int c0 = wave; c0 < nch; c0 += D * kTokWaves) {
+#pragma unroll
+      for (int s = 0; s < D; ++s) {
+        const int c = c0 + s * kTokWaves;
+        __builtin_amdgcn_sched_barrier(0);
+        if (c < nch) {
+          consume(c, ring[s]);
+          pin();
+          contract();
+        }
+        issue(c + D * kTokWaves, ring[s]);
       }
-      issue(c + 3 * kTokWaves, B);
     }
 
     // ---- epilogue: waves added in order; LDS-only barriers, so nothing waits
@@ -647,34 +652,40 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
 // Workgroup-shared token tiles (bf16, 64 < Q <= 128)
 // ---------------------------------------------------------------------------
 // With a wide query, per-wave channel stripes (above) would stage the query
-// once per wave and add every wave's partial S through LDS.  Here the four
+// once per wave and add every wave's partial S through LDS.  Here the eight
 // waves of a workgroup share each 64-channel chunk: the tile's rows (up to
-// 64 * RTW tokens) and the query's rows (16 * NQT columns) are loaded once per
-// workgroup (one 16-byte unit per thread and row group, whole cache lines),
-// staged in a double-buffered LDS stage (16-byte units XOR-swizzled by row),
-// and each wave contracts its own 16-row tiles (w, w + 4) against every query
-// column: a_{t,n} is final in the wave that owns the row, and S needs no
-// cross-wave sum.  |x|^2, |q_j|^2 and the chunk's channel sums come from the
+// 64 * RTW tokens) and the query's 128 rows are loaded once per workgroup
+// (one 16-byte unit per thread and row group, whole cache lines), staged in a
+// double-buffered LDS stage (16-byte units XOR-swizzled by row), and the
+// waves tile S as 2 row groups x 4 column groups: wave (wr, wc) contracts
+// 16-row tiles wr * 2 RTW .. wr * 2 RTW + 2 RTW - 1 against 16-column tiles
+// 2 wc, 2 wc + 1.  |x|^2, |q_j|^2 and the chunk's channel sums come from the
 // load registers (bf16 dot2), the channel sums added over the waves in wave
-// order through LDS.  One LDS-only barrier per chunk; D chunks of loads stay
-// in flight in registers.
+// order through LDS.  One LDS-only barrier per chunk; D chunks of loads in
+// flight in registers.  The row maxima and column sums of S are combined
+// across the waves through LDS at the end, in a fixed order.  Two
+// workgroups share a CU.
 constexpr int kWgQMax = 128;  // query tokens of the workgroup-shared path
-constexpr int kWgWaves = 4;
+constexpr int kWgWaves = 8;
+constexpr int kWgNQ = 128;    // query rows the stage holds (eight 16-column tiles)
 
-template <int RTW, int NQT>
+template <int RTW>
 __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_tokens, const VideoArgs<StreamArgs> va) {
   const StreamArgs f = va.v[blockIdx.y];
-  constexpr int RT = 64 * RTW;          // tile rows the stage holds
-  constexpr int NQ = 16 * NQT;          // query rows the stage holds
-  constexpr int XR = RT / 32;           // tile rows each thread loads per chunk
-  constexpr int QR = (NQ + 31) / 32;    // query rows each thread loads per chunk
-  constexpr int D = (XR + QR) * 4 * 3 <= 96 ? 3 : 2;  // chunks of loads in flight
+  constexpr int RT = 64 * RTW;                 // tile rows the stage holds
+  constexpr int NQ = kWgNQ;
+  constexpr int MTW = 2 * RTW;                 // 16-row tiles per wave
+  constexpr int NTW = 2;                       // 16-column tiles per wave
+  constexpr int XR = RT / 64;                  // tile rows each thread loads per chunk
+  constexpr int QR = NQ / 64;                  // query rows each thread loads per chunk
+  constexpr int D = 2 + (RTW == 1);            // chunks of loads in flight
   __shared__ __align__(16) u32x4 s_x[2][RT][8];
   __shared__ __align__(16) u32x4 s_q[2][NQ][8];
   __shared__ __align__(16) float s_pp[2][kWgWaves][kTokChunk];  // per-wave channel sums of a chunk
   __shared__ float s_xx[RT];
   __shared__ float s_qq[NQ];
-  __shared__ float s_sig[kWgWaves][NQ];
+  __shared__ float s_sig[2][NQ];    // column sums of S per row group
+  __shared__ float s_best[4][RT];   // row maxima of S_nj / |q_j| per column group
 
   int t, tile, sl;
   unit_of_block(blockIdx.x, f.tiles, 1, t, tile, sl);
@@ -686,8 +697,9 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
   const int TM = min(tile_tokens, N - tok0);
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave >> 2, wc = wave & 3;     // row group, column group
   const int r16 = lane & 15, grp = lane >> 4;  // MFMA layout: row / column, K group
-  const int rb = tid >> 3, lu = tid & 7;       // load layout: rows rb + 32 k, 16-byte unit lu
+  const int rb = tid >> 3, lu = tid & 7;       // load layout: rows rb + 64 k, 16-byte unit lu
   const int nch = (C + kTokChunk - 1) / kTokChunk;
 
   const __amdgpu_buffer_rsrc_t xres = make_rsrc_uniform(X + (size_t(t) * N + tok0) * C, uint32_t(TM) * C * 2);
@@ -700,24 +712,22 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
     bf16x8 q[QR];
   };
   // chunk c's units; chunks past the end, rows past the tile or the query
-  // and channels past C read zeros
+  // and channels past C read zeros (query rows past Q <= NQ lie past the end
+  // of qres; a per-lane row test here would become a branch around the load)
   auto issue = [&](int c, Slot& d) {
     const int cc = c * kTokChunk + 8 * lu;
     const bool ok = c < nch && cc < C;
 #pragma unroll
-    for (int k = 0; k < XR; ++k) d.x[k] = buf_load_bf16x8(xres, ok ? (rb + 32 * k) * C * 2 + cc * 2 : kOOB);
+    for (int k = 0; k < XR; ++k) d.x[k] = buf_load_bf16x8(xres, ok ? (rb + 64 * k) * C * 2 + cc * 2 : kOOB);
 #pragma unroll
-    for (int k = 0; k < QR; ++k) {
-      const int j = rb + 32 * k;
-      d.q[k] = buf_load_bf16x8(qres, (ok && j < NQ) ? (j * C + cc) * 2 : kOOB);
-    }
+    for (int k = 0; k < QR; ++k) d.q[k] = buf_load_bf16x8(qres, ok ? (rb + 64 * k) * C * 2 + cc * 2 : kOOB);
   };
 
-  f32x4 Sacc[RTW][NQT];
+  f32x4 Sacc[MTW][NTW];
 #pragma unroll
-  for (int i = 0; i < RTW; ++i)
+  for (int i = 0; i < MTW; ++i)
 #pragma unroll
-    for (int n = 0; n < NQT; ++n) Sacc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int n = 0; n < NTW; ++n) Sacc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
   float xx[XR], qq[QR];
 #pragma unroll
   for (int k = 0; k < XR; ++k) xx[k] = 0.f;
@@ -734,7 +744,7 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
     for (int e = 0; e < 8; ++e) cs[e] = 0.f;
 #pragma unroll
     for (int k = 0; k < XR; ++k) {
-      const int row = rb + 32 * k;
+      const int row = rb + 64 * k;
       const u32x4 v = __builtin_bit_cast(u32x4, d.x[k]);
       s_x[b][row][lu ^ (row & 7)] = v;
 #pragma unroll
@@ -746,9 +756,9 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
     }
 #pragma unroll
     for (int k = 0; k < QR; ++k) {
-      const int row = rb + 32 * k;
+      const int row = rb + 64 * k;
       const u32x4 v = __builtin_bit_cast(u32x4, d.q[k]);
-      if (row < NQ) s_q[b][row][lu ^ (row & 7)] = v;
+      s_q[b][row][lu ^ (row & 7)] = v;
 #pragma unroll
       for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
     }
@@ -765,37 +775,37 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
     }
   };
   // chunk c's channel sums, the waves' added in wave order: wave w stores
-  // channels 16 w .. 16 w + 15 of the chunk.  Every lane issues the store
-  // (the others at an offset past the buffer, which drops it), so the count
-  // of memory operations in flight is the same on every path and the waits
-  // for the ring's loads stay exact.
+  // channels 8 w .. 8 w + 7 of the chunk.  Every lane issues the store (the
+  // others at an offset past the buffer, which drops it), so the count of
+  // memory operations in flight is the same on every path and the waits for
+  // the ring's loads stay exact.
   auto pool_out = [&](int c) {
-    const int b = c & 1, k = 16 * wave + r16;
+    const int b = c & 1, k = 8 * wave + (lane & 7);
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < kWgWaves; ++w) v += s_pp[b][w][k];
     const int ch = c * kTokChunk + k;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), pres, (lane < 16 && ch < C) ? ch * 4 : kOOB, 0,
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), pres, (lane < 8 && ch < C) ? ch * 4 : kOOB, 0,
                                           kWriteThrough);
   };
   auto contract = [&](int c) {
     const int b = c & 1;
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
-      bf16x8 B[NQT];
+      bf16x8 B[NTW];
 #pragma unroll
-      for (int n = 0; n < NQT; ++n) {
-        const int row = 16 * n + r16;
+      for (int n = 0; n < NTW; ++n) {
+        const int row = 16 * (NTW * wc + n) + r16;
         B[n] = __builtin_bit_cast(bf16x8, s_q[b][row][(4 * st + grp) ^ (row & 7)]);
       }
 #pragma unroll
-      for (int i = 0; i < RTW; ++i) {
-        const int rt = wave + kWgWaves * i;
+      for (int i = 0; i < MTW; ++i) {
+        const int rt = MTW * wr + i;
         if (16 * rt < TM) {
           const int row = 16 * rt + r16;
           const bf16x8 A = __builtin_bit_cast(bf16x8, s_x[b][row][(4 * st + grp) ^ (row & 7)]);
 #pragma unroll
-          for (int n = 0; n < NQT; ++n) Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[n], Sacc[i][n], 0, 0, 0);
+          for (int n = 0; n < NTW; ++n) Sacc[i][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[n], Sacc[i][n], 0, 0, 0);
         }
       }
     }
@@ -803,13 +813,15 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
 
   // The loop runs to a multiple of D chunks: a chunk past the end reads
   // zeros, adds nothing and stores nowhere, and no branch around a load or
-  // store makes the compiler wait for the whole ring.
-  // (issued in slot order, as in the loop: the waits count the loads issued
-  // after a slot's)
-  Slot sl_[D];
+  // store makes the compiler wait for the whole ring.  The loads are issued
+  // in slot order before and in the loop (the waits count the loads issued
+  // after a slot's), and the norms' updates may not sink below a slot's
+  // reload: the slot would need a second register set, and the copy back at
+  // the end of the loop waits for the whole ring.
+  Slot ring[D];
 #pragma unroll
   for (int s = 0; s < D; ++s) {
-    issue(s, sl_[s]);
+    issue(s, ring[s]);
     __builtin_amdgcn_sched_barrier(0);
   }
   for (int c0 = 0; c0 < nch; c0 += D) {
@@ -817,16 +829,13 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
     for (int s = 0; s < D; ++s) {
       const int c = c0 + s;
       __builtin_amdgcn_sched_barrier(0);
-      consume(c, sl_[s]);
-      // the norms' updates may not sink below the slot's reload: the slot
-      // would need a second register set, and the copy back at the end of the
-      // loop waits for the whole ring
+      consume(c, ring[s]);
 #pragma unroll
       for (int k = 0; k < XR; ++k) asm volatile("" : "+v"(xx[k]));
 #pragma unroll
       for (int k = 0; k < QR; ++k) asm volatile("" : "+v"(qq[k]));
       lds_barrier();  // chunk c staged by every wave; chunk c - 2's stage no longer read
-      issue(c + D, sl_[s]);
+      issue(c + D, ring[s]);
       pool_out(c);
       contract(c);
     }
@@ -842,61 +851,62 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
 #pragma unroll
   for (int k = 0; k < XR; ++k) {
     const float v = row8_sum(xx[k]);
-    if (lu == 0) s_xx[rb + 32 * k] = v;
+    if (lu == 0) s_xx[rb + 64 * k] = v;
   }
 #pragma unroll
   for (int k = 0; k < QR; ++k) {
     const float v = row8_sum(qq[k]);
-    if (lu == 0 && rb + 32 * k < NQ) s_qq[rb + 32 * k] = v;
+    if (lu == 0) s_qq[rb + 64 * k] = v;
   }
   // sigma_j of the wave's rows: accumulator column j = 16 n + r16, the four
   // lane groups added by lane swaps (rows past the tile hold zeros)
 #pragma unroll
-  for (int n = 0; n < NQT; ++n) {
+  for (int n = 0; n < NTW; ++n) {
     float v = 0.f;
 #pragma unroll
-    for (int i = 0; i < RTW; ++i)
+    for (int i = 0; i < MTW; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) v += Sacc[i][n][e];
     v = row_sum4(v);
-    if (lane < 16) s_sig[wave][16 * n + r16] = v;
+    if (lane < 16) s_sig[wr][16 * (NTW * wc + n) + r16] = v;
   }
-  lds_barrier();
+  lds_barrier();  // s_qq, s_xx, s_sig complete
   if (tid < Q) {
-    float v = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWgWaves; ++w) v += s_sig[w][tid];
-    f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = v;
+    f.sig_part[(size_t(t) * f.tiles + tile) * Q + tid] = s_sig[0][tid] + s_sig[1][tid];
     if (tile == 0) f.qg_part[size_t(t) * Q + tid] = s_qq[tid];
   }
-  // a_{t,n} = max_j S_nj / (|q_j| |x_n|) over the query's columns
-  float rq[NQT];
+  // the wave's row maxima of S_nj / |q_j| over its columns j < Q
+  float rq[NTW];
+  bool live[NTW];
 #pragma unroll
-  for (int n = 0; n < NQT; ++n) {
-    const int j = 16 * n + r16;
+  for (int n = 0; n < NTW; ++n) {
+    const int j = 16 * (NTW * wc + n) + r16;
     const float qv = s_qq[j];
     rq[n] = qv > 0.f ? 1.0f / sqrtf(qv) : 0.f;
+    live[n] = j < Q;
   }
 #pragma unroll
-  for (int i = 0; i < RTW; ++i) {
-    const int rt = wave + kWgWaves * i;
-    if (16 * rt >= TM) continue;
+  for (int i = 0; i < MTW; ++i) {
+    const int rt = MTW * wr + i;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float best = -INFINITY;
 #pragma unroll
-      for (int n = 0; n < NQT; ++n)
-        if (16 * n + r16 < Q) best = fmaxf(best, Sacc[i][n][e] * rq[n]);
+      for (int n = 0; n < NTW; ++n)
+        if (live[n]) best = fmaxf(best, Sacc[i][n][e] * rq[n]);
       best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
       best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
       best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
       best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x140, 0xF, 0xF, false)));
-      const int row = 16 * rt + 4 * grp + e;
-      if (r16 == e && row < TM) {
-        const float xn = sqrtf(s_xx[row]);
-        f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
-      }
+      if (r16 == e) s_best[wc][16 * rt + 4 * grp + e] = best;
     }
+  }
+  lds_barrier();  // s_best complete
+  // a_{t,n} = max_j S_nj / (|q_j| |x_n|): the column groups' maxima in order
+  for (int row = tid; row < TM; row += kWgWaves * 64) {
+    const float best = fmaxf(fmaxf(s_best[0][row], s_best[1][row]), fmaxf(s_best[2][row], s_best[3][row]));
+    const float xn = sqrtf(s_xx[row]);
+    f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
   }
 }
 
@@ -1114,16 +1124,11 @@ hipError_t launch_relevance_stream(const wz_config& c, const void* X, const void
     if (pl.ntg == 1) { WZ_TOK(1) } else if (pl.ntg == 2) { WZ_TOK(2) } else { WZ_TOK(4) }
 #undef WZ_TOK
   } else if (pl.kind == kRelWg) {
-    if (va.v[0].groups > 1 || va.v[0].Q > 16 * pl.ntg) return hipErrorInvalidValue;
-#define WZ_WG(RTW)                                                                                               \
-  switch (pl.ntg) {                                                                                              \
-    case 1: hipLaunchKernelGGL((k_relevance_wg<RTW, 1>), dim3(pl.grid, V), dim3(256), 0, s, pl.tile_tokens, va); break; \
-    case 2: hipLaunchKernelGGL((k_relevance_wg<RTW, 2>), dim3(pl.grid, V), dim3(256), 0, s, pl.tile_tokens, va); break; \
-    case 4: hipLaunchKernelGGL((k_relevance_wg<RTW, 4>), dim3(pl.grid, V), dim3(256), 0, s, pl.tile_tokens, va); break; \
-    default: hipLaunchKernelGGL((k_relevance_wg<RTW, 8>), dim3(pl.grid, V), dim3(256), 0, s, pl.tile_tokens, va); break; \
-  }
-    if (pl.rtw == 1) { WZ_WG(1) } else { WZ_WG(2) }
-#undef WZ_WG
+    if (va.v[0].groups > 1 || va.v[0].Q > kWgNQ) return hipErrorInvalidValue;
+    if (pl.rtw == 1)
+      hipLaunchKernelGGL((k_relevance_wg<1>), dim3(pl.grid, V), dim3(kWgWaves * 64), 0, s, pl.tile_tokens, va);
+    else
+      hipLaunchKernelGGL((k_relevance_wg<2>), dim3(pl.grid, V), dim3(kWgWaves * 64), 0, s, pl.tile_tokens, va);
   } else if (pl.kind == kRelMfma) {
     // queries of more than 32 tokens take several passes of 32 over the slice:
     // wider query groups no longer fit the accumulators in registers
