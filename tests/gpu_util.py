@@ -34,16 +34,45 @@ def rel_err(got, want, floor_frac=1e-3):
     return float(np.max(np.abs(got - want) / den))
 
 
-def within(got, want, tol):
-    """rel_err with the floor that belongs to `tol` is at most `tol`."""
-    return rel_err(got, want, FLOOR[tol]) <= tol
+def unfloored_err(got, want):
+    """Max over the elements with want != 0 of |got - want| / |want| (0 when there are none)."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    nz = want != 0
+    if not nz.any():
+        return 0.0
+    return float(np.max(np.abs(got[nz] - want[nz]) / np.abs(want[nz])))
+
+
+def needed_floor(got, want, tol):
+    """Smallest floor fraction f with rel_err(got, want, f) <= tol (0 when no element needs one)."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    if want.size == 0:
+        return 0.0
+    m = float(np.max(np.abs(want)))
+    diff = np.abs(got - want)
+    over = diff > tol * np.abs(want)
+    if not over.any():
+        return 0.0
+    return float(np.max(diff[over])) / (tol * m) if m > 0 else float("inf")
+
+
+def within(got, want, tol, label="tensor"):
+    """rel_err with the floor that belongs to `tol` is at most `tol`.  Prints the floored and the
+    unfloored maximum error and the smallest floor that would still pass, so the run's log records
+    how far below the bar each tensor is."""
+    floored = rel_err(got, want, FLOOR[tol])
+    print(f"[err] {label}: floored {floored:.3e} (floor {FLOOR[tol]:g} x max, bar {tol:g}), "
+          f"unfloored {unfloored_err(got, want):.3e}, needed floor {needed_floor(got, want, tol):.2e}", flush=True)
+    return floored <= tol
 
 
 def tol_for(in_dtype):
     return TOL_BF16_IN if in_dtype == "bf16" else TOL_F32_IN
 
 
-@functools.lru_cache(maxsize=2)
+@functools.lru_cache(maxsize=6)
 def workload_case(name):
     """Inputs and oracle output of a named workload (cached per test session)."""
     wl = synth.WORKLOADS[name]

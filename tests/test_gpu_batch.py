@@ -39,6 +39,7 @@ def _case(name):
 
 
 @pytest.mark.parametrize("name,out_dtype", [("tiny", wz.WZ_F32), ("t64_14x14_c3584", wz.WZ_BF16),
+                                            ("t32_14x14_c3584", wz.WZ_BF16), ("t256_27x27_c1152", wz.WZ_BF16),
                                             ("t128_13x13_c3584", wz.WZ_F32), ("odd_3x5", wz.WZ_F32),
                                             ("many_frames", wz.WZ_F32)])
 def test_condense_batch_matches_single(name, out_dtype):

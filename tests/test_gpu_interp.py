@@ -38,10 +38,11 @@ def _check(wl, out, tok, idx, b, o, out_dtype):
     assert np.array_equal(_np(b), out["budget"]) and np.array_equal(_np(o), out["offset"])
     assert np.array_equal(_np(idx)[:n], out["index"])
     tol = G.tol_for(wl.dtype) if out_dtype == wz.WZ_F32 else G.TOL_BF16_OUT
-    assert G.within(_np(tok)[:n], out["tokens"], tol)
+    assert G.within(_np(tok)[:n], out["tokens"], tol, f"{wl.name} interp tokens")
 
 
 @pytest.mark.parametrize("name,out_dtype", [("tiny", wz.WZ_F32), ("t64_14x14_c3584", wz.WZ_BF16),
+                                            ("t32_14x14_c3584", wz.WZ_BF16), ("t256_27x27_c1152", wz.WZ_BF16),
                                             ("t128_13x13_c3584", wz.WZ_F32), ("odd_3x5", wz.WZ_F32),
                                             ("single_token", wz.WZ_F32), ("budget_all", wz.WZ_F32),
                                             ("row_1x7", wz.WZ_F32), ("col_7x1", wz.WZ_F32),

@@ -40,9 +40,9 @@ def _run_case(wl, inp, out, out_dtype=wz.WZ_F32, check_stage1=True):
     if check_stage1:
         a, r, d = wz.relevance(p, X, q)
         torch.cuda.synchronize()
-        assert G.within(_np(a), out["a"].ravel(), tol)
-        assert G.within(_np(r), out["r"], tol)
-        assert G.within(_np(d), out["delta"], tol)
+        assert G.within(_np(a), out["a"].ravel(), tol, f"{wl.name} a")
+        assert G.within(_np(r), out["r"], tol, f"{wl.name} r")
+        assert G.within(_np(d), out["delta"], tol, f"{wl.name} delta")
     tok, idx, b, o = wz.condense(p, X, q)
     torch.cuda.synchronize()
     n = int(out["offset"][-1])
@@ -50,9 +50,9 @@ def _run_case(wl, inp, out, out_dtype=wz.WZ_F32, check_stage1=True):
     assert np.array_equal(_np(o), out["offset"])
     assert np.array_equal(_np(idx)[:n], out["index"])
     if out_dtype == wz.WZ_F32:
-        assert G.within(_np(tok)[:n], out["tokens"], tol)
+        assert G.within(_np(tok)[:n], out["tokens"], tol, f"{wl.name} tokens")
     else:
-        assert G.within(_np(tok)[:n], out["tokens"], G.TOL_BF16_OUT)
+        assert G.within(_np(tok)[:n], out["tokens"], G.TOL_BF16_OUT, f"{wl.name} tokens (bf16 out)")
     return tok, idx, b, o
 
 

@@ -55,6 +55,7 @@ def _case(name):
                                               ("odd_3x5", 3, wz.WZ_F32), ("q20_x3", 3, wz.WZ_F32),
                                               ("small_query_bf16", 8, wz.WZ_BF16), ("q40_x2", 2, wz.WZ_F32),
                                               ("tiny", 3, wz.WZ_F32), ("t128_13x13_c3584", 2, wz.WZ_F32),
+                                              ("t256_27x27_c1152", 2, wz.WZ_BF16),
                                               # several passes over X, each shared by a group of queries
                                               ("t64_14x14_c3584", 4, wz.WZ_BF16), ("odd_3x5", 5, wz.WZ_F32),
                                               ("q20_x3", 5, wz.WZ_F32)])
