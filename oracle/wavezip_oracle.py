@@ -224,12 +224,13 @@ def allocate_budget_trace(r_tilde, B, N):
     The record holds the quotas `q` of the frames `active` in that round, the
     number `left` of leftover tokens handed out by fractional part, whether the
     all-zero-weight rule (`uniform`) or the spread-after-capping rule
-    (`reactivated`) fired, and the frames fixed at N (`capped`).
+    (`reactivated`) fired, the frames fixed at N (`capped`), and the quotas of
+    every round in order (`rounds`, the capping rounds included).
     """
     L = len(r_tilde)
     n = np.zeros(L, dtype=np.int64)
     trace = dict(q=np.zeros(0), active=np.zeros(0, dtype=np.int64), left=0,
-                 uniform=False, reactivated=False, capped=np.zeros(L, dtype=bool))
+                 uniform=False, reactivated=False, capped=np.zeros(L, dtype=bool), rounds=[])
     if B >= L * N:
         n[:] = N
         trace["capped"][:] = True
@@ -249,6 +250,7 @@ def allocate_budget_trace(r_tilde, B, N):
             trace["reactivated"] = True
         idx = np.nonzero(active)[0]
         q = R * w[idx] / np.sum(w[idx])
+        trace["rounds"].append(q)
         full = q >= N
         if np.any(full):
             n[idx[full]] = N

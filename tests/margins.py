@@ -10,6 +10,7 @@ Decisions and margins (oracle float64 values):
   selection boundary, per frame   a_(n) - a_(n+1)        >= M_A
   saliency / gate ranges          max - min               >= M_A or exactly 0
   remainder cut-off               frac_(left) - frac_(left+1) >= M_Q tokens
+  cap (every round)               |q_t - N|               >= M_Q tokens
   all-weights-zero switch         |max r_tilde|           >= M_R
   weight signs (re-activation)    |r_tilde_m|             >= M_R
   frame filter (tau > 0)          |delta_t - tau|         >= M_D
@@ -55,6 +56,10 @@ def check(out, N, B, tau=0.0):
     _, trace = oracle.allocate_budget_trace(rt, int(B), N)
     if trace["reactivated"] and np.any(np.abs(rt) < M_R):
         bad.append(("weight_sign", float(np.min(np.abs(rt)))))
+    for k, qr in enumerate(trace["rounds"]):
+        near = np.abs(qr - N) < M_Q
+        if np.any(near):
+            bad.append(("cap", (k, float(np.min(np.abs(qr - N))))))
     q, left = trace["q"], trace["left"]
     if 0 < left < len(q):
         frac = np.sort(q - np.floor(q))[::-1]
