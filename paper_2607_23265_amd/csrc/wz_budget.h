@@ -5,8 +5,10 @@
 // standalone budget kernel and by the fused selection and gather kernel.
 //
 // The budget is a few fp64 operations per frame, so it runs in ONE workgroup
-// with every array in LDS: one wave when T <= 64 (no cross-wave
-// synchronisation at all), 256 threads up to T = 256, 1024 beyond.  Steps:
+// with every array in LDS, or in one wave: up to T = 64 with every value in
+// registers (budget_wave_compute), up to T = 256 with four frames per lane
+// and the arrays in LDS (budget_body with NT = 64: no cross-wave
+// synchronisation at all); 1024 threads beyond.  Steps:
 //   gamma  = min-max(delta) over all T frames (0 if all equal);
 //   M      = {0} U {t >= 1 : delta_t >= tau}, compacted in temporal order;
 //   WTA    = J levels of orthonormal Haar analysis of r over M (odd lengths
@@ -132,6 +134,73 @@ __device__ int bscan_excl(int v, int& total, Sh& sh) {
     total += sh.ired[i];
   }
   return before + inc - v;
+}
+
+// One wave hands the `need` extra tokens of the last apportionment round to
+// the active positions ranked first by (fractional part desc, index asc);
+// position i is lane i % 64's slot i / 64, its fractional part in w[i].
+// Non-negative doubles order like their bit patterns, so a descent over the
+// bits finds them: positions with the current bit set are taken whole while
+// they fit, else the search continues among them; positions still tied after
+// the last bit go by index (slot, then lane).
+template <int TV, typename Sh>
+__device__ void remainder_extras_wave(const double* w, Sh& sh, int L, int need) {
+  constexpr int SL = (TV + kWave - 1) / kWave;
+  const int lane = threadIdx.x & 63;
+  uint64_t fb[SL], cand[SL], chosen[SL];
+  uint64_t any = 0ull, all = ~0ull;
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    const int i = s * kWave + lane;
+    const bool act = i < L && sh.state[i] == kActive;
+    fb[s] = act ? __builtin_bit_cast(uint64_t, w[i]) : 0ull;
+    cand[s] = __ballot(act);
+    chosen[s] = 0ull;
+    if (act) {
+      any |= fb[s];
+      all &= fb[s];
+    }
+  }
+  // bits on which every active position agrees decide nothing: start below them
+  any = wave_reduce_u64(any, [](uint64_t x, uint64_t y) { return x | y; });
+  all = wave_reduce_u64(all, [](uint64_t x, uint64_t y) { return x & y; });
+  const int top = (any ^ all) ? 63 - __clzll(any ^ all) : -1;
+  for (int bit = top; bit >= 0 && need > 0; --bit) {
+    int cnt = 0;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) cnt += __popcll(cand[s]);
+    if (cnt <= need) break;
+    uint64_t ones[SL];
+    int c1 = 0;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      ones[s] = cand[s] & __ballot((fb[s] >> bit) & 1ull);
+      c1 += __popcll(ones[s]);
+    }
+    if (c1 <= need) {
+#pragma unroll
+      for (int s = 0; s < SL; ++s) {
+        chosen[s] |= ones[s];
+        cand[s] &= ~ones[s];
+      }
+      need -= c1;
+    } else {
+#pragma unroll
+      for (int s = 0; s < SL; ++s) cand[s] = ones[s];
+    }
+  }
+  // the remaining candidates all fit, or are exact ties: smaller index first
+#pragma unroll
+  for (int s = 0; s < SL; ++s)
+    for (; need > 0 && cand[s]; --need) {
+      chosen[s] |= cand[s] & (~cand[s] + 1ull);
+      cand[s] &= cand[s] - 1ull;
+    }
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    const int i = s * kWave + lane;
+    if (i < L && ((chosen[s] >> lane) & 1ull)) sh.n[i] += 1;
+  }
 }
 
 // NT threads handle up to TV frames; thread tid owns frames tid*kPer .. tid*kPer+kPer-1.
@@ -329,6 +398,10 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
       }
       const int left = int(R) - bsum_int<NT>(base_sum, sh);
       // +1 for the `left` active frames ranked first by (fraction desc, index asc)
+      if constexpr (NT == kWave) {
+        bsync<NT>();
+        remainder_extras_wave<TV>(w, sh, L, left);
+      } else
       for (int i = tid; i < L; i += NT) {
         if (sh.state[i] != kActive) continue;
         const double f = w[i];

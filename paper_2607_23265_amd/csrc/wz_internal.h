@@ -172,9 +172,10 @@ __device__ __forceinline__ void unit_of_block(int b, int tiles, int slices, int&
 
 constexpr int kMaxFrames = 2048;
 // frames up to which the budget is folded into the selection kernel (one
-// wave computes it); above, one workgroup of its own computes it once, which
-// costs less than every selection workgroup repeating a workgroup-wide budget
-constexpr int kFusedTMax = 64;
+// wave computes it: up to 64 frames in registers, up to 256 four frames per
+// lane in LDS); above, one workgroup of its own computes it once, which costs
+// less than every selection workgroup repeating a workgroup-wide budget
+constexpr int kFusedTMax = 256;
 
 // Workspace carve-up (all offsets 256-byte aligned).
 struct Workspace {

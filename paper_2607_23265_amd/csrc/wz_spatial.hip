@@ -7,8 +7,9 @@
 // bit and no kernel boundary separates the budget from its use.
 //
 // Workgroup (t, p), p < P, 1024 threads, works on frame t:
-//   A. wave 0 computes the budgets (T <= 64; above, they come from the budget
-//      kernel launched before this one) while
+//   A. wave 0 computes the budgets (T <= 256: in registers up to 64 frames,
+//      four frames per lane in LDS above; beyond 256 they come from the
+//      budget kernel launched before this one) while
 //      the other waves take the frame's selection ranks and block gates
 //      (from the per-frame kernel, or formed here from the scores when the
 //      stage runs on its own, wz_rank.h) and form the rows of the first
@@ -21,7 +22,7 @@
 //      higher rank of ALL frames are then shared out evenly over all
 //      workgroups (every workgroup knows every budget), so frames with large
 //      budgets do not leave a few CUs working alone.  With the offsets given
-//      (T > 64, or the stage on its own) each workgroup emits its frame's
+//      (T > 256, or the stage on its own) each workgroup emits its frame's
 //      kept tokens of rank p, p + P, ... instead, the next part's block reads
 //      in flight while one is finished.  A token's row is its 2x2 Haar block
 //      (the last row / column repeated when H or W is odd) through the
@@ -291,6 +292,10 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
 
   // s_ext[t] = kept tokens of rank >= kp in frames before t (one wave; the
   // budgets are in s_nb)
+  auto fused_budget = [&]() {
+    if (T <= kWave) budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+    else budget_body<kWave, kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+  };
   auto extra_prefix = [&]() {
     int carry = 0;
     for (int t0 = 0; t0 < T; t0 += kWave) {
@@ -326,13 +331,13 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
       }
       if (ahead) modulate(xp, gp, yp);
     } else {
-      budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+      fused_budget();
       extra_prefix();
     }
   } else {
     // the frame's order from its scores, all waves (after the budgets)
     if constexpr (MODE == kWaveBudget) {
-      if (wave == 0) budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+      if (wave == 0) fused_budget();
     }
     const __amdgpu_buffer_rsrc_t ares = make_rsrc(f.tok_score + size_t(t) * N, uint32_t(N) * 4);
     float lo = INFINITY, hi = -INFINITY;
