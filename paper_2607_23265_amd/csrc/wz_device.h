@@ -57,6 +57,37 @@ __device__ __forceinline__ void buf_store_wt_b64(uint64_t v, __amdgpu_buffer_rsr
   __builtin_amdgcn_raw_buffer_store_b64(u32x2v{uint32_t(v), uint32_t(v >> 32)}, r, off, 0, kWriteThrough);
 }
 
+// Transposing sum over the eight lanes u, u + 8, ..., u + 56 of a wave (the
+// lanes with equal lane & 7): each of them holds eight values v[0..7], and
+// lane 8k + u ends with the total of value k over the eight.  Three butterfly
+// steps, each halving the values a lane keeps: partner lane +-8 (DPP row
+// rotation by 8), +-16 (permlane16 swap), +-32 (permlane32 swap); at each the
+// lane keeps the half its own index bit selects and adds the partner's copy
+// of it.  About 24 instructions instead of three reductions per value.
+__device__ __forceinline__ float lane_transpose_sum8(const float (&v)[8]) {
+  const int lane = __lane_id();
+  const bool b0 = (lane >> 3) & 1;
+  // step 1: keep the values of index parity b0 (m -> index 2m + b0)
+  float w[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const float keep = b0 ? v[2 * m + 1] : v[2 * m];
+    const float send = b0 ? v[2 * m] : v[2 * m + 1];
+    w[m] = keep + __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(send), 0x128, 0xF, 0xF, false));
+  }
+  // step 2: rows 2r and 2r + 1 (lane bit 4); even rows keep m = 0, 2, odd rows m = 1, 3
+  float x[2];
+#pragma unroll
+  for (int n = 0; n < 2; ++n) {
+    const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(w[2 * n]), __float_as_uint(w[2 * n + 1]), false,
+                                                    false);
+    x[n] = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+  }
+  // step 3: lower and upper 32 lanes (lane bit 5); the lower keep n = 0, the upper n = 1
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[0]), __float_as_uint(x[1]), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
 // Sum over the four 16-lane rows of a wave, every lane getting the total of
 // its column (lane & 15): ((row0 + row1) + (row2 + row3)).  gfx950's lane
 // swaps do it in the vector ALU, without the LDS crossbar.

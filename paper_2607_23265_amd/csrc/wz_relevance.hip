@@ -452,21 +452,11 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
 #pragma unroll
         for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
       }
-      // channel sums over the wave's rows: lanes lu, lu + 8, ..., lu + 56 in a fixed order
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float v = cs[e];
-        v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
-        const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-        v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-        const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-        cs[e] = __uint_as_float(b[0]) + __uint_as_float(b[1]);
-      }
+      // channel sums over the wave's rows (lanes lu, lu + 8, ..., lu + 56, in a
+      // fixed order): lane 8 lr + lu ends with channel 8 lu + lr's
+      const float cw = lane_transpose_sum8(cs);
       const int c0 = c * kTokChunk + 8 * lu;
-      if (sums && lane < 8 && c0 < C) {
-        *reinterpret_cast<f32x4*>(pool + c0) = f32x4{cs[0], cs[1], cs[2], cs[3]};
-        *reinterpret_cast<f32x4*>(pool + c0 + 4) = f32x4{cs[4], cs[5], cs[6], cs[7]};
-      }
+      if (sums && c0 < C) pool[c0 + lr] = cw;
     };
     auto contract = [&]() {
 #pragma unroll
@@ -762,30 +752,24 @@ __global__ __launch_bounds__(kWgWaves * 64, 2) void k_relevance_wg(int tile_toke
 #pragma unroll
       for (int e = 0; e < 4; ++e) qq[k] = dot2(v[e], v[e], qq[k]);
     }
-    // the wave's channel sums: lanes lu, lu + 8, ..., lu + 56 in a fixed order
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v = cs[e];
-      v += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x128, 0xF, 0xF, false));  // row_ror:8
-      cs[e] = row_sum4(v);
-    }
-    if (lane < 8) {
-      *reinterpret_cast<f32x4*>(&s_pp[b][wave][8 * lane]) = f32x4{cs[0], cs[1], cs[2], cs[3]};
-      *reinterpret_cast<f32x4*>(&s_pp[b][wave][8 * lane + 4]) = f32x4{cs[4], cs[5], cs[6], cs[7]};
-    }
+    // the wave's channel sums (lanes lu, lu + 8, ..., lu + 56, in a fixed
+    // order): lane 8 k + lu ends with channel 8 lu + k's
+    s_pp[b][wave][8 * lu + (lane >> 3)] = lane_transpose_sum8(cs);
   };
-  // chunk c's channel sums, the waves' added in wave order: wave w stores
-  // channels 8 w .. 8 w + 7 of the chunk.  Every lane issues the store (the
-  // others at an offset past the buffer, which drops it), so the count of
+  // chunk c's channel sums, the waves' added in wave order by wave 0 (lane k:
+  // channel k of the chunk).  Every lane of every wave issues the store (all
+  // but wave 0's past the end of the buffer, which drops them), so the count of
   // memory operations in flight is the same on every path and the waits for
-  // the ring's loads stay exact.
+  // the ring's loads stay exact; the sums themselves sit behind a scalar branch.
   auto pool_out = [&](int c) {
-    const int b = c & 1, k = 8 * wave + (lane & 7);
+    const int b = c & 1;
     float v = 0.f;
+    if (wave == 0) {
 #pragma unroll
-    for (int w = 0; w < kWgWaves; ++w) v += s_pp[b][w][k];
-    const int ch = c * kTokChunk + k;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), pres, (lane < 8 && ch < C) ? ch * 4 : kOOB, 0,
+      for (int w = 0; w < kWgWaves; ++w) v += s_pp[b][w][lane];
+    }
+    const int ch = c * kTokChunk + lane;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), pres, (wave == 0 && ch < C) ? ch * 4 : kOOB, 0,
                                           kWriteThrough);
   };
   auto contract = [&](int c) {
