@@ -422,7 +422,7 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       for (int i = 0; i < RT; ++i)
 #pragma unroll
         for (int c = 0; c < 8; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-      u32x4 xr[8];  // tokens 8g + e of the current step, channels 8 r16 .. +7
+      // tokens 8g + e of a step, channels 8 r16 .. +7; past the frame: zeros
       auto load_step = [&](int k0, u32x4 (&d)[8]) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -430,18 +430,15 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
           d[e] = __builtin_amdgcn_raw_buffer_load_b128(xres, (n < N && coff != kOOB) ? n * rb + coff : kOOB, 0, 0);
         }
       };
-      load_step(0, xr);
-      for (int k0 = 0; k0 < NP; k0 += 32) {
-        u32x4 xn[8];
-        load_step(k0 + 32, xn);  // past the frame: zeros
+      auto step = [&](int k0, const u32x4 (&x)[8]) {
         // 8 x 8 transpose of bf16: w[c'] dword j = tokens (2j, 2j+1) of channel c'
         u32x4 w[8];
 #pragma unroll
         for (int m = 0; m < 4; ++m)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            w[2 * m][j] = __builtin_amdgcn_perm(xr[2 * j + 1][m], xr[2 * j][m], 0x05040100u);
-            w[2 * m + 1][j] = __builtin_amdgcn_perm(xr[2 * j + 1][m], xr[2 * j][m], 0x07060302u);
+            w[2 * m][j] = __builtin_amdgcn_perm(x[2 * j + 1][m], x[2 * j][m], 0x05040100u);
+            w[2 * m + 1][j] = __builtin_amdgcn_perm(x[2 * j + 1][m], x[2 * j][m], 0x07060302u);
           }
 #pragma unroll
         for (int i = 0; i < RT; ++i) {
@@ -457,8 +454,21 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
             acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw, acc[i][c], 0, 0, 0);
           }
         }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) xr[e] = xn[e];
+      };
+      // a two-slot ring of steps, issued in slot order and reloaded in place
+      // (a register copy of a slot still loading would wait for the load): the
+      // next step's block is in flight while one is contracted
+      u32x4 xa[8], xb[8];
+      load_step(0, xa);
+      __builtin_amdgcn_sched_barrier(0);
+      load_step(32, xb);
+      for (int k0 = 0; k0 < NP; k0 += 64) {
+        __builtin_amdgcn_sched_barrier(0);
+        step(k0, xa);
+        load_step(k0 + 64, xa);
+        __builtin_amdgcn_sched_barrier(0);
+        if (k0 + 32 < NP) step(k0 + 32, xb);
+        load_step(k0 + 96, xb);
       }
 #pragma unroll
       for (int i = 0; i < RT; ++i) {
