@@ -17,17 +17,19 @@
 // the three detail bands get G.  Only i with s_u[h][i] != 0 contribute (at
 // most F / 2 of them), j likewise.
 //
-// Workgroup (frame t, slice of 512 channels), 256 threads:
+// Workgroup (frame t, channel slice), 512 threads (eight waves share the
+// slice-independent setup, which every slice's workgroup repeats):
 //   1. ranks the frame's tokens from their scores (wz_rank.h) and lists its
 //      n_t kept tokens (rank < n_t) in raster order;
 //   2. forms G and the per-axis analysis rows a_u in LDS;
 //   3. per chunk of KR kept tokens builds their rows L_p in LDS (fp32,
 //      through the partial sums B_i(w') = sum_j over the width) and
 //      contracts them with the frame's slice, a dense product of KR rows,
-//      H*W tokens and 512 channels: for bf16 inputs on MFMA (the rows split
-//      into bf16 high and low parts, fp32 accumulation; each wave takes 128
-//      channels), for fp32 inputs on the vector ALU (each wave takes a
-//      quarter of the rows, fp32); then writes the rows to
+//      H*W tokens and the slice's channels: for bf16 inputs on MFMA (the rows
+//      split into bf16 high and low parts, fp32 accumulation; each wave takes
+//      128 channels of a 1024-channel slice), for fp32 inputs on the vector
+//      ALU (512-channel slices, each wave an eighth of the rows, fp32); then
+//      writes the rows to
 //      out_tokens[offset_t + k] (k = raster position among the kept tokens),
 //      their flat indices to out_index.
 // The frame's slice is read once per chunk of KR kept tokens (from L2 after
@@ -38,9 +40,13 @@
 namespace wz {
 namespace {
 
-constexpr int kFThreads = 256;
+constexpr int kFThreads = 512;
 constexpr int kFWaves = kFThreads / kWave;
-constexpr int kFSlice = kWave * 8;  // channels of a workgroup: 8 per lane
+// channels of a workgroup: 128 per wave on MFMA (bf16 inputs); 8 per lane on
+// the vector ALU (fp32 inputs), where the waves split the rows instead
+constexpr int kFSliceMf = kFWaves * 128;
+constexpr int kFSliceValu = kWave * 8;
+constexpr int filter_slice(bool mfma) { return mfma ? kFSliceMf : kFSliceValu; }
 constexpr int kMaxAct = kMaxTaps / 2;  // synthesis rows touching one output sample
 
 struct FilterArgs {
@@ -184,7 +190,8 @@ template <typename In, typename Out, int KR>
 __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<FilterArgs> va, const Bank bank) {
   constexpr int RW = KR / kFWaves;  // rows a wave contracts
   const FilterArgs& f = va.v[blockIdx.y];
-  const int S = (f.C + kFSlice - 1) / kFSlice;
+  constexpr int SLICE = filter_slice(sizeof(In) == 2);
+  const int S = (f.C + SLICE - 1) / SLICE;
   const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
   const int t = (slot / S) * kXcds + xcd, sl = slot % S;
   if (t >= f.T) return;  // whole workgroup
@@ -415,7 +422,7 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       constexpr int RT = (KR + 15) / 16;  // 16-row tiles
       const int rtiles = (nr + 15) / 16;
       const int r16 = lane & 15, g = lane >> 4;
-      const int cw = sl * kFSlice + wave * 128 + 8 * r16;  // the lane's first channel
+      const int cw = sl * SLICE + wave * 128 + 8 * r16;  // the lane's first channel
       const int coff = cw < C ? cw * 2 : kOOB;
       f32x4 acc[RT][8];
 #pragma unroll
@@ -527,9 +534,9 @@ int filter_rows(int H, int W, int F, bool mfma) {
 template <typename In, typename Out>
 void launch_filter_typed(const wz_config& c, const VideoArgs<FilterArgs>& va, int V, const Bank& bank,
                          hipStream_t s) {
-  const int S = (c.C + kFSlice - 1) / kFSlice;
-  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
   constexpr bool mfma = sizeof(In) == 2;
+  const int S = (c.C + filter_slice(mfma) - 1) / filter_slice(mfma);
+  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
   const int kr = filter_rows(c.H, c.W, bank.F, mfma);
   const size_t lds = filter_lds(c.H, c.W, bank.F, kr, mfma).bytes;
   if (kr == 32) hipLaunchKernelGGL((k_filter_assign<In, Out, 32>), grid, block, lds, s, va, bank);
