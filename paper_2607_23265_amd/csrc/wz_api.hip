@@ -108,11 +108,11 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   vs.out = cfg->B * cfg->C * s_out;
   vs.idx = cfg->B * 4;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // a filter-bank spatial basis ranks each frame in its own kernel: the
-  // per-frame kernel then forms r and delta only
+  // the per-frame kernel also ranks every frame's tokens (for a filter-bank
+  // spatial basis its block gates go unused)
   const bool filt = cfg->spatial_basis != WZ_HAAR;
   WZ_TRY(from_hip(launch_relevance_stream(*cfg, X, query, w.tok_score, w, s, vs)));
-  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, !filt, s, vs)));
+  WZ_TRY(from_hip(launch_frame(*cfg, w, w.tok_score, w.frame_rel, w.frame_delta, true, s, vs)));
   vs.bud = budget ? (long long)cfg->T * 4 : vs.ws;
   vs.off = offset ? ((long long)cfg->T + 1) * 4 : vs.ws;
   if (cfg->T <= kFusedTMax && cfg->temporal_basis == WZ_HAAR && !filt) {  // budgets inside the selection kernel
@@ -124,7 +124,7 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
   WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s, vs)));
-  if (filt) return from_hip(launch_filter_assign(*cfg, X, w.tok_score, off, out_tokens, out_index, s, vs));
+  if (filt) return from_hip(launch_filter_assign(*cfg, X, w.tok_score, off, w.rank, out_tokens, out_index, s, vs));
   return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, &w, nullptr, nullptr, out_tokens,
                                        out_index, s, vs));
 }
@@ -207,7 +207,8 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
   }
   if (cfg->spatial_basis != WZ_HAAR)
     return from_hip(
-        launch_filter_assign(*cfg, X, tok_score, offset, out_tokens, out_index, static_cast<hipStream_t>(stream)));
+        launch_filter_assign(*cfg, X, tok_score, offset, nullptr, out_tokens, out_index,
+                             static_cast<hipStream_t>(stream)));
   return from_hip(launch_assign_gather(*cfg, X, tok_score, nullptr, nullptr, offset, nullptr, nullptr, nullptr,
                                        out_tokens, out_index, static_cast<hipStream_t>(stream)));
 }

@@ -19,8 +19,9 @@
 //
 // Workgroup (frame t, channel slice), 512 threads (eight waves share the
 // slice-independent setup, which every slice's workgroup repeats):
-//   1. ranks the frame's tokens from their scores (wz_rank.h) and lists its
-//      n_t kept tokens (rank < n_t) in raster order;
+//   1. takes the frame's selection ranks (from the per-frame kernel, or forms
+//      them from the scores, wz_rank.h) and lists its n_t kept tokens
+//      (rank < n_t) in raster order;
 //   2. forms G and the per-axis analysis rows a_u in LDS;
 //   3. per chunk of KR kept tokens builds their rows L_p in LDS (fp32,
 //      through the partial sums B_i(w') = sum_j over the width) and
@@ -53,6 +54,7 @@ struct FilterArgs {
   const void* X;            // [T][H][W][C]
   const float* tok_score;   // [T][H*W]
   const int32_t* offset;    // [T+1]
+  const int32_t* rank;      // [T][H*W] selection ranks from the per-frame kernel, or null (ranked here)
   void* out_tokens;         // [B][C]
   int32_t* out_index;       // [B]
   long long B;
@@ -253,7 +255,19 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
         }
       }
     }
-    rank_frame<kFThreads>(N, H, W, f.lam, lo, hi, rl);
+    if (f.rank) {
+      // the per-frame kernel's ranks (the same ranking of the same keys); the
+      // frame's score extremes per wave, as the ranking leaves them
+      for (int n = tid; n < N; n += kFThreads) rl.rank[n] = f.rank[size_t(t) * N + n];
+      lo = wave_min_f32(lo);
+      hi = wave_max_f32(hi);
+      if (lane == 0) {
+        s_mm[wave] = lo;
+        s_mm[kFWaves + wave] = hi;
+      }
+    } else {
+      rank_frame<kFThreads>(N, H, W, f.lam, lo, hi, rl);
+    }
   }
   __syncthreads();
   {
@@ -552,7 +566,8 @@ bool filter_assign_supported(const wz_config& c) {
 }
 
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
-                                void* out_tokens, int32_t* out_index, hipStream_t s, const Videos& vs) {
+                                const int32_t* rank, void* out_tokens, int32_t* out_index, hipStream_t s,
+                                const Videos& vs) {
   if (!filter_assign_supported(c) || c.spatial_basis == WZ_HAAR) return hipErrorInvalidValue;
   const Bank bank = make_bank(c.spatial_basis);
   VideoArgs<FilterArgs> va{};
@@ -561,6 +576,7 @@ hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* 
     a.X = advance(X, v * vs.x);
     a.tok_score = advance(tok_score, v * vs.ws);
     a.offset = advance(offset, v * vs.off);
+    a.rank = advance(rank, v * vs.ws);
     a.out_tokens = advance(out_tokens, v * vs.out);
     a.out_index = advance(out_index, v * vs.idx);
     a.B = c.B;

@@ -300,7 +300,10 @@ int assign_groups_per_frame(const wz_config& c, int V = 1);
 // offsets (each workgroup ranks its frame itself).  Needs
 // filter_assign_supported(c).
 bool filter_assign_supported(const wz_config& c);
+// With rank (the per-frame kernel's selection ranks, [T][H*W]) each workgroup
+// reads its frame's ranks instead of forming them.
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
-                                void* out_tokens, int32_t* out_index, hipStream_t s, const Videos& vs = Videos{});
+                                const int32_t* rank, void* out_tokens, int32_t* out_index, hipStream_t s,
+                                const Videos& vs = Videos{});
 
 }  // namespace wz
