@@ -375,7 +375,9 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
     }
     __syncthreads();
     // ---- 3b. L_p(h', w') = sum_i E_i(h') B1_i(w') + P_i(h') B2_i(w'): thread
-    // tid builds row tid % KR at tokens tid / KR, + 256 / KR, ... ----
+    // tid builds row tid % KR at columns w' = tid / KR, + 512 / KR, ..., each
+    // column's B values in registers and the height factors read per h' (the
+    // same for all of the row's threads: one LDS broadcast) ----
     {
       const int r = tid % KR, nstep = kFThreads / KR;
       const bool live = c0 + r < nt;
@@ -390,18 +392,7 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
       }
       const float* B1 = s_B + (r * 2 + 0) * kMaxAct * W;
       const float* B2 = s_B + (r * 2 + 1) * kMaxAct * W;
-      int n = tid / KR, y = n / W, x = n - y * W;
-      const int dy = nstep / W, dx = nstep - dy * W;
-      for (; n < (MF ? NP : N); n += nstep) {
-        float acc = 0.f;
-        if (n < N) {
-#pragma unroll
-          for (int ii = 0; ii < kMaxAct; ++ii) {
-            const float e = ew[ii] * s_AH[ih[ii] * H + y];
-            const float pp = e + pw[ii] * s_AH[(nh + ih[ii]) * H + y];
-            acc += e * B1[ii * W + x] + pp * B2[ii * W + x];
-          }
-        }
+      auto put = [&](int n, float acc) {
         if constexpr (MF) {
           // bf16 high part and the rounded remainder: together about 16
           // significant bits of the row entry (tokens past N are 0)
@@ -411,13 +402,27 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
         } else {
           s_L[n * KR + r] = acc;
         }
-        x += dx;
-        y += dy;
-        if (x >= W) {
-          x -= W;
-          ++y;
+      };
+      for (int x = tid / KR; x < W; x += nstep) {
+        float b1[kMaxAct], b2[kMaxAct];
+#pragma unroll
+        for (int ii = 0; ii < kMaxAct; ++ii) {
+          b1[ii] = B1[ii * W + x];
+          b2[ii] = B2[ii * W + x];
+        }
+        for (int y = 0; y < H; ++y) {
+          float acc = 0.f;
+#pragma unroll
+          for (int ii = 0; ii < kMaxAct; ++ii) {
+            const float e = ew[ii] * s_AH[ih[ii] * H + y];
+            const float pp = e + pw[ii] * s_AH[(nh + ih[ii]) * H + y];
+            acc += e * b1[ii] + pp * b2[ii];
+          }
+          put(y * W + x, acc);
         }
       }
+      if constexpr (MF)
+        for (int n = N + tid / KR; n < NP; n += nstep) put(n, 0.f);
     }
     __syncthreads();
     // ---- 3c. the chunk's rows against the frame's slice ----
