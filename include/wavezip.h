@@ -127,8 +127,11 @@ typedef struct {
 
 /* Bytes of device workspace that wz_relevance and wz_condense need for `cfg`
  * (0 if cfg is invalid): per-unit partial sums of the streaming pass, the
- * intermediate scores and frame values, and budgets.  Contents on entry are ignored; one call at a time per
- * workspace.                                                                  */
+ * intermediate scores and frame values, and budgets; with a db4 / bior4.4
+ * spatial basis, bf16 inputs and frames too large for the one-kernel form
+ * of stage 3 (about 24 x 24 tokens and up), also each kept token's
+ * operator row of the modulator (B rows of 4 * 32*ceil(H*W/32) bytes).
+ * Contents on entry are ignored; one call at a time per workspace.          */
 size_t wz_workspace_bytes(const wz_config* cfg);
 
 /* Stage 1 -- Cross-Modal Scorer (similarity branch, Sec. 3.2.1) and Visual
@@ -197,8 +200,11 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X,
 /* The whole pass C(X, Q) of Eq. (4)/(6): stage 1, 2 and 3 in sequence on one
  * stream, intermediates kept in `ws`.  Three kernel launches: the pass over
  * X, the per-frame scores, and one kernel that computes the budgets (every
- * workgroup alike) and performs stage 3; for T > 64 the budgets get a
- * launch of their own.  out_tokens [B][C] (cfg->out_dtype) and
+ * workgroup alike) and performs stage 3; for T > 256 or a db4 / bior4.4
+ * basis the budgets get a launch of their own, and with a db4 / bior4.4
+ * spatial basis on large frames (bf16 inputs) stage 3 takes two: the
+ * modulator's operator rows of the kept tokens, once per frame, into the
+ * workspace, then their product with the frames' channels.  out_tokens [B][C] (cfg->out_dtype) and
  * out_index [B] receive offset[T] rows (= B unless the frame filter leaves
  * fewer than B tokens).  budget [T] and offset [T+1] are optional outputs
  * (NULL: kept in the workspace).                                              */

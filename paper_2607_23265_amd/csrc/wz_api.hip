@@ -124,7 +124,8 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
   WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s, vs)));
-  if (filt) return from_hip(launch_filter_assign(*cfg, X, w.tok_score, off, w.rank, out_tokens, out_index, s, vs));
+  if (filt)
+    return from_hip(launch_filter_assign(*cfg, X, w.tok_score, off, w.rank, w.frows, out_tokens, out_index, s, vs));
   return from_hip(launch_assign_gather(*cfg, X, w.tok_score, nullptr, nullptr, off, &w, nullptr, nullptr, out_tokens,
                                        out_index, s, vs));
 }
@@ -207,7 +208,7 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X, const flo
   }
   if (cfg->spatial_basis != WZ_HAAR)
     return from_hip(
-        launch_filter_assign(*cfg, X, tok_score, offset, nullptr, out_tokens, out_index,
+        launch_filter_assign(*cfg, X, tok_score, offset, nullptr, nullptr, out_tokens, out_index,
                              static_cast<hipStream_t>(stream)));
   return from_hip(launch_assign_gather(*cfg, X, tok_score, nullptr, nullptr, offset, nullptr, nullptr, nullptr,
                                        out_tokens, out_index, static_cast<hipStream_t>(stream)));

@@ -55,6 +55,7 @@ struct FilterArgs {
   const float* tok_score;   // [T][H*W]
   const int32_t* offset;    // [T+1]
   const int32_t* rank;      // [T][H*W] selection ranks from the per-frame kernel, or null (ranked here)
+  uint16_t* rows;           // [B][2][pad_tokens(H*W)] the row kernel's output (bf16 high, low part)
   void* out_tokens;         // [B][C]
   int32_t* out_index;       // [B]
   long long B;
@@ -188,12 +189,15 @@ __device__ __forceinline__ void contract_rows(const ContractArgs& a) {
   }
 }
 
-template <typename In, typename Out, int KR>
+// ROWS (bf16 inputs): the row kernel of the split form, one workgroup per
+// frame: steps 1-3b, then the chunk's operator rows (MFMA form) go to
+// f.rows and their flat indices to out_index, for k_filter_contract.
+template <typename In, typename Out, int KR, bool ROWS = false>
 __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<FilterArgs> va, const Bank bank) {
   constexpr int RW = KR / kFWaves;  // rows a wave contracts
   const FilterArgs& f = va.v[blockIdx.y];
   constexpr int SLICE = filter_slice(sizeof(In) == 2);
-  const int S = (f.C + SLICE - 1) / SLICE;
+  const int S = ROWS ? 1 : (f.C + SLICE - 1) / SLICE;
   const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
   const int t = (slot / S) * kXcds + xcd, sl = slot % S;
   if (t >= f.T) return;  // whole workgroup
@@ -425,8 +429,20 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
         for (int n = N + tid / KR; n < NP; n += nstep) put(n, 0.f);
     }
     __syncthreads();
+    if constexpr (ROWS) {
+      // ---- 3c. the chunk's rows to the row buffer (both parts, NP tokens
+      // each; 16 bytes a thread) and their flat indices ----
+      const int nr = min(KR, nt - c0), vr = NP / 8;
+      for (int q = tid; q < nr * 2 * vr; q += kFThreads) {
+        const int r = q / (2 * vr), rem = q - r * (2 * vr), part = rem / vr, v8 = rem - part * vr;
+        if (base + c0 + r < total)
+          *reinterpret_cast<u32x4*>(f.rows + (size_t(base + c0 + r) * 2 + part) * NP + 8 * v8) =
+              *reinterpret_cast<const u32x4*>(s_Lh + (part * LR + r) * LS + 8 * v8);
+      }
+      for (int r = tid; r < nr; r += kFThreads)
+        if (base + c0 + r < total) f.out_index[base + c0 + r] = t * N + s_kept[c0 + r];
+    } else if constexpr (MF) {
     // ---- 3c. the chunk's rows against the frame's slice ----
-    if constexpr (MF) {
       // MFMA: C[rows][channels] += L[rows][tokens] X[tokens][channels] with
       // v_mfma_f32_16x16x32_bf16, the wave's 128 channels in 8 MFMAs per
       // 16-row tile and 32-token step.  Lane (r16, g) = (lane % 16, lane / 16)
@@ -540,6 +556,150 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   }
 }
 
+// The split form's contraction (bf16 inputs): out_tokens rows of frame t =
+// its operator rows (from the row kernel) times the frame's tokens.
+struct RowsArgs {
+  const void* X;           // [T][H][W][C] bf16
+  const int32_t* offset;   // [T+1]
+  const uint16_t* rows;    // [B][2][pad_tokens(N)]
+  void* out_tokens;        // [B][C]
+  long long B;
+  int T, N, C;
+};
+static_assert(sizeof(VideoArgs<RowsArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
+// A frame's channels in S slices of at most eight 128-channel waves, the
+// slices balanced (each a multiple of 128 channels).
+constexpr int kRcWaveCh = 128;
+__host__ __device__ inline int rc_slices(int C) { return (C + kFWaves * kRcWaveCh - 1) / (kFWaves * kRcWaveCh); }
+__host__ __device__ inline int rc_slice_width(int C, int S) {
+  return ((C + S - 1) / S + kRcWaveCh - 1) / kRcWaveCh * kRcWaveCh;
+}
+
+// Workgroup (frame t, channel slice), 8 waves of 128 channels each, no LDS
+// and no barriers: sweeps of up to 16 RT rows, whose accumulators stay in
+// registers while the wave streams the frame's slice and the rows' operator
+// entries once.  C[rows][channels] += L[rows][tokens] X[tokens][channels]
+// with v_mfma_f32_16x16x32_bf16, 8 MFMAs per 16-row tile and 32-token step
+// (each twice: the rows' bf16 high and low parts).  Lane (r16, g) =
+// (lane % 16, lane / 16) loads tokens 8g .. 8g+7 of a step for its channels
+// 8 r16 .. 8 r16+7 (16 bytes a token); the B operand of MFMA c' (8 K values
+// of column r16) is channel 8 r16 + c' of those tokens, formed by byte
+// permutes just before its MFMAs, so that the columns of MFMA c' are
+// channels 8 r16 + c'.  The A operand (row 16i + r16, tokens 8g .. 8g+7) is
+// one 16-byte load per part.  Lane (r16, g) ends with rows 4g .. 4g+3 of
+// each tile for its 8 consecutive channels.
+template <typename Out, int RT>
+__global__ __launch_bounds__(kFThreads) void k_filter_contract(const VideoArgs<RowsArgs> va) {
+  const RowsArgs& f = va.v[blockIdx.y];
+  const int S = rc_slices(f.C);
+  const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
+  const int t = (slot / S) * kXcds + xcd, sl = slot % S;
+  if (t >= f.T) return;  // whole workgroup
+  const int N = f.N, C = f.C, NP = pad_tokens(N);
+  const long long base = f.offset[t];
+  const int nt = min(max(f.offset[t + 1] - int(base), 0), N);
+  const long long total = min((long long)f.offset[f.T], f.B);
+  // the rows the call may write (those past total were not formed either)
+  const int nrow = int(max(0LL, min((long long)nt, total - base)));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c_lo = sl * rc_slice_width(C, S) + wave * kRcWaveCh;
+  if (nrow == 0 || wave * kRcWaveCh >= rc_slice_width(C, S) || c_lo >= C) return;  // whole wave
+  const int r16 = lane & 15, g = lane >> 4;
+  const int cw = c_lo + 8 * r16;  // the lane's first channel
+  const int rb = C * 2;
+  const __amdgpu_buffer_rsrc_t xres =
+      make_rsrc(static_cast<const uint16_t*>(f.X) + size_t(t) * N * C, uint32_t(N) * rb);
+  // the frame's rows, 4 NP bytes each; tokens past the frame and rows past
+  // nrow fall beyond a descriptor and load zeros (lanes past C start at kOOB;
+  // offsets stay below 2^31)
+  const __amdgpu_buffer_rsrc_t lres = make_rsrc(f.rows + size_t(base) * 2 * NP, uint32_t(nrow) * 4 * NP);
+  const int vx = 8 * g * rb + (cw < C ? cw * 2 : kOOB);
+  // a sweep of NT row tiles from row c0 (the last sweep may have fewer
+  // tiles: each count is its own code, without per-tile tests)
+  auto sweep = [&](auto tiles, int c0) __attribute__((always_inline)) {
+    constexpr int NT = decltype(tiles)::value;
+    const int va0 = (c0 + r16) * 4 * NP + 16 * g;  // row c0 + r16, high part, tokens 8g ..
+    f32x4 acc[NT][8];
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // a step's X block and operator entries; each load's uniform part as one
+    // scalar, so that the compiler adds it to the lane's base instead of
+    // holding a base per load
+    auto load = [&](int k0, u32x4 (&x)[8], u32x4 (&ah)[NT], u32x4 (&al)[NT]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        x[e] = __builtin_amdgcn_raw_buffer_load_b128(xres, vx + __builtin_amdgcn_readfirstlane((k0 + e) * rb), 0, 0);
+#pragma unroll
+      for (int i = 0; i < NT; ++i) {
+        const int su = __builtin_amdgcn_readfirstlane(i * 64 * NP + 2 * k0);
+        ah[i] = __builtin_amdgcn_raw_buffer_load_b128(lres, va0 + su, 0, 0);
+        al[i] = __builtin_amdgcn_raw_buffer_load_b128(lres, va0 + su + 2 * NP, 0, 0);
+      }
+    };
+    // per channel c', its B operand, then the MFMAs of every tile, the high
+    // parts first, so that the two products into one accumulator are NT
+    // MFMAs apart
+    auto step = [&](const u32x4 (&x)[8], const u32x4 (&ah)[NT], const u32x4 (&al)[NT]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        u32x4 wc;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          wc[j] = __builtin_amdgcn_perm(x[2 * j + 1][c >> 1], x[2 * j][c >> 1], (c & 1) ? 0x07060302u : 0x05040100u);
+        const bf16x8 bw = __builtin_bit_cast(bf16x8, wc);
+#pragma unroll
+        for (int i = 0; i < NT; ++i)
+          acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ah[i]), bw, acc[i][c], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < NT; ++i)
+          acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, al[i]), bw, acc[i][c], 0, 0, 0);
+      }
+    };
+    // a two-slot ring of steps, issued in slot order and reloaded in place
+    // (a register copy of a slot still loading would wait for the load)
+    u32x4 xa[8], xb[8], aha[NT], ala[NT], ahb[NT], alb[NT];
+    load(0, xa, aha, ala);
+    __builtin_amdgcn_sched_barrier(0);
+    load(32, xb, ahb, alb);
+    for (int k0 = 0; k0 < NP; k0 += 64) {
+      __builtin_amdgcn_sched_barrier(0);
+      step(xa, aha, ala);
+      load(k0 + 64, xa, aha, ala);
+      __builtin_amdgcn_sched_barrier(0);
+      if (k0 + 32 < NP) step(xb, ahb, alb);
+      load(k0 + 96, xb, ahb, alb);
+    }
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      // one descriptor per 16-row tile (the lanes' rows differ); its size
+      // stops at the last row the call may write
+      const long long row0 = base + c0 + 16 * i;
+      const int rows = min(16, nrow - c0 - 16 * i);
+      if (rows <= 0) break;
+      const __amdgpu_buffer_rsrc_t ores =
+          make_rsrc_uniform(static_cast<Out*>(f.out_tokens) + size_t(row0) * C, uint32_t(rows * C * sizeof(Out)));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int rt = 4 * g + e;
+        if (rt < rows) {
+          float y8[8];
+#pragma unroll
+          for (int c = 0; c < 8; ++c) y8[c] = acc[i][c][e];
+          if (cw < C) store8<Out>(ores, (rt * C + cw) * int(sizeof(Out)), y8);
+        }
+      }
+    }
+  };
+  for (int c0 = 0; c0 < nrow; c0 += 16 * RT) {
+    const int rtiles = (nrow - c0 + 15) / 16;  // uniform
+    if (rtiles >= 3) sweep(std::integral_constant<int, 3>{}, c0);
+    else if (rtiles == 2) sweep(std::integral_constant<int, 2>{}, c0);
+    else sweep(std::integral_constant<int, 1>{}, c0);
+  }
+}
+
 // dynamic LDS a workgroup may take (the static arrays use about 2 KB)
 constexpr size_t kFilterLdsMax = (160 - 4) * 1024;
 
@@ -548,6 +708,23 @@ int filter_rows(int H, int W, int F, bool mfma) {
   for (int kr = 32; kr >= 8; kr /= 2)
     if (filter_lds(H, W, F, kr, mfma).bytes <= kFilterLdsMax) return kr;
   return 0;
+}
+
+// the row kernel: one workgroup per frame
+void launch_filter_rows(const wz_config& c, const VideoArgs<FilterArgs>& va, int V, const Bank& bank, hipStream_t s) {
+  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds), V), block(kFThreads);
+  const int kr = filter_rows(c.H, c.W, bank.F, true);
+  const size_t lds = filter_lds(c.H, c.W, bank.F, kr, true).bytes;
+  if (kr == 32) hipLaunchKernelGGL((k_filter_assign<uint16_t, uint16_t, 32, true>), grid, block, lds, s, va, bank);
+  else if (kr == 16) hipLaunchKernelGGL((k_filter_assign<uint16_t, uint16_t, 16, true>), grid, block, lds, s, va, bank);
+  else hipLaunchKernelGGL((k_filter_assign<uint16_t, uint16_t, 8, true>), grid, block, lds, s, va, bank);
+}
+
+template <typename Out>
+void launch_contract_typed(const wz_config& c, const VideoArgs<RowsArgs>& va, int V, hipStream_t s) {
+  const int S = rc_slices(c.C);
+  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
+  hipLaunchKernelGGL((k_filter_contract<Out, 3>), grid, block, 0, s, va);
 }
 
 template <typename In, typename Out>
@@ -570,10 +747,23 @@ bool filter_assign_supported(const wz_config& c) {
          filter_rows(c.H, c.W, kMaxTaps, false) > 0;
 }
 
+// The split form pays a second launch and a round trip of the rows through
+// memory; it wins where the fused kernel's LDS holds full-frame rows for at
+// most 16 kept tokens at a time (large frames), so that frames with more
+// kept tokens would read their slice of X from memory once per chunk.
+bool filter_split(const wz_config& c) {
+  return c.spatial_basis != WZ_HAAR && c.in_dtype == WZ_BF16 && filter_rows(c.H, c.W, kMaxTaps, true) < 32;
+}
+
+size_t filter_rows_bytes(const wz_config& c) {
+  return filter_split(c) ? size_t(c.B) * 4 * pad_tokens(c.H * c.W) : 0;
+}
+
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
-                                const int32_t* rank, void* out_tokens, int32_t* out_index, hipStream_t s,
-                                const Videos& vs) {
+                                const int32_t* rank, uint16_t* rows, void* out_tokens, int32_t* out_index,
+                                hipStream_t s, const Videos& vs) {
   if (!filter_assign_supported(c) || c.spatial_basis == WZ_HAAR) return hipErrorInvalidValue;
+  if (rows && c.in_dtype != WZ_BF16) return hipErrorInvalidValue;
   const Bank bank = make_bank(c.spatial_basis);
   VideoArgs<FilterArgs> va{};
   for (int v = 0; v < vs.V; ++v) {
@@ -582,6 +772,7 @@ hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* 
     a.tok_score = advance(tok_score, v * vs.ws);
     a.offset = advance(offset, v * vs.off);
     a.rank = advance(rank, v * vs.ws);
+    a.rows = advance(rows, v * vs.ws);
     a.out_tokens = advance(out_tokens, v * vs.out);
     a.out_index = advance(out_index, v * vs.idx);
     a.B = c.B;
@@ -591,7 +782,24 @@ hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* 
     a.C = c.C;
     a.lam = c.lambda_;
   }
-  if (c.in_dtype == WZ_BF16) {
+  if (rows) {
+    // split form: the rows once per frame, then the contraction per slice
+    launch_filter_rows(c, va, vs.V, bank, s);
+    VideoArgs<RowsArgs> ra{};
+    for (int v = 0; v < vs.V; ++v) {
+      RowsArgs& a = ra.v[v];
+      a.X = va.v[v].X;
+      a.offset = va.v[v].offset;
+      a.rows = va.v[v].rows;
+      a.out_tokens = va.v[v].out_tokens;
+      a.B = c.B;
+      a.T = c.T;
+      a.N = c.H * c.W;
+      a.C = c.C;
+    }
+    if (c.out_dtype == WZ_BF16) launch_contract_typed<uint16_t>(c, ra, vs.V, s);
+    else launch_contract_typed<float>(c, ra, vs.V, s);
+  } else if (c.in_dtype == WZ_BF16) {
     if (c.out_dtype == WZ_BF16) launch_filter_typed<uint16_t, uint16_t>(c, va, vs.V, bank, s);
     else launch_filter_typed<uint16_t, float>(c, va, vs.V, bank, s);
   } else {

@@ -178,6 +178,9 @@ constexpr int kMaxFrames = 2048;
 constexpr int kFusedTMax = 256;
 
 // Workspace carve-up (all offsets 256-byte aligned).
+// Bytes of the filter-bank operator rows in the workspace (0 if unused).
+size_t filter_rows_bytes(const wz_config& c);
+
 struct Workspace {
   float* s_part;       // [T][slices][N][qpad(Q)] per-slice x . q_j (only with several slices)
   float* g_part;       // [T][slices][N]          per-slice |x|^2 (only with several slices)
@@ -193,6 +196,7 @@ struct Workspace {
   float* frame_delta;  // [T]
   int32_t* budget;     // [T]
   int32_t* offset;     // [T+1]
+  uint16_t* frows;     // [B][2][pad(H*W)]        filter-bank operator rows (bf16 inputs, filter spatial basis)
   size_t bytes;
 };
 
@@ -219,6 +223,8 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
   w.budget = reinterpret_cast<int32_t*>(take(T * 4));
   w.offset = reinterpret_cast<int32_t*>(take((T + 1) * 4));
+  const size_t frows = filter_rows_bytes(c);
+  w.frows = frows ? reinterpret_cast<uint16_t*>(take(frows)) : nullptr;
   w.bytes = off;
   return w;
 }
@@ -265,6 +271,7 @@ inline Workspace advance(const Workspace& w, long long bytes) {
   o.frame_delta = advance(w.frame_delta, bytes);
   o.budget = advance(w.budget, bytes);
   o.offset = advance(w.offset, bytes);
+  o.frows = advance(w.frows, bytes);
   return o;
 }
 
@@ -301,9 +308,13 @@ int assign_groups_per_frame(const wz_config& c, int V = 1);
 // filter_assign_supported(c).
 bool filter_assign_supported(const wz_config& c);
 // With rank (the per-frame kernel's selection ranks, [T][H*W]) each workgroup
-// reads its frame's ranks instead of forming them.
+// reads its frame's ranks instead of forming them.  With rows (bf16 inputs; at
+// least filter_rows_bytes(c) bytes, 16-byte aligned) the split form runs: a
+// row kernel forms each kept token's operator row once per frame into rows,
+// then a contraction kernel applies them to the frame's channels; without it
+// one fused kernel per (frame, channel slice) forms the rows it uses.
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
-                                const int32_t* rank, void* out_tokens, int32_t* out_index, hipStream_t s,
-                                const Videos& vs = Videos{});
+                                const int32_t* rank, uint16_t* rows, void* out_tokens, int32_t* out_index,
+                                hipStream_t s, const Videos& vs = Videos{});
 
 }  // namespace wz

@@ -36,9 +36,15 @@ def _np(t):
     return t.detach().float().cpu().numpy() if t.dtype in (torch.bfloat16, torch.float32) else t.cpu().numpy()
 
 
-# the edge cases of the parity tests, plus the largest grids the filter banks take
+# the edge cases of the parity tests, plus the largest grids the filter banks
+# take; with bf16 inputs on large grids the operator rows are formed once per
+# frame and contracted by a second kernel (the split form): a ragged channel
+# count (a partly filled wave), several 48-row sweeps per frame, and two
+# balanced channel slices of 640 and 512 channels
 CASE_EDGE = dict(EDGE, grid_32x32=dict(T=3, H=32, W=32, C=96, Q=16, B=300),
-                 grid_16x64=dict(T=2, H=16, W=64, C=72, Q=16, B=200))
+                 grid_16x64=dict(T=2, H=16, W=64, C=72, Q=16, B=200),
+                 split_32x32_c200=dict(T=3, H=32, W=32, C=200, Q=16, B=300),
+                 split_27x27_c1152=dict(T=2, H=27, W=27, C=1152, Q=16, B=420))
 
 
 def _case(name, tb, sb):
@@ -98,6 +104,10 @@ CASES = [
     ("query_128_passes", wz.WZ_BIOR44, wz.WZ_BIOR44, wz.WZ_BF16),
     ("grid_32x32", wz.WZ_DB4, wz.WZ_DB4, wz.WZ_F32),
     ("grid_16x64", wz.WZ_BIOR44, wz.WZ_BIOR44, wz.WZ_F32),
+    ("t256_27x27_c1152", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("split_32x32_c200", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_BF16),
+    ("split_32x32_c200", wz.WZ_BIOR44, wz.WZ_BIOR44, wz.WZ_F32),
+    ("split_27x27_c1152", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_BF16),
 ]
 
 
@@ -116,7 +126,8 @@ def test_condense_bases(name, tb, sb, out_dtype):
 
 
 @pytest.mark.parametrize("name,sb", [("tiny", wz.WZ_DB4), ("t64_14x14_c3584", wz.WZ_BIOR44),
-                                     ("t128_13x13_c3584", wz.WZ_DB4), ("odd_3x5", wz.WZ_BIOR44)])
+                                     ("t128_13x13_c3584", wz.WZ_DB4), ("odd_3x5", wz.WZ_BIOR44),
+                                     ("split_32x32_c200", wz.WZ_DB4)])
 def test_stage_spatial_bases(name, sb):
     """wz_spatial_dwt_condense with a filter bank, fed the oracle's scores (as fp32) and offsets."""
     wl, inp, out = _case(name, wz.WZ_HAAR, sb)
@@ -181,10 +192,13 @@ def test_stage_temporal_budget_bases(T, tb):
     assert checked > 0
 
 
-def test_bases_batch_matches_single_calls():
-    """Two videos through wz_condense_batch with filter banks: each bitwise equal to its single call."""
-    wl, inp, _ = G.workload_case("tiny")
-    p = wz.problem_of(wl, wz.WZ_F32, temporal_basis=wz.WZ_BIOR44, spatial_basis=wz.WZ_DB4)
+@pytest.mark.parametrize("name", ["tiny", "split_32x32_c200"])
+def test_bases_batch_matches_single_calls(name):
+    """Two videos through wz_condense_batch with filter banks (the fused form, and the split form
+    with bf16 inputs on a large grid): each bitwise equal to its single call."""
+    wl, inp, _ = _case(name, wz.WZ_BIOR44, wz.WZ_DB4)
+    p = wz.problem_of(wl, wz.WZ_F32 if wl.dtype == "f32" else wz.WZ_BF16, temporal_basis=wz.WZ_BIOR44,
+                      spatial_basis=wz.WZ_DB4)
     X, q = wz.to_device(inp, DEV)
     X2, q2 = X.flip(0).contiguous(), q.flip(0).contiguous()
     tok, idx, b, o = wz.condense_batch(p, torch.stack([X, X2]), torch.stack([q, q2]))
