@@ -6,9 +6,10 @@
 //
 // The budget is a few fp64 operations per frame, so it runs in ONE workgroup
 // with every array in LDS, or in one wave: up to T = 64 with every value in
-// registers (budget_wave_compute), up to T = 256 with four frames per lane
-// and the arrays in LDS (budget_body with NT = 64: no cross-wave
-// synchronisation at all); 1024 threads beyond.  Steps:
+// registers (budget_wave_compute), up to T = 256 with four frames per lane,
+// also in registers (budget_wave_slots; budget_body with NT = 64 keeps the
+// same layout in LDS, for the filter-bank bases); 1024 threads beyond.
+// Steps:
 //   gamma  = min-max(delta) over all T frames (0 if all equal);
 //   M      = {0} U {t >= 1 : delta_t >= tau}, compacted in temporal order;
 //   WTA    = J levels of orthonormal Haar analysis of r over M (odd lengths
@@ -586,6 +587,307 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
     if (rel_rect) rel_rect[lane] = keep ? float(rt) : 0.f;
   }
   if (lane == T - 1) offset[T] = incl;
+}
+
+// ---------------------------------------------------------------------------
+// T <= TV (TV = 64 SL, at most 256): one wave, frame t and retained position
+// i in slot t / 64 (i / 64) of lane t % 64 (i % 64), every value in
+// registers except each level's detail coefficients (LDS); the compaction
+// to the retained positions and the way back go through LDS only when the
+// frame filter drops a frame.  The positions' layout is budget_body<64, TV>'s
+// and so are its sums (a lane's slots in order, then the same butterfly), so
+// the budgets are bit for bit that function's; its LDS arrays and their
+// ordering points are what this version saves.
+// ---------------------------------------------------------------------------
+template <int TV>
+__device__ void budget_wave_slots(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
+                                  long long B, int levels, float tau, int32_t* __restrict__ budget,
+                                  int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
+  constexpr int SL = TV / kWave;
+  static_assert(TV % kWave == 0 && SL >= 1 && SL <= 4, "one to four slots per lane");
+  const double inv_sqrt2 = 0.70710678118654752440;
+  const int lane = threadIdx.x & 63;
+  const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
+  __shared__ double s_det[TV + kMaxLevels];  // every level's gated details, level after level
+  __shared__ int s_doff[kMaxLevels];        // where each level's start
+  __shared__ double s_mv[2][TV];
+  __shared__ int s_nmv[TV];
+  auto order = []() {  // one wave: its LDS accesses in program order
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  };
+
+  // ---- gamma = min-max(delta); retained set M ----
+  double x[SL], g[SL];
+  bool keep[SL];
+  uint64_t kmask[SL];
+  int kpos[SL];  // retained position of the slot's frame
+  float dlo = INFINITY, dhi = -INFINITY;
+  double dv[SL];
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    const int t = s * kWave + lane;
+    const bool valid = t < T;
+    const float df = valid ? delta[t] : 0.f;
+    dv[s] = double(df);
+    x[s] = valid ? double(rel[t]) : 0.0;
+    if (valid) {
+      dlo = fminf(dlo, df);
+      dhi = fmaxf(dhi, df);
+    }
+    keep[s] = valid && (t == 0 || dv[s] >= double(tau));
+    kmask[s] = __ballot(keep[s]);
+  }
+  // delta arrives in fp32, so its extremes are exact in fp32
+  const double lo = double(wave_min_f32(dlo)), hi = double(wave_max_f32(dhi));
+  int L = 0;
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    g[s] = hi > lo ? (dv[s] - lo) / (hi - lo) : 0.0;
+    kpos[s] = L + __popcll(kmask[s] & below);
+    L += __popcll(kmask[s]);
+  }
+  const bool moved = L < T;  // uniform: some frame dropped, positions differ from frames
+  if (moved) {
+#pragma unroll
+    for (int s = 0; s < SL; ++s)
+      if (keep[s]) {
+        s_mv[0][kpos[s]] = x[s];
+        s_mv[1][kpos[s]] = g[s];
+      }
+    order();
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      x[s] = s_mv[0][s * kWave + lane];  // positions past L: values nobody reads
+      g[s] = s_mv[1][s * kWave + lane];
+    }
+  }
+
+  // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)); output k = 64 s +
+  // lane reads inputs 2k and min(2k + 1, len - 1), both in slot 2s or 2s + 1
+  int len = L, doff = 0;
+  for (int lev = 0; lev < levels; ++lev) {
+    const int half = (len + 1) / 2;
+    if (lane == 0) s_doff[lev] = doff;
+    double xn[SL], gn[SL];
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      xn[s] = 0.0;
+      gn[s] = 0.0;
+      if constexpr (true) {
+        const int k = s * kWave + lane;
+        const int i0 = 2 * k, i1 = min(2 * k + 1, max(len - 1, 0));
+        auto fetch = [&](const double (&v)[SL], int i) {
+          // slot 2s or 2s + 1 (the value of a slot past the array is never used)
+          const double a = 2 * s < SL ? __shfl(v[min(2 * s, SL - 1)], i & 63, kWave) : 0.0;
+          const double b = 2 * s + 1 < SL ? __shfl(v[min(2 * s + 1, SL - 1)], i & 63, kWave) : 0.0;
+          return (i >> 6) == 2 * s ? a : b;
+        };
+        if (2 * s < SL) {
+          const double x0 = fetch(x, i0), x1 = fetch(x, i1);
+          const double gp = 0.5 * (fetch(g, i0) + fetch(g, i1));
+          if (k < half) s_det[doff + k] = gp * ((x0 - x1) * inv_sqrt2);
+          xn[s] = (x0 + x1) * inv_sqrt2;
+          gn[s] = gp;
+        }
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      x[s] = xn[s];
+      g[s] = gn[s];
+    }
+    doff += half;
+    len = half;
+  }
+  order();
+  // ---- inverse DWT (Eq. (11)): output i = 64 s + lane from coefficient
+  // k = i / 2 (slot s / 2, lane 32 (s % 2) + lane / 2) ----
+  for (int lev = levels - 1; lev >= 0; --lev) {
+    const int d0 = s_doff[lev];
+    double xn[SL];
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      const int i = s * kWave + lane, k = i >> 1;
+      const double A = __shfl(x[s >> 1], 32 * (s & 1) + (lane >> 1), kWave);
+      const double D = s_det[min(d0 + k, TV + kMaxLevels - 1)];  // past the level: a value nobody uses
+      xn[s] = (i & 1) ? (A - D) * inv_sqrt2 : (A + D) * inv_sqrt2;
+    }
+#pragma unroll
+    for (int s = 0; s < SL; ++s) x[s] = xn[s];
+  }
+  // x[s] at position 64 s + lane < L: r~ of that retained position
+
+  // ---- budgets (Eq. (16), Eq. (5)) ----
+  int n[SL];
+  uint64_t inM[SL];
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    n[s] = 0;
+    inM[s] = __ballot(s * kWave + lane < L);
+  }
+  if (B >= (long long)L * N) {
+#pragma unroll
+    for (int s = 0; s < SL; ++s) n[s] = s * kWave + lane < L ? N : 0;
+  } else {
+    double w[SL], wsum = 0.0;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      w[s] = s * kWave + lane < L ? fmax(x[s], 0.0) : 0.0;
+      if (s * kWave + lane < L) wsum += w[s];
+    }
+    wsum = wave_sum_f64(wsum);
+    uint64_t active[SL], full[SL];
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      if (wsum == 0.0 && s * kWave + lane < L) w[s] = 1.0;
+      active[s] = __ballot(s * kWave + lane < L && w[s] > 0.0);
+      full[s] = 0ull;
+    }
+    long long R = B;
+    while (R > 0) {
+      int na = 0;
+#pragma unroll
+      for (int s = 0; s < SL; ++s) na += __popcll(active[s]);
+      if (na == 0) {  // every weighted frame is full: spread the rest evenly
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+          active[s] = inM[s] & ~full[s];
+          if ((active[s] >> lane) & 1ull) w[s] = 1.0;
+        }
+      }
+      double S = 0.0;
+#pragma unroll
+      for (int s = 0; s < SL; ++s)
+        if ((active[s] >> lane) & 1ull) S += w[s];
+      S = wave_sum_f64(S);
+      const double Rd = double(R);
+      double q[SL];
+      int nfull = 0;
+      uint64_t cap[SL];
+#pragma unroll
+      for (int s = 0; s < SL; ++s) {
+        const bool act = (active[s] >> lane) & 1ull;
+        q[s] = act ? Rd * w[s] / S : 0.0;
+        cap[s] = __ballot(act && q[s] >= double(N));
+        nfull += __popcll(cap[s]);
+      }
+      if (nfull > 0) {
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+          if ((cap[s] >> lane) & 1ull) n[s] = N;
+          full[s] |= cap[s];
+          active[s] &= ~cap[s];
+        }
+        R -= (long long)nfull * N;
+        continue;
+      }
+      int base_sum = 0;
+      uint64_t fb[SL], cand[SL], chosen[SL];
+      uint64_t any = 0ull, all = ~0ull;
+#pragma unroll
+      for (int s = 0; s < SL; ++s) {
+        const bool act = (active[s] >> lane) & 1ull;
+        const double b = floor(q[s]);
+        if (act) {
+          n[s] = int(b);
+          base_sum += int(b);
+        }
+        // fractional parts in [0, 1): non-negative doubles order like their
+        // bit patterns
+        fb[s] = act ? __builtin_bit_cast(uint64_t, q[s] - b) : 0ull;
+        if (act) {
+          any |= fb[s];
+          all &= fb[s];
+        }
+        cand[s] = active[s];
+        chosen[s] = 0ull;
+      }
+      int need = int(R) - wave_reduce_sum_i32(base_sum);
+      // +1 for the `need` active positions ranked first by (fraction desc,
+      // index asc): a descent over the bits takes positions with the current
+      // bit set whole while they fit, else continues among them; bits on
+      // which every active position agrees decide nothing
+      any = wave_reduce_u64(any, [](uint64_t a, uint64_t b) { return a | b; });
+      all = wave_reduce_u64(all, [](uint64_t a, uint64_t b) { return a & b; });
+      const int top = (any ^ all) ? 63 - __clzll(any ^ all) : -1;
+      for (int bit = top; bit >= 0 && need > 0; --bit) {
+        int cnt = 0;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) cnt += __popcll(cand[s]);
+        if (cnt <= need) break;
+        uint64_t ones[SL];
+        int c1 = 0;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+          ones[s] = cand[s] & __ballot((fb[s] >> bit) & 1ull);
+          c1 += __popcll(ones[s]);
+        }
+        if (c1 <= need) {
+#pragma unroll
+          for (int s = 0; s < SL; ++s) {
+            chosen[s] |= ones[s];
+            cand[s] &= ~ones[s];
+          }
+          need -= c1;
+        } else {
+#pragma unroll
+          for (int s = 0; s < SL; ++s) cand[s] = ones[s];
+        }
+      }
+      // the remaining candidates all fit, or are exact ties: smaller index first
+#pragma unroll
+      for (int s = 0; s < SL; ++s)
+        for (; need > 0 && cand[s]; --need) {
+          chosen[s] |= cand[s] & (~cand[s] + 1ull);
+          cand[s] &= cand[s] - 1ull;
+        }
+#pragma unroll
+      for (int s = 0; s < SL; ++s)
+        if ((chosen[s] >> lane) & 1ull) n[s] += 1;
+      R = 0;
+    }
+  }
+
+  // ---- back to frames, offsets, rectified relevance ----
+  int nb[SL];
+  double rt[SL];
+  if (moved) {
+    order();
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      const int i = s * kWave + lane;
+      if (i < L) {
+        s_nmv[i] = n[s];
+        s_mv[0][i] = x[s];
+      }
+    }
+    order();
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      nb[s] = keep[s] ? s_nmv[kpos[s]] : 0;
+      rt[s] = keep[s] ? s_mv[0][kpos[s]] : 0.0;
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      nb[s] = keep[s] ? n[s] : 0;
+      rt[s] = keep[s] ? x[s] : 0.0;
+    }
+  }
+  int carry = 0;
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    const int t = s * kWave + lane;
+    const int incl = wave_incl_scan_i32(nb[s]);
+    if (t < T) {
+      budget[t] = nb[s];
+      offset[t] = carry + incl - nb[s];
+      if (rel_rect) rel_rect[t] = float(rt[s]);
+    }
+    carry += __builtin_amdgcn_readlane(incl, kWave - 1);
+  }
+  if (lane == 0) offset[T] = carry;
 }
 
 // Lane t loads r_t and delta_t, then the wave computes the budgets.

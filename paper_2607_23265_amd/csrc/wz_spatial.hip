@@ -7,8 +7,8 @@
 // bit and no kernel boundary separates the budget from its use.
 //
 // Workgroup (t, p), p < P, 1024 threads, works on frame t:
-//   A. wave 0 computes the budgets (T <= 256: in registers up to 64 frames,
-//      four frames per lane in LDS above; beyond 256 they come from the
+//   A. wave 0 computes the budgets (T <= 256: in registers, one frame per
+//      lane up to 64 frames, four above; beyond 256 they come from the
 //      budget kernel launched before this one) while
 //      the other waves take the frame's selection ranks and block gates
 //      (from the per-frame kernel, or formed here from the scores when the
@@ -294,7 +294,7 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
   // budgets are in s_nb)
   auto fused_budget = [&]() {
     if (T <= kWave) budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
-    else budget_body<kWave, kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+    else budget_wave_slots<kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
   };
   auto extra_prefix = [&]() {
     int carry = 0;

@@ -28,6 +28,8 @@ __global__ __launch_bounds__(NT) void k_budget(const VideoArgs<BudgetArgs> va, i
     budget_body<NT, TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect, &bank);
   else if constexpr (NT == kWave && TV == kWave)
     budget_wave_body(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
+  else if constexpr (NT == kWave && TV <= 4 * kWave)
+    budget_wave_slots<TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
   else
     budget_body<NT, TV>(a.rel, a.delta, T, N, B, levels, tau, a.budget, a.offset, a.rel_rect);
 }
