@@ -132,9 +132,11 @@ def test_workspace_reuse_across_shapes():
         assert np.array_equal(_np(b), out["budget"]) and np.array_equal(_np(idx), out["index"])
 
 
-@pytest.mark.parametrize("T", [1, 2, 3, 1023, 1024, 1025, 2048])
+@pytest.mark.parametrize("T", [1, 2, 3, 63, 64, 65, 100, 128, 129, 200, 255, 256, 257, 1023, 1024, 1025, 2048])
 def test_stage_temporal_budget_random(T):
-    """Random fp32 r and delta straight into wz_temporal_budget, up to the 2048-frame limit."""
+    """Random fp32 r and delta straight into wz_temporal_budget, up to the 2048-frame limit: one frame per
+    lane of one wave up to 64 frames, four per lane up to 256 (with tau = 0.5 the frame filter drops frames,
+    so the retained positions move), a workgroup above."""
     rng = np.random.default_rng(T)
     for trial in range(4):
         N = int(rng.choice([1, 3, 196]))
@@ -235,6 +237,10 @@ EDGE = {
     "levels_4": dict(T=37, H=4, W=4, C=64, Q=16, B=150, levels=4),
     "odd_T_levels_2": dict(T=13, H=5, W=5, C=64, Q=16, B=90, levels=2),
     "frame_filter": dict(T=16, H=4, W=4, C=64, Q=16, B=100, tau=1.0),
+    # the budgets inside the gather with four frames per lane, frames dropped
+    # by the frame filter (their retained positions move) and several levels
+    "frame_filter_T100": dict(T=100, H=4, W=4, C=64, Q=16, B=600, tau=1.0),
+    "frame_filter_T200_levels_3": dict(T=200, H=3, W=3, C=32, Q=16, B=900, levels=3, tau=1.0),
     "lambda_zero": dict(T=4, H=4, W=4, C=64, Q=16, B=20, lam=0.0),
     "large_grid": dict(T=2, H=64, W=64, C=8, Q=16, B=3000),
     "many_frames": dict(T=512, H=2, W=2, C=16, Q=16, B=1900),
