@@ -414,6 +414,9 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
           b1[ii] = B1[ii * W + x];
           b2[ii] = B2[ii * W + x];
         }
+        // two image rows at a time: the next row's LDS reads issue before this
+        // one's entries are finished
+#pragma unroll 2
         for (int y = 0; y < H; ++y) {
           float acc = 0.f;
 #pragma unroll
