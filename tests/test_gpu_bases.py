@@ -192,6 +192,26 @@ def test_stage_temporal_budget_bases(T, tb):
     assert checked > 0
 
 
+@pytest.mark.parametrize("name,sb", [("split_32x32_c200", wz.WZ_DB4), ("split_27x27_c1152", wz.WZ_BIOR44)])
+def test_split_form_matches_fused_kernel(name, sb):
+    """bf16 inputs on a large grid: wz_condense runs the split form (the rows once per frame, then the
+    contraction), wz_spatial_dwt_condense the fused kernel.  Both form the same bf16 operator rows and
+    add each output's products in the same order (high then low part, 32-token step by step), so on the
+    same scores and offsets their rows agree bit for bit."""
+    wl, inp, _ = _case(name, wz.WZ_HAAR, sb)
+    X, q = wz.to_device(inp, DEV)
+    for out_dtype in (wz.WZ_BF16, wz.WZ_F32):
+        p = wz.problem_of(wl, out_dtype, spatial_basis=sb)
+        tok, idx, _, o = wz.condense(p, X, q)
+        a, _, _ = wz.relevance(p, X, q)
+        tok2, idx2 = wz.spatial_dwt_condense(p, X, a, o)
+        torch.cuda.synchronize()
+        n = int(o[-1].item())
+        assert n > 0
+        assert torch.equal(idx[:n], idx2[:n])
+        assert torch.equal(tok[:n], tok2[:n])
+
+
 @pytest.mark.parametrize("name", ["tiny", "split_32x32_c200"])
 def test_bases_batch_matches_single_calls(name):
     """Two videos through wz_condense_batch with filter banks (the fused form, and the split form
