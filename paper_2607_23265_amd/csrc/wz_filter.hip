@@ -17,8 +17,8 @@
 // the three detail bands get G.  Only i with s_u[h][i] != 0 contribute (at
 // most F / 2 of them), j likewise.
 //
-// Workgroup (frame t, channel slice), 512 threads (eight waves share the
-// slice-independent setup, which every slice's workgroup repeats):
+// Fused form, workgroup (frame t, channel slice), 512 threads (eight waves
+// share the slice-independent setup, which every slice's workgroup repeats):
 //   1. takes the frame's selection ranks (from the per-frame kernel, or forms
 //      them from the scores, wz_rank.h) and lists its n_t kept tokens
 //      (rank < n_t) in raster order;
@@ -34,7 +34,14 @@
 //      out_tokens[offset_t + k] (k = raster position among the kept tokens),
 //      their flat indices to out_index.
 // The frame's slice is read once per chunk of KR kept tokens (from L2 after
-// the first).  Supported: H, W <= 64, H*W <= 1024 (the host checks).
+// the first, while the slices of the workgroups on an XCD fit its L2).
+// Split form (bf16 inputs on frames where LDS holds full-frame rows for at
+// most 16 kept tokens, which would read the slice from memory once per
+// chunk): the same kernel with ROWS, one workgroup per frame, does 1-3 and
+// writes the rows to the workspace instead of contracting them; then
+// k_filter_contract keeps up to 48 rows in its accumulators while each wave
+// streams its 128 channels of the frame once.
+// Supported: H, W <= 64, H*W <= 1024 (the host checks).
 #include "wz_rank.h"
 #include "wz_wavelets.h"
 
