@@ -101,3 +101,25 @@ def test_condense_queries_oracle_every_query():
         assert np.array_equal(b[g].cpu().numpy(), ref["budget"]), g
         assert np.array_equal(idx[g][:k].cpu().numpy(), ref["index"]), g
         assert G.within(tok[g][:k].cpu().numpy(), ref["tokens"], G.tol_for(wl.dtype)), g
+
+
+@pytest.mark.parametrize("name,sb,n", [("t64_14x14_c3584", wz.WZ_DB4, 2), ("split_32x32_c200", wz.WZ_BIOR44, 3)])
+def test_condense_queries_filter_bank_matches_single(name, sb, n):
+    """With a db4 / bior4.4 spatial basis (the fused kernel at 14x14, the split form with its rows in the
+    workspace on a large bf16 grid) each query's outputs are bitwise those of its single call."""
+    if name == "split_32x32_c200":
+        wl, inp, _ = _random_case(0, T=3, H=32, W=32, C=200, Q=16, B=300)
+    else:
+        wl, inp, _ = _case(name)
+    p = wz.problem_of(wl, wz.WZ_BF16, spatial_basis=sb)
+    X, q0 = wz.to_device(inp, DEV)
+    qs = _queries(q0, n)
+    tok, idx, b, o = wz.condense_queries(p, X, qs)
+    singles = [wz.condense(p, X, qs[g]) for g in range(n)]
+    torch.cuda.synchronize()
+    for g, (t1, i1, b1, o1) in enumerate(singles):
+        k = int(o1[-1])
+        assert k > 0
+        assert torch.equal(b[g], b1) and torch.equal(o[g], o1), g
+        assert torch.equal(idx[g][:k], i1[:k]), g
+        assert torch.equal(_bits(tok[g][:k]), _bits(t1[:k])), g
