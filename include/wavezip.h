@@ -253,8 +253,10 @@ wz_status wz_condense_queries(const wz_config* cfg, int32_t queries,
  * forbid hipMalloc).  Same arguments, outputs and results as wz_condense
  * (bitwise), minus ws / ws_bytes: the intermediates live in a static device
  * array of wz_noalloc_scratch_bytes() = 32 MiB that the library holds on each
- * GPU it runs on until the process ends.  A problem whose
- * wz_workspace_bytes(cfg) exceeds that returns WZ_ERR_SCRATCH before anything
+ * GPU it runs on until the process ends.  When wz_workspace_bytes(cfg)
+ * exceeds that only through the filter-bank operator rows, the modulator
+ * keeps them in LDS instead (its one-kernel form; the same results); a
+ * problem that does not fit even then returns WZ_ERR_SCRATCH before anything
  * is enqueued.  The call allocates and frees nothing; its first call on a
  * device looks up that device's array (hipGetSymbolAddress) under a lock.
  * Every call on one GPU shares that GPU's array: calls that overlap on one GPU

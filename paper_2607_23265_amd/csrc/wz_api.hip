@@ -81,10 +81,12 @@ wz_status from_hip(hipError_t e) { return e == hipSuccess ? WZ_OK : WZ_ERR_DEVIC
 namespace {
 
 // The whole pass for V videos of one shape (wz_condense, wz_condense_batch).
-// V videos (shared_x false) or V queries over one video (shared_x true)
+// V videos (shared_x false) or V queries over one video (shared_x true);
+// split: the workspace layout with the filter-bank operator rows (see
+// workspace_layout)
 wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void* X, const void* query,
                           void* out_tokens, int32_t* out_index, int32_t* budget, int32_t* offset, void* ws,
-                          size_t ws_bytes, void* stream) {
+                          size_t ws_bytes, void* stream, bool split = true) {
   WZ_TRY(check_config(cfg));
   WZ_TRY(check_ptr(X, 16));
   WZ_TRY(check_ptr(query, 16));
@@ -95,7 +97,7 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   if (budget && !aligned(budget, 4)) return WZ_ERR_ALIGN;
   if (offset && !aligned(offset, 4)) return WZ_ERR_ALIGN;
   if (!ws) return WZ_ERR_NULL;
-  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws));
+  const Workspace w = workspace_layout(*cfg, static_cast<char*>(ws), split);
   if (!aligned(ws, 256) || ws_bytes / size_t(V) < w.bytes) return WZ_ERR_WORKSPACE;
   const int s_in = cfg->in_dtype == WZ_BF16 ? 2 : 4, s_out = cfg->out_dtype == WZ_BF16 ? 2 : 4;
   const long long TN = (long long)cfg->T * cfg->H * cfg->W;
@@ -225,11 +227,14 @@ size_t wz_noalloc_scratch_bytes(void) { return kScratchBytes; }
 wz_status wz_condense_noalloc(const wz_config* cfg, const void* X, const void* query, void* out_tokens,
                               int32_t* out_index, int32_t* budget, int32_t* offset, void* stream) {
   WZ_TRY(check_config(cfg));
-  const size_t need = workspace_layout(*cfg, nullptr).bytes;
-  if (need > kScratchBytes) return WZ_ERR_SCRATCH;
+  // the filter-bank operator rows in the scratch if they fit, else the
+  // modulator's fused form (the same rows bit for bit, kept in LDS)
+  const bool split = workspace_layout(*cfg, nullptr, true).bytes <= kScratchBytes;
+  if (!split && workspace_layout(*cfg, nullptr, false).bytes > kScratchBytes) return WZ_ERR_SCRATCH;
   void* ws = nullptr;
   WZ_TRY(scratch_of_current_device(&ws));
-  return condense_videos(cfg, 1, false, X, query, out_tokens, out_index, budget, offset, ws, kScratchBytes, stream);
+  return condense_videos(cfg, 1, false, X, query, out_tokens, out_index, budget, offset, ws, kScratchBytes, stream,
+                         split);
 }
 
 wz_status wz_condense_batch(const wz_config* cfg, int32_t videos, const void* X, const void* query,

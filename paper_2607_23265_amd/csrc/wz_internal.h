@@ -202,7 +202,9 @@ struct Workspace {
 
 inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-inline Workspace workspace_layout(const wz_config& c, char* base) {
+// split: room for the filter-bank operator rows when the problem uses them
+// (without it the modulator runs its fused form, which keeps them in LDS).
+inline Workspace workspace_layout(const wz_config& c, char* base, bool split = true) {
   const RelPlan pl = relevance_plan(c);
   const size_t T = c.T, N = size_t(c.H) * c.W, C = c.C, Q = c.Q, QP = qpad(c.Q), tiles = pl.tiles,
                S = pl.slices;
@@ -223,7 +225,7 @@ inline Workspace workspace_layout(const wz_config& c, char* base) {
   w.frame_delta = reinterpret_cast<float*>(take(T * 4));
   w.budget = reinterpret_cast<int32_t*>(take(T * 4));
   w.offset = reinterpret_cast<int32_t*>(take((T + 1) * 4));
-  const size_t frows = filter_rows_bytes(c);
+  const size_t frows = split ? filter_rows_bytes(c) : 0;
   w.frows = frows ? reinterpret_cast<uint16_t*>(take(frows)) : nullptr;
   w.bytes = off;
   return w;

@@ -67,6 +67,20 @@ def test_two_calls_second_smaller():
         assert G.within(_np(tok)[:n], want["tokens"], G.TOL_F32_IN if small.dtype == "f32" else G.TOL_BF16_IN)
 
 
+def test_filter_rows_beyond_scratch_use_the_fused_form():
+    """db4 on a large bf16 grid with most tokens kept: the operator rows alone would not fit the scratch,
+    so the call forms them in LDS (the fused form); its outputs equal wz_condense's (which has them in its
+    workspace) bit for bit."""
+    wl = synth.Workload("noalloc_split_T20_27x27", T=20, H=27, W=27, C=256, Q=16, dtype="bf16", B=14000)
+    p = wz.problem_of(wl, wz.WZ_BF16, spatial_basis=wz.WZ_DB4)
+    assert wz.workspace_bytes(p) > wz.lib().wz_noalloc_scratch_bytes()
+    print(f"[case] noalloc {wl.name} T={wl.T} C={wl.C} Q={wl.Q} B={wl.B} db4", flush=True)
+    X, q = wz.to_device(synth.generate(wl), DEV)
+    ref, got = _both(p, X, q)
+    assert int(ref[3][-1]) > 0
+    _same(ref, got)
+
+
 def test_rejects_problem_beyond_scratch():
     L = wz.lib()
     p = wz.Problem(T=2048, H=14, W=14, C=3584, Q=32, B=1000)
