@@ -196,7 +196,9 @@ __device__ void scores_role(const FrameArgs& f, int t) {
 template <int NTH>
 __device__ void lead_role(const FrameArgs& f, int t) {
   constexpr int kNW = NTH / kWave;
-  constexpr int TB = 4;  // tiles of the channel sums loaded at once
+  // tiles of the channel sums loaded at once (1024 threads: every tile of a
+  // frame split into up to 8, one vector each, so the reads take one round)
+  constexpr int TB = NTH <= 256 ? 4 : 8;
   __shared__ double s_red[4][kNW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int C = f.C, Q = f.Q, S = f.slices, tiles = f.tiles, K = tiles * S, C4 = C / 4;
@@ -332,7 +334,10 @@ hipError_t launch_frame(const wz_config& c, const Workspace& ws, float* tok_scor
   // key 8 B; rank, byrank, gate, bin order (and level-2 gate) 4 B
   const size_t lds = roles == 2 ? size_t(N) * (c.spatial_levels == 2 ? 28 : 24) : 0;
   const dim3 grid((c.T + kXcds - 1) / kXcds * kXcds * roles, vs.V);
-  if (pl.slices > 1) hipLaunchKernelGGL((k_frame<kPartThreads>), grid, dim3(kPartThreads), lds, s, va);
+  // 1024 threads when the scores come from slice partials, or when frames
+  // are split into many tiles (few frames: the lead's reads spread over more
+  // threads and go out in one round)
+  if (pl.slices > 1 || pl.tiles >= 8) hipLaunchKernelGGL((k_frame<kPartThreads>), grid, dim3(kPartThreads), lds, s, va);
   else hipLaunchKernelGGL((k_frame<kThreads>), grid, dim3(kThreads), lds, s, va);
   return hipGetLastError();
 }
