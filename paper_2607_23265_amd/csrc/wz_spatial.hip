@@ -293,7 +293,10 @@ __global__ __launch_bounds__(kThreads) void k_assign_gather(const VideoArgs<Assi
   // s_ext[t] = kept tokens of rank >= kp in frames before t (one wave; the
   // budgets are in s_nb)
   auto fused_budget = [&]() {
+    // (slots per lane for the frames at hand: the positions' layout and the
+    // sums do not depend on the slot count, so neither do the budgets)
     if (T <= kWave) budget_wave_compute(bd, br, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
+    else if (T <= 2 * kWave) budget_wave_slots<2 * kWave>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
     else budget_wave_slots<kFusedTMax>(f.rel, f.delta, T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr);
   };
   auto extra_prefix = [&]() {

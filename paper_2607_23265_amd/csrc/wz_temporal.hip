@@ -55,6 +55,7 @@ hipError_t launch_budget(const wz_config& c, const float* frame_rel, const float
                          advance(offset, v * vs.off), advance(rel_rect, v * vs.ws)};
   // (a filter bank's convolutions spread better over four waves)
   if (c.T <= 64) launch_k<kWave, 64>(c, va, vs.V, s);
+  else if (c.T <= 128 && c.temporal_basis == WZ_HAAR) launch_k<kWave, 128>(c, va, vs.V, s);
   else if (c.T <= 256 && c.temporal_basis == WZ_HAAR) launch_k<kWave, 256>(c, va, vs.V, s);
   else if (c.T <= 256) launch_k<256, 256>(c, va, vs.V, s);
   else launch_k<1024, kTMax>(c, va, vs.V, s);
