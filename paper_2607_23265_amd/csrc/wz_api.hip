@@ -125,6 +125,9 @@ wz_status condense_videos(const wz_config* cfg, int V, bool shared_x, const void
   }
   int32_t* bud = budget ? budget : w.budget;
   int32_t* off = offset ? offset : w.offset;
+  if (filt && filter_budget_folds(*cfg))  // budgets inside the modulator's first kernel
+    return from_hip(launch_filter_assign(*cfg, X, w.tok_score, nullptr, w.rank, w.frows, out_tokens, out_index, s, vs,
+                                         FoldedBudget{w.frame_rel, w.frame_delta, bud, off}));
   WZ_TRY(from_hip(launch_budget(*cfg, w.frame_rel, w.frame_delta, bud, off, nullptr, s, vs)));
   if (filt)
     return from_hip(launch_filter_assign(*cfg, X, w.tok_score, off, w.rank, w.frows, out_tokens, out_index, s, vs));

@@ -466,10 +466,11 @@ __device__ void budget_body(const float* __restrict__ rel, const float* __restri
 // ---------------------------------------------------------------------------
 // Runs on one whole wave (wave 0 of its workgroup).  Lane t holds delta_t
 // and r_t (anything for lanes >= T); outputs may point to global memory or
-// LDS.
-__device__ void budget_wave_compute(double d, double r, int T, int N, long long B, int levels, float tau,
-                                    int32_t* __restrict__ budget, int32_t* __restrict__ offset,
-                                    float* __restrict__ rel_rect) {
+// LDS; det is LDS for every level's detail coefficients, [levels][kWave].
+__device__ __forceinline__ void budget_wave_compute_det(double d, double r, int T, int N, long long B, int levels,
+                                                        float tau, int32_t* __restrict__ budget,
+                                                        int32_t* __restrict__ offset, float* __restrict__ rel_rect,
+                                                        double* __restrict__ det) {
   const double inv_sqrt2 = 0.70710678118654752440;
   auto dadd = [](double a, double b) { return a + b; };
   const int lane = threadIdx.x & 63;
@@ -491,13 +492,12 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
 
   // ---- WTA: J-level gated Haar analysis (Eq. (9)-(10)); lanes beyond a
   // level's length hold values nobody reads ----
-  __shared__ double s_det[kMaxLevels][kWave];
   int len = L;
   for (int lev = 0; lev < levels; ++lev) {
     const int i0 = min(2 * lane, kWave - 1), i1 = min(min(2 * lane + 1, len - 1), kWave - 1);
     const double x0 = __shfl(x, i0, kWave), x1 = __shfl(x, i1, kWave);
     const double gp = 0.5 * (__shfl(g, i0, kWave) + __shfl(g, i1, kWave));
-    s_det[lev][lane] = gp * ((x0 - x1) * inv_sqrt2);
+    det[lev * kWave + lane] = gp * ((x0 - x1) * inv_sqrt2);
     x = (x0 + x1) * inv_sqrt2;
     g = gp;
     len = (len + 1) / 2;
@@ -505,7 +505,7 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
   // ---- inverse DWT (Eq. (11)) ----
   for (int lev = levels - 1; lev >= 0; --lev) {
     const int k = lane >> 1;
-    const double A = __shfl(x, k, kWave), Dk = s_det[lev][k];
+    const double A = __shfl(x, k, kWave), Dk = det[lev * kWave + k];
     x = (lane & 1) ? (A - Dk) * inv_sqrt2 : (A + Dk) * inv_sqrt2;
   }
   // x in lane i < L: r~ of retained position i
@@ -587,6 +587,13 @@ __device__ void budget_wave_compute(double d, double r, int T, int N, long long 
     if (rel_rect) rel_rect[lane] = keep ? float(rt) : 0.f;
   }
   if (lane == T - 1) offset[T] = incl;
+}
+// The same with the detail coefficients in a static LDS array of its own.
+__device__ void budget_wave_compute(double d, double r, int T, int N, long long B, int levels, float tau,
+                                    int32_t* __restrict__ budget, int32_t* __restrict__ offset,
+                                    float* __restrict__ rel_rect) {
+  __shared__ double s_det[kMaxLevels * kWave];
+  budget_wave_compute_det(d, r, T, N, B, levels, tau, budget, offset, rel_rect, s_det);
 }
 
 // ---------------------------------------------------------------------------

@@ -21,7 +21,12 @@
 // share the slice-independent setup, which every slice's workgroup repeats):
 //   1. takes the frame's selection ranks (from the per-frame kernel, or forms
 //      them from the scores, wz_rank.h) and lists its n_t kept tokens
-//      (rank < n_t) in raster order;
+//      (rank < n_t) in raster order.  With the whole pass, T <= 64 and the
+//      Haar temporal basis, wave 0 first computes every frame's budget
+//      (Eq. (9)-(11), Eq. (16) under Eq. (5); the selection kernel's one-wave
+//      arithmetic, so every workgroup gets the same budgets bit for bit)
+//      while the other waves read the ranks, and no budget launch precedes
+//      this one;
 //   2. forms G and the per-axis analysis rows a_u in LDS;
 //   3. per chunk of KR kept tokens builds their rows L_p in LDS (fp32,
 //      through the partial sums B_i(w') = sum_j over the width) and
@@ -42,6 +47,7 @@
 // k_filter_contract keeps up to 48 rows in its accumulators while each wave
 // streams its 128 channels of the frame once.
 // Supported: H, W <= 64, H*W <= 1024 (the host checks).
+#include "wz_budget.h"
 #include "wz_rank.h"
 #include "wz_wavelets.h"
 
@@ -60,14 +66,18 @@ constexpr int kMaxAct = kMaxTaps / 2;  // synthesis rows touching one output sam
 struct FilterArgs {
   const void* X;            // [T][H][W][C]
   const float* tok_score;   // [T][H*W]
-  const int32_t* offset;    // [T+1]
+  const int32_t* offset;    // [T+1], or null: the budgets are computed here
+  const float* rel;         // [T] r_t        (budgets computed here; T <= 64, Haar temporal basis)
+  const float* delta;       // [T] delta_t
+  int32_t* budget_out;      // [T] or null    (budgets computed here; written by workgroup (0, 0))
+  int32_t* offset_out;      // [T+1]          (budgets computed here)
   const int32_t* rank;      // [T][H*W] selection ranks from the per-frame kernel, or null (ranked here)
   uint16_t* rows;           // [B][2][pad_tokens(H*W)] the row kernel's output (bf16 high, low part)
   void* out_tokens;         // [B][C]
   int32_t* out_index;       // [B]
   long long B;
-  int T, H, W, C;
-  float lam;
+  int T, H, W, C, levels;
+  float lam, tau;
 };
 static_assert(sizeof(VideoArgs<FilterArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
 
@@ -111,7 +121,7 @@ __device__ __forceinline__ void store8<float>(__amdgpu_buffer_rsrc_t r, int off,
 // Dynamic LDS of a frame of H x W tokens and chunks of kr rows: byte offsets
 // of the arrays (the operator rows 16-byte aligned) and the total.
 struct FilterLds {
-  size_t M, kept, G, AH, AW, SH, SW, B, L, bytes;
+  size_t M, kept, G, AH, AW, SH, SW, B, L, det, bytes;
 };
 // Tokens padded to whole MFMA K steps, and the row stride (bf16 elements) of
 // the operator rows in their MFMA form: 8 more than the padded length, so the
@@ -120,8 +130,9 @@ __host__ __device__ inline int pad_tokens(int N) { return (N + 31) / 32 * 32; }
 __host__ __device__ inline int mfma_row_stride(int N) { return pad_tokens(N) + 8; }
 // mfma: the operator rows as bf16 high and low parts
 // [2][max(kr, 16)][mfma_row_stride] (bf16 inputs; whole 16-row MFMA tiles)
-// instead of fp32 [N][kr].
-__host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr, bool mfma) {
+// instead of fp32 [N][kr].  det_levels: the budget's detail coefficients
+// [det_levels][kWave] fp64 last (budgets computed in the kernel), or none.
+__host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr, bool mfma, int det_levels = 0) {
   const size_t N = size_t(H) * W, nh = bank_len(H, F), nw = bank_len(W, F);
   FilterLds o;
   // the ranking's key, rank, byrank, gate and bin order come first (24 N bytes)
@@ -134,7 +145,8 @@ __host__ __device__ inline FilterLds filter_lds(int H, int W, int F, int kr, boo
   o.SW = o.SH + 2 * size_t(H) * kMaxAct * 4;  // along the width [2][W][kMaxAct]
   o.B = o.SW + 2 * size_t(W) * kMaxAct * 4;   // partial sums B1, B2 [kr][2][kMaxAct][W]
   o.L = (o.B + size_t(kr) * 2 * kMaxAct * W * 4 + 15) / 16 * 16;  // operator rows [N][kr], 16-byte aligned
-  o.bytes = o.L + (mfma ? size_t(2) * (kr < 16 ? 16 : kr) * mfma_row_stride(int(N)) * 2 : N * kr * 4);
+  o.det = o.L + (mfma ? size_t(2) * (kr < 16 ? 16 : kr) * mfma_row_stride(int(N)) * 2 : N * kr * 4);
+  o.bytes = o.det + size_t(det_levels) * kWave * 8;
   return o;
 }
 
@@ -210,16 +222,28 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   if (t >= f.T) return;  // whole workgroup
   const int H = f.H, W = f.W, N = H * W, F = bank.F, C = f.C;
   const int nh = bank_len(H, F), nw = bank_len(W, F);
-  const long long base = f.offset[t];
-  const int nt = min(max(f.offset[t + 1] - int(base), 0), N);
-  const long long total = min((long long)f.offset[f.T], f.B);
-  if (nt == 0) return;  // whole workgroup
+  // with the offsets given, a frame that keeps nothing is done; otherwise
+  // wave 0 computes the budgets (from r and delta, the selection kernel's
+  // one-wave arithmetic) while the other waves take the frame's ranks and
+  // build the tables
+  const bool wb = f.offset == nullptr;
+  long long base = 0, total = 0;
+  int nt = 0;
+  if (!wb) {
+    base = f.offset[t];
+    nt = min(max(f.offset[t + 1] - int(base), 0), N);
+    total = min((long long)f.offset[f.T], f.B);
+    if (nt == 0) return;  // whole workgroup
+  }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // threads that rank and build while wave 0 computes the budgets
+  const int g0 = wb ? kWave : 0, gtid = tid - g0, gthreads = kFThreads - g0;
 
   extern __shared__ __align__(16) char s_dyn[];
   __shared__ int s_start[kBins], s_fill[kBins];
   __shared__ float s_mm[2 * kFWaves];
   __shared__ int s_wsum[kFWaves];
+  __shared__ int32_t s_nb[kWave], s_off[kWave + 1];  // budgets and offsets (computed here)
   RankLds rl;
   rl.key = reinterpret_cast<uint64_t*>(s_dyn);
   rl.rank = reinterpret_cast<int32_t*>(rl.key + N);
@@ -231,7 +255,7 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   rl.fill = s_fill;
   rl.mm = s_mm;
   constexpr bool MF = sizeof(In) == 2;  // bf16 inputs: the contraction runs on MFMA
-  const FilterLds lo_ = filter_lds(H, W, F, KR, MF);
+  const FilterLds lo_ = filter_lds(H, W, F, KR, MF, wb ? f.levels : 0);
   float* s_M = reinterpret_cast<float*>(s_dyn + lo_.M);           // [N] saliency M
   int32_t* s_kept = reinterpret_cast<int32_t*>(s_dyn + lo_.kept);  // [nt] kept tokens in raster order
   float* s_G = reinterpret_cast<float*>(s_dyn + lo_.G);           // [nh][nw] gates
@@ -245,20 +269,28 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
   constexpr int LR = KR < 16 ? 16 : KR;                            // rows of a part: whole 16-row tiles
   const int LS = mfma_row_stride(N), NP = pad_tokens(N);
 
-  // ---- 1. ranks from the scores; kept tokens in raster order ----
-  {
+  // ---- 1. ranks from the scores (and the budgets); kept tokens in raster order ----
+  if (wb && wave == 0) {
+    const double d = lane < f.T ? double(f.delta[lane]) : 0.0, r = lane < f.T ? double(f.rel[lane]) : 0.0;
+    budget_wave_compute_det(d, r, f.T, N, f.B, f.levels, f.tau, s_nb, s_off, nullptr,
+                            reinterpret_cast<double*>(s_dyn + lo_.det));
+    if (lane == 0) {  // no scores in this wave
+      s_mm[0] = INFINITY;
+      s_mm[kFWaves] = -INFINITY;
+    }
+  } else {
     const __amdgpu_buffer_rsrc_t ares = make_rsrc(f.tok_score + size_t(t) * N, uint32_t(N) * 4);
     float lo = INFINITY, hi = -INFINITY;
-    for (int n0 = 0; n0 < N; n0 += 4 * kFThreads) {
+    for (int n0 = 0; n0 < N; n0 += 4 * gthreads) {
       float av[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int n = n0 + u * kFThreads + tid;
+        const int n = n0 + u * gthreads + gtid;
         av[u] = buf_load_f32(ares, n < N ? n * 4 : kOOB);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int n = n0 + u * kFThreads + tid;
+        const int n = n0 + u * gthreads + gtid;
         if (n < N) {
           rl.key[n] = sel_key(av[u], n);
           lo = fminf(lo, av[u]);
@@ -269,7 +301,7 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
     if (f.rank) {
       // the per-frame kernel's ranks (the same ranking of the same keys); the
       // frame's score extremes per wave, as the ranking leaves them
-      for (int n = tid; n < N; n += kFThreads) rl.rank[n] = f.rank[size_t(t) * N + n];
+      for (int n = gtid; n < N; n += gthreads) rl.rank[n] = f.rank[size_t(t) * N + n];
       lo = wave_min_f32(lo);
       hi = wave_max_f32(hi);
       if (lane == 0) {
@@ -277,10 +309,23 @@ __global__ __launch_bounds__(kFThreads) void k_filter_assign(const VideoArgs<Fil
         s_mm[kFWaves + wave] = hi;
       }
     } else {
+      // (the offsets are given whenever the ranks are not, so every wave is here)
       rank_frame<kFThreads>(N, H, W, f.lam, lo, hi, rl);
     }
   }
   __syncthreads();
+  if (wb) {
+    base = s_off[t];
+    nt = min(s_off[t + 1] - s_off[t], N);
+    total = min((long long)s_off[f.T], f.B);
+    if (t == 0 && sl == 0) {
+      for (int i = tid; i <= f.T; i += kFThreads) {
+        if (i < f.T && f.budget_out) f.budget_out[i] = s_nb[i];
+        f.offset_out[i] = s_off[i];
+      }
+    }
+    if (nt == 0) return;  // whole workgroup
+  }
   {
     // the frame's extremes, as the ranking formed them; M by Eq. (7)
     float lo = s_mm[0], hi = s_mm[kFWaves];
@@ -714,17 +759,18 @@ __global__ __launch_bounds__(kFThreads) void k_filter_contract(const VideoArgs<R
 constexpr size_t kFilterLdsMax = (160 - 4) * 1024;
 
 // rows per chunk: the most (32, 16 or 8) whose LDS fits
-int filter_rows(int H, int W, int F, bool mfma) {
+int filter_rows(int H, int W, int F, bool mfma, int det_levels = 0) {
   for (int kr = 32; kr >= 8; kr /= 2)
-    if (filter_lds(H, W, F, kr, mfma).bytes <= kFilterLdsMax) return kr;
+    if (filter_lds(H, W, F, kr, mfma, det_levels).bytes <= kFilterLdsMax) return kr;
   return 0;
 }
 
 // the row kernel: one workgroup per frame
-void launch_filter_rows(const wz_config& c, const VideoArgs<FilterArgs>& va, int V, const Bank& bank, hipStream_t s) {
+void launch_filter_rows(const wz_config& c, const VideoArgs<FilterArgs>& va, int V, const Bank& bank, int det_levels,
+                        hipStream_t s) {
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds), V), block(kFThreads);
-  const int kr = filter_rows(c.H, c.W, bank.F, true);
-  const size_t lds = filter_lds(c.H, c.W, bank.F, kr, true).bytes;
+  const int kr = filter_rows(c.H, c.W, bank.F, true, det_levels);
+  const size_t lds = filter_lds(c.H, c.W, bank.F, kr, true, det_levels).bytes;
   if (kr == 32) hipLaunchKernelGGL((k_filter_assign<uint16_t, uint16_t, 32, true>), grid, block, lds, s, va, bank);
   else if (kr == 16) hipLaunchKernelGGL((k_filter_assign<uint16_t, uint16_t, 16, true>), grid, block, lds, s, va, bank);
   else hipLaunchKernelGGL((k_filter_assign<uint16_t, uint16_t, 8, true>), grid, block, lds, s, va, bank);
@@ -739,12 +785,12 @@ void launch_contract_typed(const wz_config& c, const VideoArgs<RowsArgs>& va, in
 
 template <typename In, typename Out>
 void launch_filter_typed(const wz_config& c, const VideoArgs<FilterArgs>& va, int V, const Bank& bank,
-                         hipStream_t s) {
+                         int det_levels, hipStream_t s) {
   constexpr bool mfma = sizeof(In) == 2;
   const int S = (c.C + filter_slice(mfma) - 1) / filter_slice(mfma);
   const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
-  const int kr = filter_rows(c.H, c.W, bank.F, mfma);
-  const size_t lds = filter_lds(c.H, c.W, bank.F, kr, mfma).bytes;
+  const int kr = filter_rows(c.H, c.W, bank.F, mfma, det_levels);
+  const size_t lds = filter_lds(c.H, c.W, bank.F, kr, mfma, det_levels).bytes;
   if (kr == 32) hipLaunchKernelGGL((k_filter_assign<In, Out, 32>), grid, block, lds, s, va, bank);
   else if (kr == 16) hipLaunchKernelGGL((k_filter_assign<In, Out, 16>), grid, block, lds, s, va, bank);
   else hipLaunchKernelGGL((k_filter_assign<In, Out, 8>), grid, block, lds, s, va, bank);
@@ -765,22 +811,41 @@ bool filter_split(const wz_config& c) {
   return c.spatial_basis != WZ_HAAR && c.in_dtype == WZ_BF16 && filter_rows(c.H, c.W, kMaxTaps, true) < 32;
 }
 
+bool filter_budget_folds(const wz_config& c) {
+  if (c.T > kWave || c.temporal_basis != WZ_HAAR || c.spatial_basis == WZ_HAAR || !filter_assign_supported(c))
+    return false;
+  // only where the budget's LDS leaves the rows per chunk as they are
+  const int F = make_bank(c.spatial_basis).F;
+  const bool mf = c.in_dtype == WZ_BF16;
+  return filter_rows(c.H, c.W, F, mf, c.levels) == filter_rows(c.H, c.W, F, mf) &&
+         filter_rows(c.H, c.W, F, true, c.levels) == filter_rows(c.H, c.W, F, true);
+}
+
 size_t filter_rows_bytes(const wz_config& c) {
   return filter_split(c) ? size_t(c.B) * 4 * pad_tokens(c.H * c.W) : 0;
 }
 
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
                                 const int32_t* rank, uint16_t* rows, void* out_tokens, int32_t* out_index,
-                                hipStream_t s, const Videos& vs) {
+                                hipStream_t s, const Videos& vs, const FoldedBudget& fb) {
   if (!filter_assign_supported(c) || c.spatial_basis == WZ_HAAR) return hipErrorInvalidValue;
   if (rows && c.in_dtype != WZ_BF16) return hipErrorInvalidValue;
+  // budgets computed in the kernel: one wave, Haar temporal basis, with the
+  // per-frame kernel's ranks; otherwise the offsets are given
+  const bool wb = fb.rel != nullptr;
+  if (wb ? (!filter_budget_folds(c) || !rank || !fb.delta || !fb.offset) : !offset) return hipErrorInvalidValue;
+  const int det_levels = wb ? c.levels : 0;
   const Bank bank = make_bank(c.spatial_basis);
   VideoArgs<FilterArgs> va{};
   for (int v = 0; v < vs.V; ++v) {
     FilterArgs& a = va.v[v];
     a.X = advance(X, v * vs.x);
     a.tok_score = advance(tok_score, v * vs.ws);
-    a.offset = advance(offset, v * vs.off);
+    a.offset = wb ? nullptr : advance(offset, v * vs.off);
+    a.rel = wb ? advance(fb.rel, v * vs.ws) : nullptr;
+    a.delta = wb ? advance(fb.delta, v * vs.ws) : nullptr;
+    a.budget_out = wb ? advance(fb.budget, v * vs.bud) : nullptr;
+    a.offset_out = wb ? advance(fb.offset, v * vs.off) : nullptr;
     a.rank = advance(rank, v * vs.ws);
     a.rows = advance(rows, v * vs.ws);
     a.out_tokens = advance(out_tokens, v * vs.out);
@@ -790,16 +855,18 @@ hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* 
     a.H = c.H;
     a.W = c.W;
     a.C = c.C;
+    a.levels = c.levels;
     a.lam = c.lambda_;
+    a.tau = c.tau;
   }
   if (rows) {
     // split form: the rows once per frame, then the contraction per slice
-    launch_filter_rows(c, va, vs.V, bank, s);
+    launch_filter_rows(c, va, vs.V, bank, det_levels, s);
     VideoArgs<RowsArgs> ra{};
     for (int v = 0; v < vs.V; ++v) {
       RowsArgs& a = ra.v[v];
       a.X = va.v[v].X;
-      a.offset = va.v[v].offset;
+      a.offset = wb ? va.v[v].offset_out : va.v[v].offset;
       a.rows = va.v[v].rows;
       a.out_tokens = va.v[v].out_tokens;
       a.B = c.B;
@@ -810,11 +877,11 @@ hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* 
     if (c.out_dtype == WZ_BF16) launch_contract_typed<uint16_t>(c, ra, vs.V, s);
     else launch_contract_typed<float>(c, ra, vs.V, s);
   } else if (c.in_dtype == WZ_BF16) {
-    if (c.out_dtype == WZ_BF16) launch_filter_typed<uint16_t, uint16_t>(c, va, vs.V, bank, s);
-    else launch_filter_typed<uint16_t, float>(c, va, vs.V, bank, s);
+    if (c.out_dtype == WZ_BF16) launch_filter_typed<uint16_t, uint16_t>(c, va, vs.V, bank, det_levels, s);
+    else launch_filter_typed<uint16_t, float>(c, va, vs.V, bank, det_levels, s);
   } else {
-    if (c.out_dtype == WZ_BF16) launch_filter_typed<float, uint16_t>(c, va, vs.V, bank, s);
-    else launch_filter_typed<float, float>(c, va, vs.V, bank, s);
+    if (c.out_dtype == WZ_BF16) launch_filter_typed<float, uint16_t>(c, va, vs.V, bank, det_levels, s);
+    else launch_filter_typed<float, float>(c, va, vs.V, bank, det_levels, s);
   }
   return hipGetLastError();
 }

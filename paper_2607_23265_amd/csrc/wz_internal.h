@@ -315,8 +315,21 @@ bool filter_assign_supported(const wz_config& c);
 // row kernel forms each kept token's operator row once per frame into rows,
 // then a contraction kernel applies them to the frame's channels; without it
 // one fused kernel per (frame, channel slice) forms the rows it uses.
+// Whether the filter-bank modulator computes the budgets itself (T <= 64,
+// Haar temporal basis, and LDS for them without fewer rows per chunk).
+bool filter_budget_folds(const wz_config& c);
+// With fb.rel set (filter_budget_folds(c), rank given; offset unused)
+// the kernel computes the budgets itself from fb.rel and fb.delta ([T] r_t
+// and delta_t) and writes them to fb.budget ([T], may be null) and the row
+// offsets to fb.offset ([T+1]).
+struct FoldedBudget {
+  const float* rel = nullptr;
+  const float* delta = nullptr;
+  int32_t* budget = nullptr;
+  int32_t* offset = nullptr;
+};
 hipError_t launch_filter_assign(const wz_config& c, const void* X, const float* tok_score, const int32_t* offset,
                                 const int32_t* rank, uint16_t* rows, void* out_tokens, int32_t* out_index,
-                                hipStream_t s, const Videos& vs = Videos{});
+                                hipStream_t s, const Videos& vs = Videos{}, const FoldedBudget& fb = FoldedBudget{});
 
 }  // namespace wz

@@ -108,6 +108,22 @@ CASES = [
     ("split_32x32_c200", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_BF16),
     ("split_32x32_c200", wz.WZ_BIOR44, wz.WZ_BIOR44, wz.WZ_F32),
     ("split_27x27_c1152", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_BF16),
+    # Haar temporal basis with a filter-bank spatial basis at T <= 64: the budgets
+    # inside the modulator's first kernel (fused form, the split form's row
+    # kernel): frames that keep nothing, every token, one frame, the frame
+    # filter, several levels, fp32 inputs, lambda = 0, one-token frames
+    ("budget_zero", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("budget_one", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
+    ("budget_all", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("single_frame", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
+    ("frame_filter", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("levels_4", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
+    ("odd_T_levels_2", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("fp32_query32", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("lambda_zero", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
+    ("single_token", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
+    ("t32_14x14_c3584", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_BF16),
+    ("split_32x32_c200", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
 ]
 
 
@@ -212,12 +228,14 @@ def test_split_form_matches_fused_kernel(name, sb):
         assert torch.equal(tok[:n], tok2[:n])
 
 
+@pytest.mark.parametrize("tb", [wz.WZ_BIOR44, wz.WZ_HAAR])
 @pytest.mark.parametrize("name", ["tiny", "split_32x32_c200"])
-def test_bases_batch_matches_single_calls(name):
+def test_bases_batch_matches_single_calls(name, tb):
     """Two videos through wz_condense_batch with filter banks (the fused form, and the split form
-    with bf16 inputs on a large grid): each bitwise equal to its single call."""
-    wl, inp, _ = _case(name, wz.WZ_BIOR44, wz.WZ_DB4)
-    p = wz.problem_of(wl, wz.WZ_F32 if wl.dtype == "f32" else wz.WZ_BF16, temporal_basis=wz.WZ_BIOR44,
+    with bf16 inputs on a large grid; with the Haar temporal basis the budgets are computed in the
+    modulator's first kernel): each bitwise equal to its single call."""
+    wl, inp, _ = _case(name, tb, wz.WZ_DB4)
+    p = wz.problem_of(wl, wz.WZ_F32 if wl.dtype == "f32" else wz.WZ_BF16, temporal_basis=tb,
                       spatial_basis=wz.WZ_DB4)
     X, q = wz.to_device(inp, DEV)
     X2, q2 = X.flip(0).contiguous(), q.flip(0).contiguous()
