@@ -200,8 +200,9 @@ wz_status wz_spatial_dwt_condense(const wz_config* cfg, const void* X,
 /* The whole pass C(X, Q) of Eq. (4)/(6): stage 1, 2 and 3 in sequence on one
  * stream, intermediates kept in `ws`.  Three kernel launches: the pass over
  * X, the per-frame scores, and one kernel that computes the budgets (every
- * workgroup alike) and performs stage 3; for T > 256 or a db4 / bior4.4
- * basis the budgets get a launch of their own, and with a db4 / bior4.4
+ * workgroup alike) and performs stage 3; for T > 256, a db4 / bior4.4
+ * temporal basis, or a db4 / bior4.4 spatial basis with T > 64 the budgets
+ * get a launch of their own, and with a db4 / bior4.4
  * spatial basis on large frames (bf16 inputs) stage 3 takes two: the
  * modulator's operator rows of the kept tokens, once per frame, into the
  * workspace, then their product with the frames' channels.  out_tokens [B][C] (cfg->out_dtype) and

@@ -124,6 +124,10 @@ CASES = [
     ("single_token", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_F32),
     ("t32_14x14_c3584", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_BF16),
     ("split_32x32_c200", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
+    # above 64 frames (the budget kernel first), the frame filter moving the
+    # retained positions
+    ("t128_13x13_c3584", wz.WZ_HAAR, wz.WZ_DB4, wz.WZ_BF16),
+    ("frame_filter_T100", wz.WZ_HAAR, wz.WZ_BIOR44, wz.WZ_F32),
 ]
 
 
