@@ -622,15 +622,20 @@ struct RowsArgs {
   int T, N, C;
 };
 static_assert(sizeof(VideoArgs<RowsArgs>) <= 4096, "per-video arguments exceed the kernel argument limit");
-// A frame's channels in S slices of at most eight 128-channel waves, the
-// slices balanced (each a multiple of 128 channels).
+// A frame's channels in S slices of at most four 128-channel waves, the
+// slices balanced (each a multiple of 128 channels).  At the contraction's
+// register use (two waves a SIMD) a CU holds eight of its waves: four-wave
+// workgroups, two to a CU, keep more of them live than eight-wave ones when a
+// frame's channels leave part of a workgroup without any (at C = 1152: six
+// live waves a CU against four or five).
 constexpr int kRcWaveCh = 128;
-__host__ __device__ inline int rc_slices(int C) { return (C + kFWaves * kRcWaveCh - 1) / (kFWaves * kRcWaveCh); }
+constexpr int kRcWaves = 4;
+__host__ __device__ inline int rc_slices(int C) { return (C + kRcWaves * kRcWaveCh - 1) / (kRcWaves * kRcWaveCh); }
 __host__ __device__ inline int rc_slice_width(int C, int S) {
   return ((C + S - 1) / S + kRcWaveCh - 1) / kRcWaveCh * kRcWaveCh;
 }
 
-// Workgroup (frame t, channel slice), 8 waves of 128 channels each, no LDS
+// Workgroup (frame t, channel slice), 4 waves of 128 channels each, no LDS
 // and no barriers: sweeps of up to 16 RT rows, whose accumulators stay in
 // registers while the wave streams the frame's slice and the rows' operator
 // entries once.  C[rows][channels] += L[rows][tokens] X[tokens][channels]
@@ -644,7 +649,7 @@ __host__ __device__ inline int rc_slice_width(int C, int S) {
 // one 16-byte load per part.  Lane (r16, g) ends with rows 4g .. 4g+3 of
 // each tile for its 8 consecutive channels.
 template <typename Out, int RT>
-__global__ __launch_bounds__(kFThreads) void k_filter_contract(const VideoArgs<RowsArgs> va) {
+__global__ __launch_bounds__(kRcWaves * kWave) __attribute__((amdgpu_waves_per_eu(2))) void k_filter_contract(const VideoArgs<RowsArgs> va) {
   const RowsArgs& f = va.v[blockIdx.y];
   const int S = rc_slices(f.C);
   const int b = blockIdx.x, xcd = b % kXcds, slot = b / kXcds;
@@ -779,7 +784,7 @@ void launch_filter_rows(const wz_config& c, const VideoArgs<FilterArgs>& va, int
 template <typename Out>
 void launch_contract_typed(const wz_config& c, const VideoArgs<RowsArgs>& va, int V, hipStream_t s) {
   const int S = rc_slices(c.C);
-  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kFThreads);
+  const dim3 grid(unsigned((c.T + kXcds - 1) / kXcds * kXcds * S), V), block(kRcWaves * kWave);
   hipLaunchKernelGGL((k_filter_contract<Out, 3>), grid, block, 0, s, va);
 }
 
