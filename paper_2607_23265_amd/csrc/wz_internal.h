@@ -108,7 +108,7 @@ inline RelPlan relevance_plan(const wz_config& c) {
     p.mt = 0;
     p.slices = 1;
     p.kc = c.C;
-    p.threads = 8 * 64;
+    p.threads = 8 * 64;  // (the launcher takes four waves for one pass of two query tiles)
   } else if (p.kind == kRelWg) {
     // tiles of at most 128 tokens; two workgroups share a CU.  Every
     // workgroup streams its tile's rows and the whole query through LDS:

@@ -323,9 +323,11 @@ constexpr uint32_t kBf16OneHi = 0x3F800000u;  // bf16 pair (0, 1)
 // ---------------------------------------------------------------------------
 // A workgroup owns one tile of at most 64 tokens of one frame with ALL its
 // channels, so a_{t,n} is final here and no per-slice partial scores are
-// written; its tokens are one contiguous stretch of X.  The eight waves split
-// the channels into 64-channel chunks (wave w takes chunks w, w + 8, ...) and
-// never wait for each other until the epilogue.  Per chunk a wave
+// written; its tokens are one contiguous stretch of X.  The W waves (eight;
+// four for one pass of two query tiles with the channel sums in LDS, where
+// that measured faster) split the channels into 64-channel chunks (wave w
+// takes chunks w, w + W, ...) and never wait for each other until the
+// epilogue.  Per chunk a wave
 //   1. loads the tile's rows and the query's rows for the chunk (8 rows x 128
 //      bytes per instruction, whole cache lines; the query is L2-resident);
 //   2. stores both to its own LDS buffers (16-byte units XOR-swizzled by row)
@@ -354,8 +356,11 @@ constexpr int kTokQMax = 256;      // query tokens: at most four passes of 64 ov
 // pass over the tile per NQ query rows (its later reads mostly from cache),
 // a_{t,n} the maximum over the passes, the channel sums taken in the first.
 enum TokMode { kTokOne = 0, kTokGroups = 1, kTokPasses = 2 };
-template <int NTG, int IPC, bool POOL, int MODE>
-__global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_tokens, const VideoArgs<StreamArgs> va) {
+// WV: the workgroup's waves.
+template <int NTG, int IPC, bool POOL, int MODE, int WV = kTokWaves>
+__global__ __launch_bounds__(WV * 64) void k_relevance_tok(int tile_tokens, const VideoArgs<StreamArgs> va) {
+  constexpr int kTokRowsPerThread = kTokRows * 8 / (WV * kWave);  // epilogue rows of a thread (8 threads a row)
+  static_assert(kTokRowsPerThread * WV * kWave == kTokRows * 8, "whole epilogue rows per thread");
   const StreamArgs f = va.v[blockIdx.y];
   const uint16_t* __restrict__ X = static_cast<const uint16_t*>(f.X);
   const uint16_t* __restrict__ query = static_cast<const uint16_t*>(f.query);
@@ -367,12 +372,12 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   // per-wave chunk buffers (16-byte units swizzled by row): rows 0 .. 63 of a
   // wave's region stage its tile rows, rows 64 .. 64 + NQ - 1 its query rows;
   // after the loop the region holds the wave's partial S [64 rows][NQ] floats
-  __shared__ __align__(16) u32x4 s_xq[kTokWaves][kTokRows + NQ][8];
+  __shared__ __align__(16) u32x4 s_xq[WV][kTokRows + NQ][8];
   __shared__ __align__(16) float s_pool[POOL ? kTokPoolMax : 4];
-  __shared__ float s_xx[kTokWaves][kTokRows];
-  __shared__ float s_qq[kTokWaves][NQ];
+  __shared__ float s_xx[WV][kTokRows];
+  __shared__ float s_qq[WV][NQ];
   __shared__ float s_rq[NQ];
-  __shared__ float s_sig[kTokWaves][NQ];  // per-wave column sums of S
+  __shared__ float s_sig[WV][NQ];  // per-wave column sums of S
 
   int t, tile, sl;
   unit_of_block(blockIdx.x, f.tiles, 1, t, tile, sl);
@@ -389,7 +394,9 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   const __amdgpu_buffer_rsrc_t xres = make_rsrc_uniform(X + (size_t(t) * N + tok0) * C, uint32_t(TM) * C * 2);
   constexpr bool GR = MODE == kTokGroups;
   const int npass = MODE == kTokPasses ? (Q + NQ - 1) / NQ : 1;
-  float best_all = -INFINITY;
+  float best_all[kTokRowsPerThread];
+#pragma unroll
+  for (int k = 0; k < kTokRowsPerThread; ++k) best_all[k] = -INFINITY;
   for (int h = 0; h < npass; ++h) {
     const int qb = h * NQ, Qh = min(NQ, Q - qb);
     const bool sums = h == 0;
@@ -498,20 +505,20 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     Slot ring[D];
 #pragma unroll
     for (int s = 0; s < D; ++s) {
-      issue(wave + s * kTokWaves, ring[s]);
+      issue(wave + s * WV, ring[s]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    for (int c0 = wave; c0 < nch; c0 += D * kTokWaves) {
+    for (int c0 = wave; c0 < nch; c0 += D * WV) {
 #pragma unroll
       for (int s = 0; s < D; ++s) {
-        const int c = c0 + s * kTokWaves;
+        const int c = c0 + s * WV;
         __builtin_amdgcn_sched_barrier(0);
         if (c < nch) {
           consume(c, ring[s]);
           pin();
           contract();
         }
-        issue(c + D * kTokWaves, ring[s]);
+        issue(c + D * WV, ring[s]);
       }
     }
 
@@ -563,7 +570,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     if (tid < Qh) {
       float v = 0.f, qv = 0.f;
 #pragma unroll
-      for (int w = 0; w < kTokWaves; ++w) {
+      for (int w = 0; w < WV; ++w) {
         v += s_sig[w][tid];
         qv += s_qq[w][tid];
       }
@@ -578,53 +585,70 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
     }
     if (tid < NQ) {
       float qv = 0.f;
-      for (int w = 0; w < kTokWaves; ++w) qv += s_qq[w][tid];
+      for (int w = 0; w < WV; ++w) qv += s_qq[w][tid];
       s_rq[tid] = qv > 0.f ? 1.0f / sqrtf(qv) : 0.f;
     }
-    // thread -> row tid / 8, columns CPT * (tid % 8) .. + CPT - 1
+    // thread -> rows tid / 8 + RS k (k < kTokRowsPerThread), columns CPT * (tid % 8) .. + CPT - 1;
+    // every row's partials are read before the first barrier (the query maxima below reuse wave 0's region)
     constexpr int CPT = NQ / 8;
-    const int row = tid >> 3, cg = (tid & 7) * CPT;
-    float sv[CPT], rq[CPT];
+    constexpr int RS = WV * kWave / 8;  // rows the threads cover at once
+    const int cg = (tid & 7) * CPT;
+    float sv[kTokRowsPerThread][CPT], x2[kTokRowsPerThread];
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) {
-      float v = 0.f;
+    for (int k = 0; k < kTokRowsPerThread; ++k) {
+      const int row = (tid >> 3) + RS * k;
 #pragma unroll
-      for (int w = 0; w < kTokWaves; ++w) v += s_part(w, row, cg + e);
-      sv[e] = v;
+      for (int e = 0; e < CPT; ++e) {
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < WV; ++w) v += s_part(w, row, cg + e);
+        sv[k][e] = v;
+      }
+      x2[k] = 0.f;
+#pragma unroll
+      for (int w = 0; w < WV; ++w) x2[k] += s_xx[w][row];
     }
-    float x2 = 0.f;
-#pragma unroll
-    for (int w = 0; w < kTokWaves; ++w) x2 += s_xx[w][row];
     lds_barrier();  // 1 / |q_j| in s_rq
+    float rq[CPT];
 #pragma unroll
     for (int e = 0; e < CPT; ++e) rq[e] = s_rq[cg + e];
     if constexpr (GR) {
-      // the row's S_nj / |q_j| into LDS (wave 0's region: every read of the
-      // partials is behind the last barrier); thread g of the row's eight takes
+      // the rows' S_nj / |q_j| into LDS (wave 0's region: every read of the
+      // partials is behind the last barrier); thread g of a row's eight takes
       // the maximum over query g's columns
       float* s_cos = reinterpret_cast<float*>(&s_xq[0][0][0]);  // [64 rows][NQ]
 #pragma unroll
-      for (int e = 0; e < CPT; ++e) s_cos[row * NQ + cg + e] = sv[e] * rq[e];
+      for (int k = 0; k < kTokRowsPerThread; ++k)
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) s_cos[((tid >> 3) + RS * k) * NQ + cg + e] = sv[k][e] * rq[e];
       lds_barrier();
       const int g = tid & 7;
-      if (g < f.groups && row < TM) {
-        float best = -INFINITY;
-        for (int j = 0; j < f.qg; ++j) best = fmaxf(best, s_cos[row * NQ + g * f.qg + j]);
-        const float xn = sqrtf(x2);
-        advance(f.tok_score, g * f.gws)[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+#pragma unroll
+      for (int k = 0; k < kTokRowsPerThread; ++k) {
+        const int row = (tid >> 3) + RS * k;
+        if (g < f.groups && row < TM) {
+          float best = -INFINITY;
+          for (int j = 0; j < f.qg; ++j) best = fmaxf(best, s_cos[row * NQ + g * f.qg + j]);
+          const float xn = sqrtf(x2[k]);
+          advance(f.tok_score, g * f.gws)[size_t(t) * N + tok0 + row] = xn > 0.f ? best / xn : 0.f;
+        }
       }
     } else {
-      float best = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < CPT; ++e)
-        if (cg + e < Qh) best = fmaxf(best, sv[e] * rq[e]);
-      best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
-      best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
-      best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
-      best_all = fmaxf(best_all, best);
-      if (h == npass - 1 && (tid & 7) == 0 && row < TM) {
-        const float xn = sqrtf(x2);
-        f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best_all / xn : 0.f;
+      for (int k = 0; k < kTokRowsPerThread; ++k) {
+        const int row = (tid >> 3) + RS * k;
+        float best = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < CPT; ++e)
+          if (cg + e < Qh) best = fmaxf(best, sv[k][e] * rq[e]);
+        best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0xB1, 0xF, 0xF, false)));
+        best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x4E, 0xF, 0xF, false)));
+        best = fmaxf(best, __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(best), 0x141, 0xF, 0xF, false)));
+        best_all[k] = fmaxf(best_all[k], best);
+        if (h == npass - 1 && (tid & 7) == 0 && row < TM) {
+          const float xn = sqrtf(x2[k]);
+          f.tok_score[size_t(t) * N + tok0 + row] = xn > 0.f ? best_all[k] / xn : 0.f;
+        }
       }
     }
     if (h + 1 < npass) lds_barrier();  // the next pass rewrites every wave's region
@@ -633,7 +657,7 @@ __global__ __launch_bounds__(kTokWaves * 64) void k_relevance_tok(int tile_token
   if (POOL) {
     const __amdgpu_buffer_rsrc_t pres =
         make_rsrc_uniform(f.pool_part + (size_t(t) * f.tiles + tile) * C, uint32_t(C) * 4);
-    for (int c4 = tid; c4 < C / 4; c4 += kTokWaves * kWave)
+    for (int c4 = tid; c4 < C / 4; c4 += WV * kWave)
       buf_store_wt_b128(reinterpret_cast<const u32x4*>(s_pool)[c4], pres, c4 * 16);
   }
 }
@@ -1031,15 +1055,37 @@ void launch_mfma(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipS
 
 template <int NTG, int IPC, int MODE>
 void launch_tok_mode(const RelPlan& pl, const VideoArgs<StreamArgs>& va, int V, hipStream_t s) {
+  const int C = va.v[0].C;
+  // Four waves for a query of 17 to 32 tokens in one pass with the channel
+  // sums in LDS (measured faster than eight).  A pass shared by queries of
+  // that size (64 query columns) takes four waves too: a wave's chunks set
+  // the order in which each query's sums are added, so that each query's
+  // results are bitwise those of its own pass.
+  const bool four = MODE == kTokGroups ? (va.v[0].qg + 15) / 16 == 2 && C <= kTokPoolMax
+                                       : NTG == 2 && MODE == kTokOne && C <= kTokPoolMax;
   // with 64 query columns the staging regions leave no room for the gathered channel sums
   if constexpr (NTG <= 2) {
-    if (va.v[0].C <= kTokPoolMax) {
-      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true, MODE>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+    if (C <= kTokPoolMax) {
+      if constexpr (NTG == 2 && MODE == kTokOne) {
+        if (four) {
+          hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true, MODE, 4>), dim3(pl.grid, V), dim3(4 * kWave), 0, s,
+                             pl.tile_tokens, va);
+          return;
+        }
+      }
+      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, true, MODE>), dim3(pl.grid, V), dim3(kTokWaves * kWave), 0, s,
                          pl.tile_tokens, va);
       return;
     }
   }
-  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false, MODE>), dim3(pl.grid, V), dim3(pl.threads), 0, s,
+  if constexpr (NTG == 4 && MODE == kTokGroups) {
+    if (four) {
+      hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false, MODE, 4>), dim3(pl.grid, V), dim3(4 * kWave), 0, s,
+                         pl.tile_tokens, va);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((k_relevance_tok<NTG, IPC, false, MODE>), dim3(pl.grid, V), dim3(kTokWaves * kWave), 0, s,
                      pl.tile_tokens, va);
 }
 template <int NTG, int IPC>
