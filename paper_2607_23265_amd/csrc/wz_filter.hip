@@ -635,18 +635,21 @@ __host__ __device__ inline int rc_slice_width(int C, int S) {
   return ((C + S - 1) / S + kRcWaveCh - 1) / kRcWaveCh * kRcWaveCh;
 }
 
-// Workgroup (frame t, channel slice), 4 waves of 128 channels each, no LDS
-// and no barriers: sweeps of up to 16 RT rows, whose accumulators stay in
-// registers while the wave streams the frame's slice and the rows' operator
-// entries once.  C[rows][channels] += L[rows][tokens] X[tokens][channels]
-// with v_mfma_f32_16x16x32_bf16, 8 MFMAs per 16-row tile and 32-token step
-// (each twice: the rows' bf16 high and low parts).  Lane (r16, g) =
+// Workgroup (frame t, channel slice), 4 waves of 128 channels each: sweeps
+// of up to 16 RT rows, whose accumulators stay in registers while each wave
+// streams its 128 channels of the frame once.  The sweep's operator entries
+// (the same for every wave) are staged once per workgroup through LDS in
+// 128-token blocks, double-buffered: the next block's entries load while the
+// block is contracted, one LDS barrier a block; a wave without channels only
+// stages.  C[rows][channels] += L[rows][tokens] X[tokens][channels] with
+// v_mfma_f32_16x16x32_bf16, 8 MFMAs per 16-row tile and 32-token step (each
+// twice: the rows' bf16 high and low parts).  Lane (r16, g) =
 // (lane % 16, lane / 16) loads tokens 8g .. 8g+7 of a step for its channels
 // 8 r16 .. 8 r16+7 (16 bytes a token); the B operand of MFMA c' (8 K values
 // of column r16) is channel 8 r16 + c' of those tokens, formed by byte
 // permutes just before its MFMAs, so that the columns of MFMA c' are
 // channels 8 r16 + c'.  The A operand (row 16i + r16, tokens 8g .. 8g+7) is
-// one 16-byte load per part.  Lane (r16, g) ends with rows 4g .. 4g+3 of
+// one 16-byte LDS read per part.  Lane (r16, g) ends with rows 4g .. 4g+3 of
 // each tile for its 8 consecutive channels.
 template <typename Out, int RT>
 __global__ __launch_bounds__(kRcWaves * kWave) __attribute__((amdgpu_waves_per_eu(2))) void k_filter_contract(const VideoArgs<RowsArgs> va) {
@@ -663,45 +666,67 @@ __global__ __launch_bounds__(kRcWaves * kWave) __attribute__((amdgpu_waves_per_e
   const int nrow = int(max(0LL, min((long long)nt, total - base)));
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c_lo = sl * rc_slice_width(C, S) + wave * kRcWaveCh;
-  if (nrow == 0 || wave * kRcWaveCh >= rc_slice_width(C, S) || c_lo >= C) return;  // whole wave
+  if (nrow == 0) return;  // whole workgroup
+  // waves without channels stage operator entries and keep the barriers only
+  const bool live = !(wave * kRcWaveCh >= rc_slice_width(C, S) || c_lo >= C);
+  const int tid = threadIdx.x;
   const int r16 = lane & 15, g = lane >> 4;
   const int cw = c_lo + 8 * r16;  // the lane's first channel
   const int rb = C * 2;
   const __amdgpu_buffer_rsrc_t xres =
       make_rsrc(static_cast<const uint16_t*>(f.X) + size_t(t) * N * C, uint32_t(N) * rb);
-  // the frame's rows, 4 NP bytes each; tokens past the frame and rows past
-  // nrow fall beyond a descriptor and load zeros (lanes past C start at kOOB;
-  // offsets stay below 2^31)
   const __amdgpu_buffer_rsrc_t lres = make_rsrc(f.rows + size_t(base) * 2 * NP, uint32_t(nrow) * 4 * NP);
-  const int vx = 8 * g * rb + (cw < C ? cw * 2 : kOOB);
-  // a sweep of NT row tiles from row c0 (the last sweep may have fewer
-  // tiles: each count is its own code, without per-tile tests)
+  const int vx = 8 * g * rb + (live && cw < C ? cw * 2 : kOOB);
+  // staged operator entries: per buffer RT tiles x 2 parts x 16 rows of kBlk
+  // tokens, each row kRowB bytes (16 more than its entries, so that the 16
+  // rows read at once fall in distinct banks)
+  constexpr int kBlk = 128;
+  constexpr int kRowB = kBlk * 2 + 16;
+  __shared__ __align__(16) char s_a[2][RT * 2 * 16 * kRowB];
   auto sweep = [&](auto tiles, int c0) __attribute__((always_inline)) {
     constexpr int NT = decltype(tiles)::value;
-    const int va0 = (c0 + r16) * 4 * NP + 16 * g;  // row c0 + r16, high part, tokens 8g ..
+    constexpr int UPT = NT * 2 * 16 * 16 / (kRcWaves * kWave);  // 16-byte units a thread stages per block
+    static_assert(UPT * kRcWaves * kWave == NT * 2 * 16 * 16, "whole units per thread");
     f32x4 acc[NT][8];
 #pragma unroll
     for (int i = 0; i < NT; ++i)
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // a step's X block and operator entries; each load's uniform part as one
-    // scalar, so that the compiler adds it to the lane's base instead of
-    // holding a base per load
-    auto load = [&](int k0, u32x4 (&x)[8], u32x4 (&ah)[NT], u32x4 (&al)[NT]) __attribute__((always_inline)) {
+    auto loadx = [&](int k0, u32x4 (&x)[8]) __attribute__((always_inline)) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         x[e] = __builtin_amdgcn_raw_buffer_load_b128(xres, vx + __builtin_amdgcn_readfirstlane((k0 + e) * rb), 0, 0);
+    };
+    // unit q of a block: token group q % 16, row (q / 16) % 16, part (q / 256) % 2, tile q / 512
+    // half hf of a block's units (UPT / 2 a thread)
+    auto stage_load = [&](int blk, int hf, u32x4 (&u)[UPT / 2]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < NT; ++i) {
-        const int su = __builtin_amdgcn_readfirstlane(i * 64 * NP + 2 * k0);
-        ah[i] = __builtin_amdgcn_raw_buffer_load_b128(lres, va0 + su, 0, 0);
-        al[i] = __builtin_amdgcn_raw_buffer_load_b128(lres, va0 + su + 2 * NP, 0, 0);
+      for (int k2 = 0; k2 < UPT / 2; ++k2) {
+        const int k = hf * (UPT / 2) + k2;
+        const int q = tid + k * kRcWaves * kWave;
+        const int uu = q & 15, r = (q >> 4) & 15, p = (q >> 8) & 1, i = q >> 9;
+        const int tok = blk * kBlk + 8 * uu;
+        const int off = (c0 + 16 * i + r) * 4 * NP + p * 2 * NP + 2 * tok;
+        u[k2] = __builtin_amdgcn_raw_buffer_load_b128(lres, tok < NP ? off : kOOB, 0, 0);
       }
     };
-    // per channel c', its B operand, then the MFMAs of every tile, the high
-    // parts first, so that the two products into one accumulator are NT
-    // MFMAs apart
-    auto step = [&](const u32x4 (&x)[8], const u32x4 (&ah)[NT], const u32x4 (&al)[NT]) __attribute__((always_inline)) {
+    auto stage_store = [&](int buf, int hf, const u32x4 (&u)[UPT / 2]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int k2 = 0; k2 < UPT / 2; ++k2) {
+        const int k = hf * (UPT / 2) + k2;
+        const int q = tid + k * kRcWaves * kWave;
+        const int uu = q & 15, r = (q >> 4) & 15, p = (q >> 8) & 1, i = q >> 9;
+        *reinterpret_cast<u32x4*>(&s_a[buf][((i * 2 + p) * 16 + r) * kRowB + uu * 16]) = u[k2];
+      }
+    };
+    // one 32-token step at token kk of buffer buf's block
+    auto step = [&](const u32x4 (&x)[8], int buf, int kk) __attribute__((always_inline)) {
+      u32x4 ah[NT], al[NT];
+#pragma unroll
+      for (int i = 0; i < NT; ++i) {
+        ah[i] = *reinterpret_cast<const u32x4*>(&s_a[buf][((i * 2 + 0) * 16 + r16) * kRowB + (kk + 8 * g) * 2]);
+        al[i] = *reinterpret_cast<const u32x4*>(&s_a[buf][((i * 2 + 1) * 16 + r16) * kRowB + (kk + 8 * g) * 2]);
+      }
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         u32x4 wc;
@@ -717,20 +742,41 @@ __global__ __launch_bounds__(kRcWaves * kWave) __attribute__((amdgpu_waves_per_e
           acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, al[i]), bw, acc[i][c], 0, 0, 0);
       }
     };
-    // a two-slot ring of steps, issued in slot order and reloaded in place
-    // (a register copy of a slot still loading would wait for the load)
-    u32x4 xa[8], xb[8], aha[NT], ala[NT], ahb[NT], alb[NT];
-    load(0, xa, aha, ala);
-    __builtin_amdgcn_sched_barrier(0);
-    load(32, xb, ahb, alb);
-    for (int k0 = 0; k0 < NP; k0 += 64) {
+    const int nblk = (NP + kBlk - 1) / kBlk;
+    u32x4 xa[8], xb[8], su[UPT / 2];
+    if (live) {
+      loadx(0, xa);
       __builtin_amdgcn_sched_barrier(0);
-      step(xa, aha, ala);
-      load(k0 + 64, xa, aha, ala);
-      __builtin_amdgcn_sched_barrier(0);
-      if (k0 + 32 < NP) step(xb, ahb, alb);
-      load(k0 + 96, xb, ahb, alb);
+      loadx(32, xb);
     }
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      stage_load(0, hf, su);
+      stage_store(0, hf, su);
+    }
+    lds_barrier();
+    // block blk from buffer blk % 2 while the next block is staged into the
+    // other, half of it in each half of the block's steps; one barrier a block
+    for (int blk = 0; blk < nblk; ++blk) {
+      const int buf = blk & 1;
+      const bool next = blk + 1 < nblk;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        if (next) stage_load(blk + 1, hf, su);
+        const int k0 = blk * kBlk + 64 * hf;
+        if (live && k0 < NP) {
+          __builtin_amdgcn_sched_barrier(0);
+          step(xa, buf, 64 * hf);
+          loadx(k0 + 64, xa);
+          __builtin_amdgcn_sched_barrier(0);
+          if (k0 + 32 < NP) step(xb, buf, 64 * hf + 32);
+          loadx(k0 + 96, xb);
+        }
+        if (next) stage_store(buf ^ 1, hf, su);
+      }
+      lds_barrier();
+    }
+    if (!live) return;
 #pragma unroll
     for (int i = 0; i < NT; ++i) {
       // one descriptor per 16-row tile (the lanes' rows differ); its size
