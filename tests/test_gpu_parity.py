@@ -258,6 +258,12 @@ EDGE = {
     "query_128_passes": dict(T=5, H=9, W=9, C=136, Q=128, B=60),
     "query_256_passes": dict(T=3, H=8, W=8, C=72, Q=256, B=30),
     "query_100_large_c": dict(T=2, H=7, W=7, C=16384, Q=100, B=20),
+    # 17 to 32 query tokens (four-wave workgroups when the channel sums fit
+    # LDS): one 64-channel chunk (three waves without a chunk), the largest
+    # channel count whose sums fit, and one past it (eight waves)
+    "query_20_one_chunk": dict(T=3, H=5, W=5, C=40, Q=20, B=20),
+    "query_32_c8192": dict(T=2, H=7, W=7, C=8192, Q=32, B=20),
+    "query_32_c8200": dict(T=2, H=7, W=7, C=8200, Q=32, B=20),
 }
 
 
