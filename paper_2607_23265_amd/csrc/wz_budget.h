@@ -556,7 +556,7 @@ __device__ __forceinline__ void budget_wave_compute_det(double d, double r, int 
       const int top = (any ^ all) ? 63 - __clzll(any ^ all) : -1;
       uint64_t cand = active, chosen = 0;
       for (int bit = top; bit >= 0 && need > 0; --bit) {
-        if (__popcll(cand) <= need) break;
+        if (int(__popcll(cand)) <= need) break;
         const uint64_t ones = cand & __ballot((fb >> bit) & 1ull);
         const int c1 = __popcll(ones);
         if (c1 <= need) {
@@ -898,9 +898,9 @@ __device__ void budget_wave_slots(const float* __restrict__ rel, const float* __
 }
 
 // Lane t loads r_t and delta_t, then the wave computes the budgets.
-__device__ void budget_wave_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
-                                 long long B, int levels, float tau, int32_t* __restrict__ budget,
-                                 int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
+__device__ inline void budget_wave_body(const float* __restrict__ rel, const float* __restrict__ delta, int T, int N,
+                                        long long B, int levels, float tau, int32_t* __restrict__ budget,
+                                        int32_t* __restrict__ offset, float* __restrict__ rel_rect) {
   const int lane = threadIdx.x & 63;
   const double d = lane < T ? double(delta[lane]) : 0.0;
   const double r = lane < T ? double(rel[lane]) : 0.0;
